@@ -1,0 +1,249 @@
+/*
+ * damp.h - C ABI of libdamp: the decode-step recurrent-state update of Gated
+ * DeltaNet (GDN) and Kimi Delta Attention (KDA) over a mixed-precision state,
+ * as described in "DAMP: Decay-Aware Mixed-Precision Recurrent-State
+ * Quantization" (arXiv 2608.27513), on AMD Instinct MI355X (gfx950).
+ *
+ * Conventions shared by every call below
+ * --------------------------------------
+ *  - Pointers are DEVICE pointers unless the argument comment says "host".
+ *  - bf16 tensors are passed as uint16_t bit patterns.
+ *  - Every tensor is owned by the caller. The library never keeps a pointer
+ *    after a call returns and allocates device memory only inside
+ *    damp_select_channels (freed before it returns).
+ *  - Calls taking `stream` (a hipStream_t passed as void*, NULL = the null
+ *    stream) only enqueue work and return without synchronising, except
+ *    damp_select_channels, which synchronises `stream`.
+ *  - Arguments are validated on the host before anything is enqueued. A
+ *    failed validation returns DAMP_ERR_INVALID_ARG (or DAMP_ERR_UNSUPPORTED
+ *    for a valid layout that has no kernel) and touches no memory; the
+ *    message is available from damp_last_error() on the calling thread.
+ *    HIP launch failures return DAMP_ERR_HIP.
+ *  - State values must be finite. A row whose values span more than
+ *    ~3e38 is outside the quantizer's domain.
+ *
+ * State orientation (paper section 3.1): one head's state S has d_k rows
+ * (key channels u) and d_v columns. The read-out is o = S^T q.
+ *
+ * Packed tile (paper section 5.2 and App. A.5, Eq. (17), with the per-row
+ * low tier used here): one tile holds the state of one (layer, request slot,
+ * value head). Its rows are in the calibrated order pi: tile row r holds key
+ * channel pi[r]; rows 0..k_hi-1 are the protected channels. Bytes, in order:
+ *
+ *   DAMP_STATE_MIXED:
+ *     [hi]   k_hi x d_v bf16, row-major
+ *     [code] (d_k - k_hi) x d_v uint8 codes, row-major
+ *     [meta] (d_k - k_hi) x {s, z} fp32 (8 bytes per low-tier row)
+ *   DAMP_STATE_FP32:
+ *     d_k x d_v fp32, row-major
+ *
+ * A low-tier row x (d_v values) is stored with the asymmetric affine
+ * quantizer of Eq. (3), one (s, z) pair per row:
+ *     s = (max x - min x) / 255,  z = round(-min x / s),
+ *     c = clamp(round(x / s) + z, 0, 255),  x_hat = s * (c - z),
+ * with round = round-half-to-even. A row whose s is not a normal fp32 number
+ * (a constant row) uses s = |min x| / 255, or s = 1 if that is not normal
+ * either, so the all-zero row is stored as codes 0, s = 1, z = 0.
+ * The tile stride in a pool is the tile size rounded up to 128 bytes.
+ */
+#ifndef DAMP_H
+#define DAMP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DAMP_OK = 0,
+  DAMP_ERR_INVALID_ARG = 1, /* bad pointer, size or layout; nothing was touched */
+  DAMP_ERR_UNSUPPORTED = 2, /* valid layout with no kernel instance */
+  DAMP_ERR_HIP = 3          /* a HIP runtime call failed */
+} damp_status;
+
+typedef enum { DAMP_DT_FP32 = 0, DAMP_DT_BF16 = 1, DAMP_DT_FP16 = 2 } damp_dtype;
+
+typedef enum {
+  DAMP_STATE_FP32 = 0,  /* uncompressed state (the deployment baseline) */
+  DAMP_STATE_MIXED = 1  /* k_hi bf16 rows + uint8 rows; k_hi = 0 is uniform INT8 */
+} damp_state_kind;
+
+/* Storage layout of one head's state (section 5.1, Eq. (7); section 5.2).
+ * All fields are plain int32 so the struct has one fixed ABI. */
+typedef struct {
+  int32_t d_k;        /* key channels (rows) */
+  int32_t d_v;        /* value channels (columns) */
+  int32_t k_hi;       /* protected rows held in the high-precision tier */
+  int32_t kind;       /* damp_state_kind */
+  int32_t hi_dtype;   /* damp_dtype of the high tier (BF16 has kernels) */
+  int32_t group;      /* values per (s, z) pair along d_v; d_v = one per row */
+  int32_t meta_dtype; /* damp_dtype of s and z (FP32 has kernels) */
+  int32_t hadamard;   /* 1 = block-32 Hadamard before quantization (no kernels) */
+} damp_layout;
+
+/* Fills `out` with the default layout: BF16 high tier, one fp32 (s, z) pair
+ * per low-tier row, no Hadamard. Kernels exist for d_k == d_v in
+ * {16, 32, 64, 128}. Returns DAMP_ERR_INVALID_ARG if out is NULL,
+ * d_k or d_v is not positive, or k_hi is outside [0, d_k]. */
+damp_status damp_layout_init(damp_layout* out, int32_t d_k, int32_t d_v,
+                             int32_t k_hi, int32_t kind);
+
+/* Bytes of one packed tile (the sum of its regions, before padding).
+ * Returns 0 for an invalid layout. For d_k = d_v = 128, k_hi = 16 the default
+ * mixed layout takes 19328 bytes; the FP32 layout takes 65536. */
+size_t damp_tile_bytes(const damp_layout* layout);
+
+/* Tile stride used inside a pool: damp_tile_bytes rounded up to 128. */
+size_t damp_tile_stride(const damp_layout* layout);
+
+/* Storage cost in bits per state value including metadata, following
+ * Eq. (7): b = b_lo + (k_hi / d_k)(b_hi - b_lo), where b_lo counts the code
+ * bits plus the (s, z) bits amortised over `group` values. Returns a
+ * negative value for an invalid layout. The paper's operating point (FP16
+ * high tier, 16 of 128 rows, INT8 with FP16 (s, z) per 32 values) gives the
+ * 9.875 of Eq. (12). */
+double damp_bits_per_value(const damp_layout* layout);
+
+/* A slot-indexed state pool: tiles addressed as
+ *   base + ((layer * num_slots + slot) * num_v_heads + head) * tile_stride.
+ * Plain data; the memory at `base` belongs to the caller. */
+typedef struct {
+  damp_layout layout;
+  int32_t num_layers;
+  int32_t num_slots;
+  int32_t num_v_heads;
+  int32_t reserved;
+  void* base;          /* device memory, 256-byte aligned */
+  size_t tile_stride;  /* bytes */
+  size_t bytes;        /* bytes the pool spans */
+} damp_pool;
+
+/* Bytes a pool of this shape spans (0 if an argument is invalid). */
+size_t damp_pool_required_bytes(const damp_layout* layout, int32_t num_layers,
+                                int32_t num_slots, int32_t num_v_heads);
+
+/* Describes `bytes` of caller memory at `base` as a pool. Fails with
+ * DAMP_ERR_INVALID_ARG if base is NULL or not 256-byte aligned, a count is
+ * not positive, the layout is invalid, or `bytes` is smaller than
+ * damp_pool_required_bytes. Writes nothing to device memory. */
+damp_status damp_pool_init(damp_pool* pool, const damp_layout* layout,
+                           int32_t num_layers, int32_t num_slots,
+                           int32_t num_v_heads, void* base, size_t bytes);
+
+/* Writes the packed zero state into every head of `n` slots (for a new
+ * request). `layer` selects one layer, or -1 for all layers. `slots` is a
+ * device int32[n]; entries outside [0, num_slots) are skipped. */
+damp_status damp_pool_reset_slots(const damp_pool* pool, int32_t layer,
+                                  const int32_t* slots, int32_t n, void* stream);
+
+/* One GDN decode step for one layer (section 3.1, Eq. (1)-(2), with the
+ * state stored per section 5.2 / App. A.5), for B requests at once.
+ *
+ * For request b and value head h (key head hk = h / (HV / num_k_heads)):
+ *   a      = exp(g[b,h])                          (scalar decay, Lambda = a I)
+ *   S_bar  = a * S                                (decay first)
+ *   delta  = v[b,h] - S_bar^T k~                  (delta-rule residual)
+ *   S'     = S_bar + beta[b,h] * k~ delta^T       (Eq. (1))
+ *   o[b,h] = scale * S'^T q~                      (read-out of the updated,
+ *                                                  not yet re-quantized S')
+ * then S' is re-encoded into the tile in place (bf16 rounding for the high
+ * tier, Eq. (3) per low-tier row). k~[r] = k[b,hk,perm[h,r]] and likewise
+ * for q: operands arrive in natural channel order and are permuted inside
+ * the kernel.
+ *
+ *  pool       pool descriptor (host pointer); its layout picks the kernel.
+ *  layer      layer index in [0, num_layers).
+ *  slot_idx   int32[B]: the pool slot of each request. A slot outside
+ *             [0, num_slots) marks a padded row: its state is untouched and
+ *             its o is written as zeros. Two requests must not share a slot
+ *             in one call (their tiles would race).
+ *  B          requests (0 is a no-op).
+ *  num_k_heads HK; num_v_heads of the pool (HV) must be a multiple of it.
+ *  q, k       bf16 [B, HK, d_k], natural channel order (q already
+ *             normalised as the model wants; `scale` multiplies o).
+ *  v          bf16 [B, HV, d_v].
+ *  g          bf16 [B, HV]: log-decay (log a); a = exp(g) is taken in fp32.
+ *  beta       bf16 [B, HV]: delta-rule step size.
+ *  perm       uint8 [HV, d_k] for this layer (tile row -> key channel), or
+ *             NULL for the identity. Each row must be a permutation.
+ *  o          [B, HV, d_v] in o_dtype (DAMP_DT_FP32 or DAMP_DT_BF16).
+ */
+damp_status damp_state_update_gdn(const damp_pool* pool, int32_t layer,
+                                  const int32_t* slot_idx, int32_t B,
+                                  int32_t num_k_heads, const uint16_t* q,
+                                  const uint16_t* k, const uint16_t* v,
+                                  const uint16_t* g, const uint16_t* beta,
+                                  const uint8_t* perm, float scale, void* o,
+                                  int32_t o_dtype, void* stream);
+
+/* One KDA decode step: as damp_state_update_gdn, except that the decay is
+ * per key channel, Lambda = diag(exp(g)) (section 3.1), so
+ *   g is bf16 [B, HV, d_k] in natural channel order and row r of the tile
+ *   decays by exp(g[b,h,perm[h,r]]),
+ * and q, k are [B, num_k_heads, d_k] with num_k_heads = HV or a divisor. */
+damp_status damp_state_update_kda(const damp_pool* pool, int32_t layer,
+                                  const int32_t* slot_idx, int32_t B,
+                                  int32_t num_k_heads, const uint16_t* q,
+                                  const uint16_t* k, const uint16_t* v,
+                                  const uint16_t* g, const uint16_t* beta,
+                                  const uint8_t* perm, float scale, void* o,
+                                  int32_t o_dtype, void* stream);
+
+/* Packs natural-order fp32 states into pool tiles (the persistent
+ * representation of Eq. (17)): tile row r receives S[b,h,perm[h,r],:],
+ * stored in the tier row r belongs to.
+ *  S     fp32 [B, HV, d_k, d_v], natural channel order.
+ *  perm  uint8 [HV, d_k] or NULL (identity).
+ * Slots outside [0, num_slots) are skipped. */
+damp_status damp_state_pack(const damp_pool* pool, int32_t layer,
+                            const int32_t* slot_idx, int32_t B, const float* S,
+                            const uint8_t* perm, void* stream);
+
+/* Decodes pool tiles back to natural-order fp32 states:
+ * S_out[b,h,perm[h,r],:] = decode(tile row r). Rows of a skipped slot (outside
+ * [0, num_slots)) are written as zeros. */
+damp_status damp_state_unpack(const damp_pool* pool, int32_t layer,
+                              const int32_t* slot_idx, int32_t B,
+                              const uint8_t* perm, float* S_out, void* stream);
+
+/* Offline selection of the protected key channels of every head (section
+ * 5.1, Eq. (8)-(10); App. A.2, Eq. (14)-(15); Alg. 1 in App. A.4).
+ *
+ * For each head h and key channel u, over the N calibration samples n:
+ *   E_u   = mean_n || Q_lo(S_n[h,u,:]) - S_n[h,u,:] ||^2     (Eq. (8))
+ *           with Q_lo = the per-row quantizer above (IEEE division, no FMA),
+ *           squared errors summed in double in ascending column order and
+ *           samples summed in ascending n;
+ *   a_eff = exp(mean_n log_a[n,h(,u)])                      (geometric mean)
+ *   P_u   = 1 / max(1 - a_eff^2, tau)                       (Eq. (9))
+ *   C_u   = E_u * P_u, and the k_hi largest C_u are kept    (Eq. (10)),
+ *           ties broken towards the lower channel index.
+ * perm_out[h] is the stable partition of Alg. 1: the kept channels in
+ * ascending order, then the rest in ascending order.
+ *
+ *  is_kda     0: log_decay is [N, H] (one decay per head, GDN);
+ *             1: log_decay is [N, H, d_k] (per key channel, KDA).
+ *  states     fp32 [N, H, d_k, d_v] device: reference (FP32) states.
+ *  log_decay  fp32 device, see is_kda.
+ *  k_hi       in [0, d_k]; tau > 0 (the paper uses 1e-4).
+ *  sel_out    host int32 [H, k_hi], ascending per head.
+ *  perm_out   host uint8 [H, d_k] (d_k <= 256).
+ *  score_out  host double [H, d_k] receiving C_u, or NULL.
+ * Allocates and frees device scratch; synchronises `stream`. */
+damp_status damp_select_channels(int32_t is_kda, int32_t N, int32_t H,
+                                 int32_t d_k, int32_t d_v, const float* states,
+                                 const float* log_decay, int32_t k_hi,
+                                 double tau, int32_t* sel_out,
+                                 uint8_t* perm_out, double* score_out,
+                                 void* stream);
+
+/* Message describing the last failure on the calling thread ("" if none). */
+const char* damp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DAMP_H */

@@ -1,0 +1,408 @@
+/*
+ * damp_oracle.c - plain, slow CPU oracle of DAMP's decode-step state update
+ * (arXiv 2608.27513). TEST INFRASTRUCTURE ONLY: it exists so that tests, the
+ * smoke check and the benchmark's CPU baseline can check and time the HIP
+ * library. It shares no code, header, table or helper with the HIP library
+ * and the product path never calls it.
+ *
+ * Arithmetic precision. The paper's fused executor evaluates the recurrence
+ * in FP32 and quantizes the FP32 result before it is stored (section 3.2;
+ * App. A.5, "Fused decode executor"), so this oracle computes in fp32, with
+ * every sum taken in ascending index order, no contraction into FMA
+ * (built with -ffp-contract=off) and libm's expf. Channel selection follows
+ * App. A.2 in double on the host. An independent fp64 brute force of the
+ * recurrence lives in brute.py and pins this file.
+ *
+ * Readings taken where the paper is silent (each is listed in the design doc):
+ *  - round() in Eq. (3) is round-half-to-even (rintf), for z and for codes;
+ *    codes saturate to [0, 255] (App. A.1); z is not clamped.
+ *  - A row whose scale s is not a normal fp32 number (a constant row) uses
+ *    s = |min| / 255, or s = 1 if that is not normal either.
+ *  - o is read from the updated FP32 state before it is re-quantized.
+ *  - One (s, z) pair per low-tier row (the quantizer group is the whole row),
+ *    stored as fp32; the high tier is bf16 with round-to-nearest-even.
+ *  - GDN's per-head decay is applied as the same a for every row, so KDA with
+ *    a channel-constant g reproduces GDN exactly.
+ */
+#include <float.h>
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_KIND_FP32 0
+#define ORC_KIND_MIXED 1
+
+/* ---------------------------------------------------------------- formats */
+
+static float orc_from_bf16(uint16_t h) {
+  uint32_t bits = ((uint32_t)h) << 16;
+  float f;
+  memcpy(&f, &bits, sizeof f);
+  return f;
+}
+
+/* fp32 -> bf16 with round-to-nearest, ties to even (finite inputs). */
+static uint16_t orc_to_bf16(float f) {
+  uint32_t bits;
+  memcpy(&bits, &f, sizeof bits);
+  if ((bits & 0x7f800000u) == 0x7f800000u) /* inf / nan: truncate, keep quiet */
+    return (uint16_t)((bits >> 16) | ((bits & 0xffffu) ? 0x40u : 0u));
+  uint32_t lsb = (bits >> 16) & 1u;
+  bits += 0x7fffu + lsb;
+  return (uint16_t)(bits >> 16);
+}
+
+void orc_bf16_round(const float* x, uint16_t* out, int64_t n) {
+  for (int64_t i = 0; i < n; ++i) out[i] = orc_to_bf16(x[i]);
+}
+
+void orc_bf16_widen(const uint16_t* x, float* out, int64_t n) {
+  for (int64_t i = 0; i < n; ++i) out[i] = orc_from_bf16(x[i]);
+}
+
+/* ------------------------------------------------- Eq. (3): one-row INT8 */
+
+/* Scale and zero point of a row (Eq. (3) with b = 8). */
+void orc_quant_params(const float* x, int n, float* s_out, float* z_out) {
+  float lo = x[0], hi = x[0];
+  for (int j = 1; j < n; ++j) {
+    if (x[j] < lo) lo = x[j];
+    if (x[j] > hi) hi = x[j];
+  }
+  float s = (hi - lo) / 255.0f;
+  if (!(s >= FLT_MIN)) {           /* constant row */
+    s = fabsf(lo) / 255.0f;
+    if (!(s >= FLT_MIN)) s = 1.0f; /* zero row */
+  }
+  *s_out = s;
+  *z_out = rintf(-lo / s);
+}
+
+/* One code: round(x / s) + z, saturated to the unsigned 8-bit range. */
+static uint8_t orc_code(float x, float s, float z) {
+  float c = rintf(x / s) + z;
+  if (c < 0.0f) c = 0.0f;
+  if (c > 255.0f) c = 255.0f;
+  return (uint8_t)c;
+}
+
+/* Reconstruction Q(x) = s * (c - z). */
+static float orc_decode(uint8_t c, float s, float z) { return s * ((float)c - z); }
+
+void orc_quant_row(const float* x, int n, uint8_t* codes, float* s, float* z) {
+  orc_quant_params(x, n, s, z);
+  for (int j = 0; j < n; ++j) codes[j] = orc_code(x[j], *s, *z);
+}
+
+void orc_dequant_row(const uint8_t* codes, int n, float s, float z, float* out) {
+  for (int j = 0; j < n; ++j) out[j] = orc_decode(codes[j], s, z);
+}
+
+/* ------------------------------------------------------- layout (Eq. 17) */
+
+/* Bytes of one tile: high tier, codes, then per-row (s, z) metadata. */
+int64_t orc_tile_bytes(int kind, int dk, int dv, int k_hi) {
+  if (kind == ORC_KIND_FP32) return (int64_t)dk * dv * 4;
+  return (int64_t)k_hi * dv * 2 + (int64_t)(dk - k_hi) * dv + (int64_t)(dk - k_hi) * 8;
+}
+
+/* Storage bits per value of a mixed layout, general form of Eq. (7): the low
+ * tier costs its code bits plus two metadata words per `group` values. */
+double orc_bits_per_value(int dk, int k_hi, int hi_bits, int code_bits, int group,
+                          int meta_bits) {
+  double b_lo = (double)code_bits + 2.0 * (double)meta_bits / (double)group;
+  double b_hi = (double)hi_bits;
+  return b_lo + ((double)k_hi / (double)dk) * (b_hi - b_lo);
+}
+
+/* Decode tile rows (in tile order) into S[dk][dv]. */
+static void orc_tile_decode(int kind, int dk, int dv, int k_hi, const uint8_t* tile,
+                            float* S) {
+  if (kind == ORC_KIND_FP32) {
+    memcpy(S, tile, (size_t)dk * dv * sizeof(float));
+    return;
+  }
+  const uint8_t* hi = tile;
+  const uint8_t* codes = tile + (size_t)k_hi * dv * 2;
+  const uint8_t* meta = codes + (size_t)(dk - k_hi) * dv;
+  for (int r = 0; r < dk; ++r) {
+    if (r < k_hi) {
+      for (int j = 0; j < dv; ++j) {
+        uint16_t h;
+        memcpy(&h, hi + ((size_t)r * dv + j) * 2, 2);
+        S[(size_t)r * dv + j] = orc_from_bf16(h);
+      }
+    } else {
+      int l = r - k_hi;
+      float sz[2];
+      memcpy(sz, meta + (size_t)l * 8, 8);
+      orc_dequant_row(codes + (size_t)l * dv, dv, sz[0], sz[1], S + (size_t)r * dv);
+    }
+  }
+}
+
+/* Encode S[dk][dv] (tile order) into the tile. */
+static void orc_tile_encode(int kind, int dk, int dv, int k_hi, const float* S,
+                            uint8_t* tile) {
+  if (kind == ORC_KIND_FP32) {
+    memcpy(tile, S, (size_t)dk * dv * sizeof(float));
+    return;
+  }
+  uint8_t* hi = tile;
+  uint8_t* codes = tile + (size_t)k_hi * dv * 2;
+  uint8_t* meta = codes + (size_t)(dk - k_hi) * dv;
+  for (int r = 0; r < dk; ++r) {
+    if (r < k_hi) {
+      for (int j = 0; j < dv; ++j) {
+        uint16_t h = orc_to_bf16(S[(size_t)r * dv + j]);
+        memcpy(hi + ((size_t)r * dv + j) * 2, &h, 2);
+      }
+    } else {
+      int l = r - k_hi;
+      float sz[2];
+      orc_quant_row(S + (size_t)r * dv, dv, codes + (size_t)l * dv, &sz[0], &sz[1]);
+      memcpy(meta + (size_t)l * 8, sz, 8);
+    }
+  }
+}
+
+static int orc_perm_at(const uint8_t* perm, int h, int dk, int r) {
+  return perm ? (int)perm[(size_t)h * dk + r] : r;
+}
+
+/* ---------------------------------------------------------- pack / unpack */
+
+/* Pool addressing: tile of (slot, head) at pool + slot*slot_stride +
+ * head*tile_stride (pool already offset to the layer). */
+void orc_pack(int kind, int dk, int dv, int k_hi, uint8_t* pool, int64_t slot_stride,
+              int64_t tile_stride, int num_slots, const int32_t* slot_idx, int B, int HV,
+              const float* S, const uint8_t* perm) {
+  int64_t ntiles = (int64_t)B * HV;
+#pragma omp parallel for schedule(static)
+  for (int64_t t = 0; t < ntiles; ++t) {
+    int b = (int)(t / HV), h = (int)(t % HV);
+    int slot = slot_idx[b];
+    if (slot < 0 || slot >= num_slots) continue;
+    float* W = (float*)malloc((size_t)dk * dv * sizeof(float));
+    const float* src = S + (size_t)t * dk * dv;
+    for (int r = 0; r < dk; ++r)
+      memcpy(W + (size_t)r * dv, src + (size_t)orc_perm_at(perm, h, dk, r) * dv,
+             (size_t)dv * sizeof(float));
+    orc_tile_encode(kind, dk, dv, k_hi, W,
+                    pool + (size_t)slot * slot_stride + (size_t)h * tile_stride);
+    free(W);
+  }
+}
+
+void orc_unpack(int kind, int dk, int dv, int k_hi, const uint8_t* pool,
+                int64_t slot_stride, int64_t tile_stride, int num_slots,
+                const int32_t* slot_idx, int B, int HV, const uint8_t* perm, float* S) {
+  int64_t ntiles = (int64_t)B * HV;
+#pragma omp parallel for schedule(static)
+  for (int64_t t = 0; t < ntiles; ++t) {
+    int b = (int)(t / HV), h = (int)(t % HV);
+    int slot = slot_idx[b];
+    float* dst = S + (size_t)t * dk * dv;
+    if (slot < 0 || slot >= num_slots) {
+      memset(dst, 0, (size_t)dk * dv * sizeof(float));
+      continue;
+    }
+    float* W = (float*)malloc((size_t)dk * dv * sizeof(float));
+    orc_tile_decode(kind, dk, dv, k_hi,
+                    pool + (size_t)slot * slot_stride + (size_t)h * tile_stride, W);
+    for (int r = 0; r < dk; ++r)
+      memcpy(dst + (size_t)orc_perm_at(perm, h, dk, r) * dv, W + (size_t)r * dv,
+             (size_t)dv * sizeof(float));
+    free(W);
+  }
+}
+
+/* ------------------------------------------------- decode-step update */
+
+/*
+ * One decode step of one layer for B requests (section 3.1, Eq. (1)):
+ *   S_bar = Lambda S;  delta = v - S_bar^T k;  S = S_bar + beta k delta^T;
+ *   o = scale * S^T q,  then S is stored per its tier (section 3.2).
+ * GDN (is_kda = 0): Lambda = exp(g[b,h]) I. KDA: Lambda = diag(exp(g[b,h,:])).
+ * All operands arrive in natural channel order; row r of a tile holds key
+ * channel perm[h][r], so k, q and g are read through the permutation
+ * (section 5.2). q, k, v, g, beta are bf16 bit patterns. o is fp32.
+ * If pre_out is not NULL it receives the updated state before re-encoding,
+ * [B, HV, dk, dv] in tile-row order (used for the error analysis of Eq. (5)).
+ */
+void orc_update(int is_kda, int kind, int dk, int dv, int k_hi, uint8_t* pool,
+                int64_t slot_stride, int64_t tile_stride, int num_slots,
+                const int32_t* slot_idx, int B, int HK, int HV, const uint16_t* q,
+                const uint16_t* k, const uint16_t* v, const uint16_t* g,
+                const uint16_t* beta, const uint8_t* perm, float scale, float* o,
+                float* pre_out) {
+  int64_t ntiles = (int64_t)B * HV;
+  int group = HV / HK;
+#pragma omp parallel for schedule(dynamic, 4)
+  for (int64_t t = 0; t < ntiles; ++t) {
+    int b = (int)(t / HV), h = (int)(t % HV);
+    int hk = h / group;
+    float* ob = o + (size_t)t * dv;
+    int slot = slot_idx[b];
+    if (slot < 0 || slot >= num_slots) {
+      for (int j = 0; j < dv; ++j) ob[j] = 0.0f;
+      continue;
+    }
+    uint8_t* tile = pool + (size_t)slot * slot_stride + (size_t)h * tile_stride;
+    float* S = (float*)malloc((size_t)dk * dv * sizeof(float));
+    float* kp = (float*)malloc((size_t)dk * sizeof(float));
+    float* qp = (float*)malloc((size_t)dk * sizeof(float));
+    float* a = (float*)malloc((size_t)dk * sizeof(float));
+    float* w = (float*)malloc((size_t)dv * sizeof(float));
+    float* delta = (float*)malloc((size_t)dv * sizeof(float));
+
+    /* operands in tile-row order */
+    const uint16_t* kb = k + ((size_t)b * HK + hk) * dk;
+    const uint16_t* qb = q + ((size_t)b * HK + hk) * dk;
+    for (int r = 0; r < dk; ++r) {
+      int u = orc_perm_at(perm, h, dk, r);
+      kp[r] = orc_from_bf16(kb[u]);
+      qp[r] = orc_from_bf16(qb[u]);
+      float gu = is_kda ? orc_from_bf16(g[((size_t)b * HV + h) * dk + u])
+                        : orc_from_bf16(g[(size_t)b * HV + h]);
+      a[r] = expf(gu);
+    }
+    float bt = orc_from_bf16(beta[(size_t)b * HV + h]);
+    const uint16_t* vb = v + ((size_t)b * HV + h) * dv;
+
+    /* dequantize, then decay: S_bar = Lambda S */
+    orc_tile_decode(kind, dk, dv, k_hi, tile, S);
+    for (int r = 0; r < dk; ++r)
+      for (int j = 0; j < dv; ++j) S[(size_t)r * dv + j] = a[r] * S[(size_t)r * dv + j];
+
+    /* key read-out and residual: delta = v - S_bar^T k */
+    for (int j = 0; j < dv; ++j) {
+      float acc = 0.0f;
+      for (int r = 0; r < dk; ++r) acc = acc + kp[r] * S[(size_t)r * dv + j];
+      w[j] = acc;
+      delta[j] = orc_from_bf16(vb[j]) - w[j];
+    }
+
+    /* rank-1 delta update: S = S_bar + beta k delta^T */
+    for (int r = 0; r < dk; ++r) {
+      float bk = bt * kp[r];
+      for (int j = 0; j < dv; ++j) S[(size_t)r * dv + j] = S[(size_t)r * dv + j] + bk * delta[j];
+    }
+
+    /* read-out of the updated state: o = scale * S^T q */
+    for (int j = 0; j < dv; ++j) {
+      float acc = 0.0f;
+      for (int r = 0; r < dk; ++r) acc = acc + qp[r] * S[(size_t)r * dv + j];
+      ob[j] = scale * acc;
+    }
+
+    if (pre_out) memcpy(pre_out + (size_t)t * dk * dv, S, (size_t)dk * dv * sizeof(float));
+
+    /* store: bf16 for the high tier, Eq. (3) per low-tier row */
+    orc_tile_encode(kind, dk, dv, k_hi, S, tile);
+
+    free(S); free(kp); free(qp); free(a); free(w); free(delta);
+  }
+}
+
+/* Packed zero state for every head of the listed slots. */
+void orc_reset(int kind, int dk, int dv, int k_hi, uint8_t* pool, int64_t slot_stride,
+               int64_t tile_stride, int num_slots, const int32_t* slots, int n, int HV) {
+  float* Z = (float*)calloc((size_t)dk * dv, sizeof(float));
+  for (int i = 0; i < n; ++i) {
+    if (slots[i] < 0 || slots[i] >= num_slots) continue;
+    for (int h = 0; h < HV; ++h)
+      orc_tile_encode(kind, dk, dv, k_hi, Z,
+                      pool + (size_t)slots[i] * slot_stride + (size_t)h * tile_stride);
+  }
+  free(Z);
+}
+
+/* -------------------------------------------- offline channel selection */
+
+/* Squared reconstruction error of one row under the low-tier quantizer,
+ * summed in double in ascending column order (one term of Eq. (8)). */
+static double orc_row_error(const float* x, int n) {
+  float s, z;
+  orc_quant_params(x, n, &s, &z);
+  double acc = 0.0;
+  for (int j = 0; j < n; ++j) {
+    float xh = orc_decode(orc_code(x[j], s, z), s, z);
+    double e = (double)xh - (double)x[j];
+    acc = acc + e * e;
+  }
+  return acc;
+}
+
+typedef struct {
+  double c;
+  int u;
+} orc_ranked;
+
+static int orc_rank_cmp(const void* pa, const void* pb) {
+  const orc_ranked* a = (const orc_ranked*)pa;
+  const orc_ranked* b = (const orc_ranked*)pb;
+  if (a->c > b->c) return -1; /* larger score first */
+  if (a->c < b->c) return 1;
+  return a->u - b->u;         /* ties: lower channel first */
+}
+
+/*
+ * Alg. 1 (App. A.4) with the estimates of App. A.2, Eq. (14)-(15), on one
+ * calibration domain (so the domain-balanced mean of Eq. (13) is a plain
+ * mean over the N samples):
+ *   E_u = (1/N) sum_n ||Q_lo(S_n[u,:]) - S_n[u,:]||^2
+ *   a_eff = exp((1/N) sum_n log a_n[u]),  P_u = 1 / max(1 - a_eff^2, tau)
+ *   C_u = E_u P_u;  keep TopK_{k_hi}(C);  perm = kept ascending ++ rest ascending.
+ * states: fp32 [N, H, dk, dv]; log_decay: [N, H] (GDN) or [N, H, dk] (KDA).
+ * Outputs: sel [H, k_hi], perm [H, dk], and optionally E, P, C [H, dk].
+ */
+int orc_select(int is_kda, int N, int H, int dk, int dv, const float* states,
+               const float* log_decay, int k_hi, double tau, int32_t* sel,
+               uint8_t* perm, double* E_out, double* P_out, double* C_out) {
+  if (N <= 0 || H <= 0 || dk <= 0 || dk > 256 || dv <= 0 || k_hi < 0 || k_hi > dk)
+    return 1;
+  double* err = (double*)malloc((size_t)N * H * dk * sizeof(double));
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < (int64_t)N * H * dk; ++i)
+    err[i] = orc_row_error(states + (size_t)i * dv, dv);
+
+  orc_ranked* rk = (orc_ranked*)malloc((size_t)dk * sizeof(orc_ranked));
+  unsigned char* keep = (unsigned char*)malloc((size_t)dk);
+  for (int h = 0; h < H; ++h) {
+    for (int u = 0; u < dk; ++u) {
+      double e = 0.0, l = 0.0;
+      for (int n = 0; n < N; ++n) {
+        e = e + err[((size_t)n * H + h) * dk + u];
+        l = l + (double)(is_kda ? log_decay[((size_t)n * H + h) * dk + u]
+                                : log_decay[(size_t)n * H + h]);
+      }
+      double E = e / (double)N;
+      double a_eff = exp(l / (double)N);
+      double one_minus = 1.0 - a_eff * a_eff;
+      double P = 1.0 / (one_minus > tau ? one_minus : tau);
+      double C = E * P;
+      if (E_out) E_out[(size_t)h * dk + u] = E;
+      if (P_out) P_out[(size_t)h * dk + u] = P;
+      if (C_out) C_out[(size_t)h * dk + u] = C;
+      rk[u].c = C;
+      rk[u].u = u;
+    }
+    qsort(rk, (size_t)dk, sizeof(orc_ranked), orc_rank_cmp);
+    memset(keep, 0, (size_t)dk);
+    for (int i = 0; i < k_hi; ++i) keep[rk[i].u] = 1;
+    int p = 0, s = 0;
+    for (int u = 0; u < dk; ++u)
+      if (keep[u]) {
+        perm[(size_t)h * dk + p++] = (uint8_t)u;
+        sel[(size_t)h * k_hi + s++] = u;
+      }
+    for (int u = 0; u < dk; ++u)
+      if (!keep[u]) perm[(size_t)h * dk + p++] = (uint8_t)u;
+  }
+  free(rk);
+  free(keep);
+  free(err);
+  return 0;
+}

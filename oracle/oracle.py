@@ -1,0 +1,260 @@
+"""CPU oracle of DAMP's decode-step state update (arXiv 2608.27513).
+
+TEST INFRASTRUCTURE ONLY. Only the tests, the smoke check and the
+benchmark's CPU-baseline leg may import this module; the product path
+(``paper_2608_27513_amd``) never does, and this module imports nothing from
+it. The arithmetic lives in ``damp_oracle.c`` (plain fp32 C, see its header
+for the precision and the readings taken); this file builds it with gcc and
+marshals numpy arrays. It also keeps its own description of the packed pool
+(tile offsets, stride), written independently of the library's.
+
+Every function cites the passage it follows:
+  update      section 3.1 Eq. (1)-(2); section 3.2; App. A.5 (fused executor)
+  quant_row   section 3.2 Eq. (3); App. A.1 (integer formats)
+  pack/unpack section 5.2; App. A.5 Eq. (17)
+  select      section 5.1 Eq. (8)-(10); App. A.2 Eq. (13)-(15); Alg. 1
+  bits        section 5.1 Eq. (7); App. A.1 Eq. (12) and the format table
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "damp_oracle.c")
+LIB = os.path.join(HERE, "liboracle.so")
+
+KIND_FP32 = 0
+KIND_MIXED = 1
+
+_lib = None
+
+
+def build(force: bool = False) -> str:
+    """Compile damp_oracle.c into liboracle.so (gcc, fp32, no contraction)."""
+    if force or not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
+        tmp = LIB + ".tmp"
+        cmd = ["gcc", "-O2", "-fno-fast-math", "-ffp-contract=off", "-fopenmp", "-fPIC",
+               "-shared", "-std=c11", SRC, "-o", tmp, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, LIB)
+    return LIB
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB):
+            build()
+        L = ctypes.CDLL(LIB)
+        vp, i32, i64, f32, f64 = (ctypes.c_void_p, ctypes.c_int, ctypes.c_int64,
+                                  ctypes.c_float, ctypes.c_double)
+        L.orc_bf16_round.argtypes = [vp, vp, i64]
+        L.orc_bf16_widen.argtypes = [vp, vp, i64]
+        L.orc_quant_params.argtypes = [vp, i32, vp, vp]
+        L.orc_quant_row.argtypes = [vp, i32, vp, vp, vp]
+        L.orc_dequant_row.argtypes = [vp, i32, f32, f32, vp]
+        L.orc_tile_bytes.argtypes = [i32, i32, i32, i32]
+        L.orc_tile_bytes.restype = i64
+        L.orc_bits_per_value.argtypes = [i32, i32, i32, i32, i32, i32]
+        L.orc_bits_per_value.restype = f64
+        L.orc_pack.argtypes = [i32, i32, i32, i32, vp, i64, i64, i32, vp, i32, i32, vp, vp]
+        L.orc_unpack.argtypes = [i32, i32, i32, i32, vp, i64, i64, i32, vp, i32, i32, vp, vp]
+        L.orc_update.argtypes = [i32, i32, i32, i32, i32, vp, i64, i64, i32, vp, i32, i32, i32,
+                                 vp, vp, vp, vp, vp, vp, f32, vp, vp]
+        L.orc_reset.argtypes = [i32, i32, i32, i32, vp, i64, i64, i32, vp, i32, i32]
+        L.orc_select.argtypes = [i32, i32, i32, i32, i32, vp, vp, i32, f64, vp, vp, vp, vp, vp]
+        L.orc_select.restype = i32
+        _lib = L
+    return _lib
+
+
+# ------------------------------------------------------------------ formats
+
+def bf16_round(x) -> np.ndarray:
+    """fp32 -> bf16 bit patterns, round-to-nearest-even."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    out = np.empty(x.shape, np.uint16)
+    lib().orc_bf16_round(_p(x), _p(out), x.size)
+    return out
+
+
+def bf16_widen(u) -> np.ndarray:
+    u = np.ascontiguousarray(u, dtype=np.uint16)
+    out = np.empty(u.shape, np.float32)
+    lib().orc_bf16_widen(_p(u), _p(out), u.size)
+    return out
+
+
+def quant_row(x):
+    """Eq. (3) on one row: returns (codes uint8, s, z)."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    codes = np.empty(x.shape, np.uint8)
+    s = ctypes.c_float()
+    z = ctypes.c_float()
+    lib().orc_quant_row(_p(x), x.size, _p(codes), ctypes.byref(s), ctypes.byref(z))
+    return codes, np.float32(s.value), np.float32(z.value)
+
+
+def dequant_row(codes, s, z) -> np.ndarray:
+    codes = np.ascontiguousarray(codes, dtype=np.uint8)
+    out = np.empty(codes.shape, np.float32)
+    lib().orc_dequant_row(_p(codes), codes.size, float(s), float(z), _p(out))
+    return out
+
+
+def qdq_row(x) -> np.ndarray:
+    """Q(x) = dequant(quant(x)) for one row."""
+    c, s, z = quant_row(x)
+    return dequant_row(c, s, z)
+
+
+# ------------------------------------------------------------------- layout
+
+def tile_bytes(kind: int, dk: int, dv: int, k_hi: int) -> int:
+    return int(lib().orc_tile_bytes(kind, dk, dv, k_hi))
+
+
+def tile_stride(kind: int, dk: int, dv: int, k_hi: int) -> int:
+    tb = tile_bytes(kind, dk, dv, k_hi)
+    return (tb + 127) // 128 * 128
+
+
+def bits_per_value(dk: int, k_hi: int, hi_bits: int = 16, code_bits: int = 8,
+                   group: int = 32, meta_bits: int = 16) -> float:
+    return float(lib().orc_bits_per_value(dk, k_hi, hi_bits, code_bits, group, meta_bits))
+
+
+class Pool:
+    """Host byte image of a slot-indexed pool, laid out as the library's."""
+
+    def __init__(self, kind: int, dk: int, dv: int, k_hi: int, num_layers: int,
+                 num_slots: int, num_v_heads: int):
+        self.kind, self.dk, self.dv, self.k_hi = kind, dk, dv, k_hi
+        self.num_layers, self.num_slots, self.hv = num_layers, num_slots, num_v_heads
+        self.tile_stride = tile_stride(kind, dk, dv, k_hi)
+        self.slot_stride = self.tile_stride * num_v_heads
+        self.layer_stride = self.slot_stride * num_slots
+        self.buf = np.zeros(self.layer_stride * num_layers, np.uint8)
+
+    def layer_ptr(self, layer: int):
+        return ctypes.c_void_p(self.buf.ctypes.data + layer * self.layer_stride)
+
+    def tile(self, layer: int, slot: int, head: int) -> np.ndarray:
+        o = layer * self.layer_stride + slot * self.slot_stride + head * self.tile_stride
+        return self.buf[o:o + tile_bytes(self.kind, self.dk, self.dv, self.k_hi)]
+
+    def copy(self) -> "Pool":
+        c = Pool.__new__(Pool)
+        c.__dict__.update(self.__dict__)
+        c.buf = self.buf.copy()
+        return c
+
+
+def _i32(a):
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def pack(pool: Pool, layer: int, slot_idx, S, perm=None) -> None:
+    """Natural-order fp32 states [B, HV, dk, dv] -> tiles (Eq. (17))."""
+    slot_idx = _i32(slot_idx)
+    S = np.ascontiguousarray(S, dtype=np.float32)
+    perm = None if perm is None else np.ascontiguousarray(perm, dtype=np.uint8)
+    B = slot_idx.size
+    assert S.shape == (B, pool.hv, pool.dk, pool.dv)
+    lib().orc_pack(pool.kind, pool.dk, pool.dv, pool.k_hi, pool.layer_ptr(layer),
+                   pool.slot_stride, pool.tile_stride, pool.num_slots, _p(slot_idx), B,
+                   pool.hv, _p(S), _p(perm))
+
+
+def unpack(pool: Pool, layer: int, slot_idx, perm=None) -> np.ndarray:
+    slot_idx = _i32(slot_idx)
+    perm = None if perm is None else np.ascontiguousarray(perm, dtype=np.uint8)
+    B = slot_idx.size
+    S = np.empty((B, pool.hv, pool.dk, pool.dv), np.float32)
+    lib().orc_unpack(pool.kind, pool.dk, pool.dv, pool.k_hi, pool.layer_ptr(layer),
+                     pool.slot_stride, pool.tile_stride, pool.num_slots, _p(slot_idx), B,
+                     pool.hv, _p(perm), _p(S))
+    return S
+
+
+def reset(pool: Pool, layer: int, slots) -> None:
+    slots = _i32(slots)
+    layers = range(pool.num_layers) if layer < 0 else [layer]
+    for l in layers:
+        lib().orc_reset(pool.kind, pool.dk, pool.dv, pool.k_hi, pool.layer_ptr(l),
+                        pool.slot_stride, pool.tile_stride, pool.num_slots, _p(slots),
+                        slots.size, pool.hv)
+
+
+def update(pool: Pool, layer: int, slot_idx, *, kda: bool, q, k, v, g, beta, perm=None,
+           scale: float = 1.0, want_pre: bool = False):
+    """One decode step (Eq. (1)) on every listed slot, in place.
+
+    q, k: bf16 bits [B, HK, dk]; v: [B, HV, dv]; g: [B, HV] (GDN) or
+    [B, HV, dk] (KDA); beta: [B, HV]. Returns o fp32 [B, HV, dv] (and the
+    pre-quantization state in tile-row order if want_pre)."""
+    slot_idx = _i32(slot_idx)
+    B = slot_idx.size
+    u16 = lambda a: np.ascontiguousarray(a, dtype=np.uint16)
+    q, k, v, g, beta = u16(q), u16(k), u16(v), u16(g), u16(beta)
+    HK = q.shape[1]
+    assert q.shape == (B, HK, pool.dk) and k.shape == q.shape
+    assert v.shape == (B, pool.hv, pool.dv) and beta.shape == (B, pool.hv)
+    assert g.shape == ((B, pool.hv, pool.dk) if kda else (B, pool.hv))
+    assert pool.hv % HK == 0
+    perm = None if perm is None else np.ascontiguousarray(perm, dtype=np.uint8)
+    o = np.empty((B, pool.hv, pool.dv), np.float32)
+    pre = np.empty((B, pool.hv, pool.dk, pool.dv), np.float32) if want_pre else None
+    lib().orc_update(int(kda), pool.kind, pool.dk, pool.dv, pool.k_hi, pool.layer_ptr(layer),
+                     pool.slot_stride, pool.tile_stride, pool.num_slots, _p(slot_idx), B, HK,
+                     pool.hv, _p(q), _p(k), _p(v), _p(g), _p(beta), _p(perm), float(scale),
+                     _p(o), _p(pre))
+    return (o, pre) if want_pre else o
+
+
+def select(*, kda: bool, states, log_decay, k_hi: int, tau: float = 1e-4) -> dict:
+    """Alg. 1 with App. A.2's estimates. states fp32 [N, H, dk, dv]."""
+    states = np.ascontiguousarray(states, dtype=np.float32)
+    log_decay = np.ascontiguousarray(log_decay, dtype=np.float32)
+    N, H, dk, dv = states.shape
+    assert log_decay.shape == ((N, H, dk) if kda else (N, H))
+    sel = np.zeros((H, k_hi), np.int32)
+    perm = np.zeros((H, dk), np.uint8)
+    E = np.zeros((H, dk))
+    P = np.zeros((H, dk))
+    C = np.zeros((H, dk))
+    rc = lib().orc_select(int(kda), N, H, dk, dv, _p(states), _p(log_decay), k_hi,
+                          float(tau), _p(sel), _p(perm), _p(E), _p(P), _p(C))
+    if rc != 0:
+        raise ValueError("orc_select rejected its arguments")
+    return dict(sel=sel, perm=perm, E=E, P=P, C=C)
+
+
+def run_fp32(S0, *, kda: bool, q, k, v, g, beta, scale: float = 1.0, sample_every: int = 0):
+    """FP32-state reference trajectory (natural channel order) over T steps.
+
+    S0: fp32 [B, HV, dk, dv]; step inputs carry a leading T axis. Returns the
+    final state, the outputs [T, B, HV, dv] and, if sample_every > 0, the
+    states after steps sample_every, 2*sample_every, ... (the calibration
+    state writes of App. A.2)."""
+    T = q.shape[0]
+    B, HV, dk, dv = S0.shape
+    pool = Pool(KIND_FP32, dk, dv, 0, 1, B, HV)
+    slots = np.arange(B, dtype=np.int32)
+    pool.buf.view(np.float32)[:] = np.ascontiguousarray(S0, np.float32).reshape(-1)
+    outs, samples = [], []
+    for t in range(T):
+        outs.append(update(pool, 0, slots, kda=kda, q=q[t], k=k[t], v=v[t], g=g[t],
+                           beta=beta[t], scale=scale))
+        if sample_every and (t + 1) % sample_every == 0:
+            samples.append(pool.buf.view(np.float32).reshape(B, HV, dk, dv).copy())
+    S = pool.buf.view(np.float32).reshape(B, HV, dk, dv).copy()
+    return S, np.stack(outs), (np.stack(samples) if samples else None)
