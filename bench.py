@@ -1,0 +1,360 @@
+#!/usr/bin/env python3
+"""Benchmark of the DAMP decode-step state update on one MI355X.
+
+Workload (the headline): GDN decode, one layer, B = 256 requests, 16 key /
+32 value heads, d_k = d_v = 128, the state pre-warmed over 512 FP32 tokens
+with 8 outlier key channels per head scaled by 10, 16 protected channels per
+head chosen by the channel selection from 64 stride-8 samples; bf16 inputs
+and bf16 output. One step = one launch of the fused update over the batch.
+
+Timing: W untimed steps, then exactly K steps between two synchronisations
+(ms_per_step = wall time / K). The pool holds `--rotations` disjoint copies
+of the batch's slots and consecutive steps use different copies, so the
+state (158 MB per copy) is not served from the 256 MB last-level cache.
+A second pass records a HIP event pair around every launch on the launch
+stream; their mean is the kernel duration the roofline uses.
+
+Also reported: the FP32-state and uniform-INT8 kernels on the same workload,
+KDA decode (B = 256, 32 heads, per-channel decay, selection from a
+2048-token calibration run), and the CPU oracle timed on the host.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--quick]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+PROFILE = os.path.join(ROOT, "profiles", "update_gdn_mixed_b256_counters.txt")
+KERNEL_SOURCES = ["paper_2608_27513_amd/csrc/update.hip", "paper_2608_27513_amd/csrc/device.hpp"]
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--rotations", type=int, default=8)
+    ap.add_argument("--quick", action="store_true", help="headline only: no baselines, no CPU")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    return ap.parse_args()
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        h.update(open(os.path.join(ROOT, p), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_bytes(tile_bytes: int, B: int, HK: int, HV: int, d: int, kda: bool,
+                      o_bytes: int = 2) -> int:
+    """Bytes one launch must move: every tile read and written once, plus
+    q, k per key head, v, o per value head, the decay (per head or per
+    channel), beta, the slot ids and the permutation."""
+    state = 2 * tile_bytes * B * HV
+    qk = 2 * B * HK * d * 2
+    vo = B * HV * d * (2 + o_bytes)
+    g = B * HV * (d if kda else 1) * 2
+    beta = B * HV * 2
+    return state + qk + vo + g + beta + 4 * B + HV * d
+
+
+def profile_traffic():
+    """(fetch + write bytes per launch, scale note) from the committed counter
+    summary, or None when the kernel sources changed since it was taken."""
+    if not os.path.exists(PROFILE):
+        return None
+    kv = {}
+    for line in open(PROFILE):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+class Workload:
+    """Pools, inputs and prepared launches of one decode configuration."""
+
+    def __init__(self, torch, D, inputs, *, kda: bool, B: int, HK: int, HV: int, d: int,
+                 k_hi: int, rotations: int, seed: int, log=print):
+        self.torch, self.D, self.inputs = torch, D, inputs
+        self.kda, self.B, self.HK, self.HV, self.d, self.k_hi = kda, B, HK, HV, d, k_hi
+        self.rotations = rotations
+        dev = "cuda"
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(seed)
+        self.mu = None
+        if kda:
+            self.mu = torch.from_numpy(inputs.kda_mu(seed, HV, d)).to(dev)
+
+        # 1. FP32 warm-up of every request over 512 tokens from the zero state
+        t0 = time.time()
+        fp_layout = D.damp_layout_init(d, d, 0, D.DAMP_STATE_FP32)
+        warm = D.Pool(fp_layout, 1, B, HV)
+        slots = torch.arange(B, dtype=torch.int32, device=dev)
+        D.damp_pool_reset_slots(warm, 0, slots)
+        o = torch.empty((B, HV, d), dtype=torch.float32, device=dev)
+        samples, logs = [], []
+        for t in range(512):
+            x = inputs.decode_inputs_device(gen, B, HK, HV, d, kda=kda, mu=self.mu)
+            fn = D.damp_state_update_kda if kda else D.damp_state_update_gdn
+            fn(warm, 0, slots, x["q"], x["k"], x["v"], x["g"], x["beta"], o=o)
+            if not kda and (t + 1) % 8 == 0:  # calibration samples of request 0
+                samples.append(D.damp_state_unpack(warm, 0, slots[:1])[0])
+                logs.append(x["g"][0].float())
+        S = D.damp_state_unpack(warm, 0, slots)
+        del warm
+        # 2. outlier channels (GDN): 8 key channels per head scaled by 10
+        if not kda:
+            ch = torch.from_numpy(inputs.outlier_channels(seed, HV, d, 8)).long().to(dev)
+            rows = torch.zeros((HV, d), dtype=torch.float32, device=dev)
+            rows.scatter_(1, ch, 9.0)
+            scale = (1.0 + rows)[None, :, :, None]
+            S *= scale
+            cal = torch.stack(samples) * scale
+            cal_logs = torch.stack(logs)
+        else:
+            # separate 2048-token calibration sequence (one request), stride 8
+            cg = torch.Generator(device=dev)
+            cg.manual_seed(seed + 1)
+            cpool = D.Pool(fp_layout, 1, 1, HV)
+            one = slots[:1]
+            D.damp_pool_reset_slots(cpool, 0, one)
+            o1 = torch.empty((1, HV, d), dtype=torch.float32, device=dev)
+            cs, cl = [], []
+            for t in range(2048):
+                x = inputs.decode_inputs_device(cg, 1, HK, HV, d, kda=True, mu=self.mu)
+                D.damp_state_update_kda(cpool, 0, one, x["q"], x["k"], x["v"], x["g"], x["beta"],
+                                        o=o1)
+                if (t + 1) % 8 == 0:
+                    cs.append(D.damp_state_unpack(cpool, 0, one)[0])
+                    cl.append(x["g"][0].float())
+            cal = torch.stack(cs)
+            cal_logs = torch.stack(cl)
+        # 3. channel selection (Alg. 1) on the device-resident samples
+        _, perm, _ = D.damp_select_channels(cal.contiguous(), cal_logs.contiguous(), k_hi, kda=kda)
+        self.perm = perm.to(dev)
+        self.n_cal = cal.shape[0]
+        del cal, cal_logs
+        self.S = S
+        self.setup_s = time.time() - t0
+        log(f"  warm-up, calibration (N={self.n_cal}) and selection in {self.setup_s:.1f} s")
+
+        # per-step inputs (a few distinct sets, cycled)
+        self.step_inputs = [inputs.decode_inputs_device(gen, B, HK, HV, d, kda=kda, mu=self.mu)
+                            for _ in range(4)]
+
+    def make_pool(self, kind: int, k_hi: int, rotations: int):
+        """A pool with `rotations` disjoint slot sets, each packed with the
+        warm state (permuted by the selection)."""
+        torch, D = self.torch, self.D
+        B, HV, d = self.B, self.HV, self.d
+        layout = D.damp_layout_init(d, d, k_hi, kind)
+        pool = D.Pool(layout, 1, B * rotations, HV)
+        order = torch.from_numpy(self.inputs.slot_order(7, B * rotations, B * rotations)).cuda()
+        slot_sets = [order[r * B:(r + 1) * B].contiguous() for r in range(rotations)]
+        for s in slot_sets:
+            D.damp_state_pack(pool, 0, s, self.S, self.perm)
+        torch.cuda.synchronize()
+        return pool, slot_sets, layout
+
+    def prepared(self, pool, slot_sets, o_dtype):
+        torch, D = self.torch, self.D
+        o = torch.empty((self.B, self.HV, self.d), dtype=o_dtype, device="cuda")
+        calls = []
+        for r, s in enumerate(slot_sets):
+            for x in self.step_inputs:
+                calls.append(D.PreparedUpdate(self.kda, pool, 0, s, x["q"], x["k"], x["v"],
+                                              x["g"], x["beta"], self.perm, 1.0, o))
+        # interleave so consecutive steps use different slot sets
+        n_in = len(self.step_inputs)
+        return [calls[(i % len(slot_sets)) * n_in + (i // len(slot_sets)) % n_in]
+                for i in range(len(calls))]
+
+
+def time_steps(torch, calls, warmup: int, steps: int):
+    """Wall time of `steps` launches between two synchronisations, then the
+    mean HIP-event duration of each launch in a second pass."""
+    n = len(calls)
+    for i in range(warmup):
+        calls[i % n]()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        calls[(warmup + i) % n]()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    for i in range(steps):
+        ev[i][0].record()
+        calls[i % n]()
+        ev[i][1].record()
+    torch.cuda.synchronize()
+    durs = sorted(a.elapsed_time(b) * 1e-3 for a, b in ev)
+    return dict(wall_s=wall, mean_launch_s=sum(durs) / len(durs), median_launch_s=durs[len(durs) // 2])
+
+
+def measure(torch, D, wl: Workload, kind: int, k_hi: int, rotations: int, warmup: int,
+            steps: int, o_dtype):
+    pool, sets, layout = wl.make_pool(kind, k_hi, rotations)
+    calls = wl.prepared(pool, sets, o_dtype)
+    t = time_steps(torch, calls, warmup, steps)
+    tb = D.damp_tile_bytes(layout)
+    nbytes = algorithmic_bytes(tb, wl.B, wl.HK, wl.HV, wl.d, wl.kda,
+                               2 if o_dtype == torch.bfloat16 else 4)
+    res = dict(
+        us_per_step=1e6 * t["wall_s"] / steps,
+        kernel_us=1e6 * t["mean_launch_s"],
+        kernel_us_median=1e6 * t["median_launch_s"],
+        bytes_per_step=nbytes,
+        gbs=nbytes * steps / t["wall_s"] / 1e9,
+        kernel_gbs=nbytes / t["mean_launch_s"] / 1e9,
+        tile_bytes=tb,
+        bits_per_value=D.damp_bits_per_value(layout),
+    )
+    res["kernel_frac_peak"] = res["kernel_gbs"] / HBM_PEAK_GBS
+    del pool, calls
+    torch.cuda.empty_cache()
+    return res
+
+
+def cpu_baseline(seconds: float, log=print):
+    """The CPU oracle on config 2 (B=256, 16/32 heads, d=128, 16 BF16 rows),
+    timed on the host: as many whole decode steps as fit in `seconds`."""
+    import numpy as np
+
+    from oracle import oracle as orc
+    from paper_2608_27513_amd import inputs
+
+    B, HK, HV, d, k_hi = 256, 16, 32, 128, 16
+    S = inputs.synthetic_states(0, B, HV, d)
+    inputs.scale_channels(S, inputs.outlier_channels(0, HV, d, 8), 10.0)
+    perm = inputs.random_perms(0, HV, d)
+    ref = orc.Pool(orc.KIND_MIXED, d, d, k_hi, 1, B, HV)
+    slots = np.arange(B, dtype=np.int32)
+    orc.pack(ref, 0, slots, S, perm)
+    del S
+    inp = inputs.step(inputs.decode_inputs(0, 1, B, HK, HV, d), 0)
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        orc.update(ref, 0, slots, kda=False, perm=perm, **inp)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= seconds or n >= 1000:
+            break
+    nbytes = algorithmic_bytes(orc.tile_bytes(orc.KIND_MIXED, d, d, k_hi), B, HK, HV, d, False, 4)
+    log(f"  cpu oracle: {n} steps in {el:.1f} s")
+    return dict(value=nbytes * n / el / 1e9, unit="GB/s", cores=orc.max_threads(), kind="oracle",
+                sample=f"{n} whole decode steps of the B=256, 32-head, d=128 GDN workload "
+                       f"(fp32 o), {el:.1f} s", ms_per_step=1e3 * el / n)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the state update has no "
+              "cross-GPU step; see DESIGN.md for how it shards.", file=sys.stderr)
+        sys.exit(2)
+    log = lambda *a: print(*a, file=sys.stderr, flush=True)
+    import torch
+
+    from paper_2608_27513_amd import damp as D
+    from paper_2608_27513_amd import inputs
+
+    if not torch.cuda.is_available():
+        raise SystemExit("no GPU visible")
+    D.lib()
+    B, HK, HV, d, k_hi = 256, 16, 32, 128, 16
+    log("setting up GDN B=256 HK=16 HV=32 d=128 K_hi=16")
+    gdn = Workload(torch, D, inputs, kda=False, B=B, HK=HK, HV=HV, d=d, k_hi=k_hi,
+                   rotations=args.rotations, seed=0, log=log)
+    head = measure(torch, D, gdn, D.DAMP_STATE_MIXED, k_hi, args.rotations, args.warmup,
+                   args.steps, torch.bfloat16)
+    log(f"  mixed: {head['us_per_step']:.1f} us/step, kernel {head['kernel_us']:.1f} us, "
+        f"{head['kernel_gbs']:.0f} GB/s ({100 * head['kernel_frac_peak']:.1f}% of peak)")
+    extra = {}
+    if not args.quick:
+        rot_fp = max(2, args.rotations // 2)
+        fp = measure(torch, D, gdn, D.DAMP_STATE_FP32, 0, rot_fp, args.warmup, args.steps,
+                     torch.bfloat16)
+        log(f"  fp32 state: {fp['us_per_step']:.1f} us/step, kernel {fp['kernel_us']:.1f} us, "
+            f"{fp['kernel_gbs']:.0f} GB/s")
+        i8 = measure(torch, D, gdn, D.DAMP_STATE_MIXED, 0, args.rotations, args.warmup,
+                     args.steps, torch.bfloat16)
+        log(f"  uniform int8: {i8['us_per_step']:.1f} us/step, kernel {i8['kernel_us']:.1f} us")
+        extra["baselines_gdn"] = {"fp32_state": fp, "uniform_int8": i8,
+                                  "speedup_vs_fp32_state": fp["kernel_us"] / head["kernel_us"]}
+        del gdn
+        torch.cuda.empty_cache()
+        log("setting up KDA B=256 H=32 d=128 K_hi=16")
+        kda = Workload(torch, D, inputs, kda=True, B=B, HK=32, HV=32, d=d, k_hi=k_hi,
+                       rotations=args.rotations, seed=1, log=log)
+        km = measure(torch, D, kda, D.DAMP_STATE_MIXED, k_hi, args.rotations, args.warmup,
+                     args.steps, torch.bfloat16)
+        kf = measure(torch, D, kda, D.DAMP_STATE_FP32, 0, max(2, args.rotations // 2),
+                     args.warmup, args.steps, torch.bfloat16)
+        log(f"  kda mixed: kernel {km['kernel_us']:.1f} us ({100 * km['kernel_frac_peak']:.1f}%),"
+            f" fp32 state kernel {kf['kernel_us']:.1f} us")
+        extra["kda_b256"] = {"mixed": km, "fp32_state": kf,
+                             "speedup_vs_fp32_state": kf["kernel_us"] / km["kernel_us"]}
+        del kda
+        torch.cuda.empty_cache()
+
+    cpu = None
+    if not args.quick and not args.no_cpu:
+        cpu = cpu_baseline(args.cpu_seconds, log=log)
+
+    traffic = profile_traffic()
+    out = {
+        "metric": "mixed-precision state-update µs/step + achieved HBM GB/s (% peak), B=256",
+        "value": round(head["gbs"], 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(head["us_per_step"] / 1e3, 5),
+        "us_per_step": round(head["us_per_step"], 2),
+        "frac_of_hbm_peak": round(head["gbs"] / HBM_PEAK_GBS, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16/u8 state, f32 compute",
+        "data": "synthetic (seeded; FP32 warm-up over 512 tokens on the GPU)",
+        "config": {"workload": "GDN decode, 1 layer: B=256, 16 key / 32 value heads, "
+                               "d_k=d_v=128, 16 of 128 key channels BF16, rest INT8 rows "
+                               "with fp32 (s, z); bf16 q/k/v/g/beta in, bf16 o out",
+                   "global_batch": B, "layers": 1, "rotations": args.rotations,
+                   "bytes_per_step": head["bytes_per_step"]},
+        "roofline": {"bound": "hbm", "achieved": round(head["kernel_gbs"], 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(head["kernel_frac_peak"], 4),
+                     "traffic": traffic,
+                     "kernel_us": round(head["kernel_us"], 2)},
+        "cpu_baseline": cpu,
+        "storage": {"tile_bytes": head["tile_bytes"], "bits_per_value": head["bits_per_value"],
+                    "reduction_vs_fp32_pct": round(100 * (1 - head["bits_per_value"] / 32), 2)},
+    }
+    out.update(extra)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -56,6 +56,7 @@ def lib():
         L = ctypes.CDLL(LIB)
         vp, i32, i64, f32, f64 = (ctypes.c_void_p, ctypes.c_int, ctypes.c_int64,
                                   ctypes.c_float, ctypes.c_double)
+        L.orc_max_threads.restype = i32
         L.orc_bf16_round.argtypes = [vp, vp, i64]
         L.orc_bf16_widen.argtypes = [vp, vp, i64]
         L.orc_quant_params.argtypes = [vp, i32, vp, vp]
@@ -74,6 +75,11 @@ def lib():
         L.orc_select.restype = i32
         _lib = L
     return _lib
+
+
+def max_threads() -> int:
+    """Threads the oracle's OpenMP loops use."""
+    return int(lib().orc_max_threads())
 
 
 # ------------------------------------------------------------------ formats

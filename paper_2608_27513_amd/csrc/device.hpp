@@ -1,0 +1,197 @@
+// Device helpers of libdamp for gfx950 (CDNA4, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cfloat>
+#include <cstdint>
+
+namespace damp {
+
+constexpr int kFp32 = 0;   // DAMP_STATE_FP32
+constexpr int kMixed = 1;  // DAMP_STATE_MIXED
+
+// ------------------------------------------------------------ conversions
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) {
+  return __uint_as_float(static_cast<uint32_t>(h) << 16);
+}
+
+// Two fp32 -> packed bf16 pair, round-to-nearest-even (v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  typedef float f2 __attribute__((ext_vector_type(2)));
+  typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+  f2 v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, b2));
+}
+
+__device__ __forceinline__ uint16_t f32_to_bf16(float a) {
+  return static_cast<uint16_t>(pack_bf16x2(a, 0.0f) & 0xffffu);
+}
+
+// Byte i of w as a float (v_cvt_f32_ubyte{i}).
+template <int I>
+__device__ __forceinline__ float ubyte(uint32_t w) {
+  return static_cast<float>((w >> (8 * I)) & 0xffu);
+}
+
+// ---------------------------------------------------- lane reductions (DPP)
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xf, 0xf, true));
+}
+
+// Min and max over aligned groups of N consecutive lanes (N in 1..16).
+// quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_half_mirror, row_mirror.
+template <int N>
+__device__ __forceinline__ void group_minmax(float& mn, float& mx) {
+  if constexpr (N >= 2) {
+    mn = fminf(mn, dpp_mov<0xb1>(mn));
+    mx = fmaxf(mx, dpp_mov<0xb1>(mx));
+  }
+  if constexpr (N >= 4) {
+    mn = fminf(mn, dpp_mov<0x4e>(mn));
+    mx = fmaxf(mx, dpp_mov<0x4e>(mx));
+  }
+  if constexpr (N >= 8) {
+    mn = fminf(mn, dpp_mov<0x141>(mn));
+    mx = fmaxf(mx, dpp_mov<0x141>(mx));
+  }
+  if constexpr (N >= 16) {
+    mn = fminf(mn, dpp_mov<0x140>(mn));
+    mx = fmaxf(mx, dpp_mov<0x140>(mx));
+  }
+}
+
+// Sum over the 64 lanes of a wave (every lane receives the total).
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m, 64);
+  return x;
+}
+
+// ------------------------------------------------------------- vector I/O
+
+template <int NBYTES>
+__device__ __forceinline__ void load_words(const uint8_t* p, uint32_t* w) {
+  static_assert(NBYTES % 4 == 0, "word-sized loads only");
+  if constexpr (NBYTES % 16 == 0) {
+#pragma unroll
+    for (int k = 0; k < NBYTES / 16; ++k) {
+      const uint4 v = reinterpret_cast<const uint4*>(p)[k];
+      w[4 * k + 0] = v.x;
+      w[4 * k + 1] = v.y;
+      w[4 * k + 2] = v.z;
+      w[4 * k + 3] = v.w;
+    }
+  } else if constexpr (NBYTES == 8) {
+    const uint2 v = *reinterpret_cast<const uint2*>(p);
+    w[0] = v.x;
+    w[1] = v.y;
+  } else {
+    static_assert(NBYTES == 4, "unsupported width");
+    w[0] = *reinterpret_cast<const uint32_t*>(p);
+  }
+}
+
+template <int NBYTES>
+__device__ __forceinline__ void store_words(uint8_t* p, const uint32_t* w) {
+  static_assert(NBYTES % 4 == 0, "word-sized stores only");
+  if constexpr (NBYTES % 16 == 0) {
+#pragma unroll
+    for (int k = 0; k < NBYTES / 16; ++k)
+      reinterpret_cast<uint4*>(p)[k] = make_uint4(w[4 * k], w[4 * k + 1], w[4 * k + 2], w[4 * k + 3]);
+  } else if constexpr (NBYTES == 8) {
+    *reinterpret_cast<uint2*>(p) = make_uint2(w[0], w[1]);
+  } else {
+    static_assert(NBYTES == 4, "unsupported width");
+    *reinterpret_cast<uint32_t*>(p) = w[0];
+  }
+}
+
+// ------------------------------------------------- Eq. (3) row quantizer
+
+// Scale, zero point and reciprocal scale of a row with extrema (mn, mx):
+// s = (mx - mn) / 255 and z = round(-mn / s) (round half to even). A row
+// whose s is not a normal fp32 number uses s = |mn| / 255, else s = 1.
+// Both quotients come from a hardware reciprocal refined by one
+// residual step, which rounds like IEEE division except in rare last-bit
+// cases.
+__device__ __forceinline__ void row_qparams(float mn, float mx, float& s, float& z,
+                                            float& inv) {
+  constexpr float k255inv = 1.0f / 255.0f;
+  const float r = mx - mn;
+  float q = r * k255inv;
+  q = fmaf(fmaf(-q, 255.0f, r), k255inv, q);
+  if (!(q >= FLT_MIN)) {
+    const float a = fabsf(mn);
+    q = a * k255inv;
+    q = fmaf(fmaf(-q, 255.0f, a), k255inv, q);
+    if (!(q >= FLT_MIN)) q = 1.0f;
+  }
+  const float rc = __builtin_amdgcn_rcpf(q);
+  const float nm = -mn;
+  float zq = nm * rc;
+  zq = fmaf(fmaf(-zq, q, nm), rc, zq);
+  s = q;
+  z = rintf(zq);
+  inv = rc;
+}
+
+// Code of x: clamp(round(x / s) + z, 0, 255), computed as round(x * (1/s) + z).
+__device__ __forceinline__ float quant_code(float x, float inv, float z) {
+  return __builtin_amdgcn_fmed3f(rintf(fmaf(x, inv, z)), 0.0f, 255.0f);
+}
+
+// Four codes (already integral in [0, 255]) packed little-endian into a word.
+__device__ __forceinline__ uint32_t pack_codes4(float c0, float c1, float c2, float c3) {
+  uint32_t w = __builtin_amdgcn_cvt_pk_u8_f32(c0, 0, 0u);
+  w = __builtin_amdgcn_cvt_pk_u8_f32(c1, 1, w);
+  w = __builtin_amdgcn_cvt_pk_u8_f32(c2, 2, w);
+  return __builtin_amdgcn_cvt_pk_u8_f32(c3, 3, w);
+}
+
+// ------------------------------------------------------------- row encode
+
+// Stores one row slice of CPT values (columns col0..col0+CPT of tile row r)
+// in its tier. Lanes cg = 0..TPR-1 of a row group hold the slices of one
+// row; the (s, z) pair of a low-tier row is written by lane cg == 0. The
+// branch on r is uniform across the TPR lanes of the row.
+template <int KIND, int D, int CPT, int TPR>
+__device__ __forceinline__ void encode_row(const float* x, int r, int k_hi, int cg, int col0,
+                                           uint8_t* tile, uint8_t* codes, float2* meta) {
+  if (KIND == kFp32) {
+    uint32_t w[CPT];
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) w[j] = __float_as_uint(x[j]);
+    store_words<CPT * 4>(tile + (static_cast<size_t>(r) * D + col0) * 4, w);
+  } else if (r < k_hi) {
+    uint32_t w[CPT / 2];
+#pragma unroll
+    for (int j = 0; j < CPT / 2; ++j) w[j] = pack_bf16x2(x[2 * j], x[2 * j + 1]);
+    store_words<CPT * 2>(tile + (static_cast<size_t>(r) * D + col0) * 2, w);
+  } else {
+    float mn = x[0], mx = x[0];
+#pragma unroll
+    for (int j = 1; j < CPT; ++j) {
+      mn = fminf(mn, x[j]);
+      mx = fmaxf(mx, x[j]);
+    }
+    group_minmax<TPR>(mn, mx);
+    float s, z, inv;
+    row_qparams(mn, mx, s, z, inv);
+    uint32_t w[CPT / 4];
+#pragma unroll
+    for (int j = 0; j < CPT / 4; ++j)
+      w[j] = pack_codes4(quant_code(x[4 * j], inv, z), quant_code(x[4 * j + 1], inv, z),
+                         quant_code(x[4 * j + 2], inv, z), quant_code(x[4 * j + 3], inv, z));
+    const int l = r - k_hi;
+    store_words<CPT>(codes + static_cast<size_t>(l) * D + col0, w);
+    if (cg == 0) meta[l] = make_float2(s, z);
+  }
+}
+
+}  // namespace damp

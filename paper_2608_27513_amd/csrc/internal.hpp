@@ -1,0 +1,49 @@
+// Library-internal declarations shared by the translation units of libdamp.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "damp.h"
+
+namespace damp {
+
+// Byte geometry of one packed tile (the format is documented in damp.h).
+struct TileGeom {
+  int32_t dk, dv, k_hi, kind;
+  size_t hi_bytes;    // k_hi * dv * 2 (mixed) or dk * dv * 4 (fp32)
+  size_t code_bytes;  // (dk - k_hi) * dv
+  size_t meta_bytes;  // (dk - k_hi) * 8
+  size_t bytes;       // sum of the regions
+  size_t stride;      // bytes rounded up to 128
+};
+
+// Fills g from a layout; returns false (and records why) if the layout is
+// not one the layout math accepts.
+bool tile_geom(const damp_layout* layout, TileGeom* g);
+
+// True if the layout has kernels: BF16 high tier, one fp32 (s, z) pair per
+// row, no Hadamard, d_k == d_v in {16, 32, 64, 128}.
+bool layout_has_kernels(const damp_layout* layout);
+
+// Validates a pool descriptor (non-null, consistent strides and counts).
+damp_status check_pool(const damp_pool* pool);
+
+// Thread-local error message.
+damp_status fail(damp_status st, const char* fmt, ...);
+void clear_error();
+
+inline uint8_t* layer_base(const damp_pool* pool, int32_t layer) {
+  return static_cast<uint8_t*>(pool->base) +
+         static_cast<size_t>(layer) * static_cast<size_t>(pool->num_slots) *
+             static_cast<size_t>(pool->num_v_heads) * pool->tile_stride;
+}
+
+inline hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
+
+// Returns DAMP_ERR_HIP with a message if the last launch failed.
+damp_status check_launch(const char* what);
+
+}  // namespace damp

@@ -1,0 +1,197 @@
+// Layout arithmetic, pool descriptors and error reporting of libdamp.
+//
+// Tile format: section 5.2 and App. A.5 (Eq. (17)) of the DAMP paper, with
+// one (s, z) pair per low-tier row; storage cost: Eq. (7) and Eq. (12).
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "internal.hpp"
+
+namespace damp {
+
+namespace {
+thread_local char g_error[512] = "";
+
+int dtype_bits(int32_t dt) {
+  switch (dt) {
+    case DAMP_DT_FP32: return 32;
+    case DAMP_DT_BF16: return 16;
+    case DAMP_DT_FP16: return 16;
+    default: return -1;
+  }
+}
+}  // namespace
+
+damp_status fail(damp_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(g_error, sizeof g_error, fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+void clear_error() { g_error[0] = '\0'; }
+
+damp_status check_launch(const char* what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(DAMP_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return DAMP_OK;
+}
+
+bool tile_geom(const damp_layout* L, TileGeom* g) {
+  if (!L) {
+    fail(DAMP_ERR_INVALID_ARG, "layout is NULL");
+    return false;
+  }
+  if (L->d_k <= 0 || L->d_v <= 0 || L->d_k > 256 || L->d_v > 4096) {
+    fail(DAMP_ERR_INVALID_ARG, "d_k = %d, d_v = %d out of range (d_k <= 256)", L->d_k, L->d_v);
+    return false;
+  }
+  if (L->kind != DAMP_STATE_FP32 && L->kind != DAMP_STATE_MIXED) {
+    fail(DAMP_ERR_INVALID_ARG, "unknown state kind %d", L->kind);
+    return false;
+  }
+  g->dk = L->d_k;
+  g->dv = L->d_v;
+  g->kind = L->kind;
+  const size_t dk = static_cast<size_t>(L->d_k), dv = static_cast<size_t>(L->d_v);
+  if (L->kind == DAMP_STATE_FP32) {
+    g->k_hi = 0;
+    g->hi_bytes = dk * dv * 4;
+    g->code_bytes = g->meta_bytes = 0;
+  } else {
+    if (L->k_hi < 0 || L->k_hi > L->d_k) {
+      fail(DAMP_ERR_INVALID_ARG, "k_hi = %d outside [0, d_k = %d]", L->k_hi, L->d_k);
+      return false;
+    }
+    const int hb = dtype_bits(L->hi_dtype), mb = dtype_bits(L->meta_dtype);
+    if (hb < 0 || mb < 0) {
+      fail(DAMP_ERR_INVALID_ARG, "unknown high-tier or metadata dtype");
+      return false;
+    }
+    if (L->group <= 0 || L->d_v % L->group != 0) {
+      fail(DAMP_ERR_INVALID_ARG, "group = %d does not divide d_v = %d", L->group, L->d_v);
+      return false;
+    }
+    const size_t lo_rows = dk - static_cast<size_t>(L->k_hi);
+    g->k_hi = L->k_hi;
+    g->hi_bytes = static_cast<size_t>(L->k_hi) * dv * static_cast<size_t>(hb / 8);
+    g->code_bytes = lo_rows * dv;
+    g->meta_bytes = lo_rows * (dv / static_cast<size_t>(L->group)) * 2 *
+                    static_cast<size_t>(mb / 8);
+  }
+  g->bytes = g->hi_bytes + g->code_bytes + g->meta_bytes;
+  g->stride = (g->bytes + 127) / 128 * 128;
+  return true;
+}
+
+bool layout_has_kernels(const damp_layout* L) {
+  if (L->d_k != L->d_v) return false;
+  if (L->d_k != 16 && L->d_k != 32 && L->d_k != 64 && L->d_k != 128) return false;
+  if (L->kind == DAMP_STATE_FP32) return true;
+  return L->hi_dtype == DAMP_DT_BF16 && L->meta_dtype == DAMP_DT_FP32 && L->group == L->d_v &&
+         L->hadamard == 0;
+}
+
+damp_status check_pool(const damp_pool* pool) {
+  if (!pool) return fail(DAMP_ERR_INVALID_ARG, "pool is NULL");
+  TileGeom g;
+  if (!tile_geom(&pool->layout, &g)) return DAMP_ERR_INVALID_ARG;
+  if (!pool->base) return fail(DAMP_ERR_INVALID_ARG, "pool base is NULL");
+  if (pool->num_layers <= 0 || pool->num_slots <= 0 || pool->num_v_heads <= 0)
+    return fail(DAMP_ERR_INVALID_ARG, "pool counts must be positive");
+  if (pool->tile_stride != g.stride)
+    return fail(DAMP_ERR_INVALID_ARG, "pool tile_stride %zu != layout stride %zu",
+                pool->tile_stride, g.stride);
+  const size_t need = g.stride * static_cast<size_t>(pool->num_layers) *
+                      static_cast<size_t>(pool->num_slots) *
+                      static_cast<size_t>(pool->num_v_heads);
+  if (pool->bytes < need)
+    return fail(DAMP_ERR_INVALID_ARG, "pool spans %zu bytes, needs %zu", pool->bytes, need);
+  return DAMP_OK;
+}
+
+}  // namespace damp
+
+using namespace damp;
+
+extern "C" {
+
+const char* damp_last_error(void) { return g_error; }
+
+damp_status damp_layout_init(damp_layout* out, int32_t d_k, int32_t d_v, int32_t k_hi,
+                             int32_t kind) {
+  clear_error();
+  if (!out) return fail(DAMP_ERR_INVALID_ARG, "out is NULL");
+  damp_layout L;
+  std::memset(&L, 0, sizeof L);
+  L.d_k = d_k;
+  L.d_v = d_v;
+  L.k_hi = kind == DAMP_STATE_FP32 ? 0 : k_hi;
+  L.kind = kind;
+  L.hi_dtype = DAMP_DT_BF16;
+  L.group = d_v;
+  L.meta_dtype = DAMP_DT_FP32;
+  L.hadamard = 0;
+  TileGeom g;
+  if (!tile_geom(&L, &g)) return DAMP_ERR_INVALID_ARG;
+  *out = L;
+  return DAMP_OK;
+}
+
+size_t damp_tile_bytes(const damp_layout* layout) {
+  TileGeom g;
+  return tile_geom(layout, &g) ? g.bytes : 0;
+}
+
+size_t damp_tile_stride(const damp_layout* layout) {
+  TileGeom g;
+  return tile_geom(layout, &g) ? g.stride : 0;
+}
+
+double damp_bits_per_value(const damp_layout* layout) {
+  TileGeom g;
+  if (!tile_geom(layout, &g)) return -1.0;
+  if (layout->kind == DAMP_STATE_FP32) return 32.0;
+  // Eq. (7): b = b_lo + (k_hi / d_k) (b_hi - b_lo), with b_lo = code bits plus
+  // two metadata words per group.
+  const double meta_bits = layout->meta_dtype == DAMP_DT_FP32 ? 32.0 : 16.0;
+  const double b_lo = 8.0 + 2.0 * meta_bits / static_cast<double>(layout->group);
+  const double b_hi = layout->hi_dtype == DAMP_DT_FP32 ? 32.0 : 16.0;
+  return b_lo + (static_cast<double>(layout->k_hi) / layout->d_k) * (b_hi - b_lo);
+}
+
+size_t damp_pool_required_bytes(const damp_layout* layout, int32_t num_layers,
+                                int32_t num_slots, int32_t num_v_heads) {
+  TileGeom g;
+  if (!tile_geom(layout, &g) || num_layers <= 0 || num_slots <= 0 || num_v_heads <= 0) return 0;
+  return g.stride * static_cast<size_t>(num_layers) * static_cast<size_t>(num_slots) *
+         static_cast<size_t>(num_v_heads);
+}
+
+damp_status damp_pool_init(damp_pool* pool, const damp_layout* layout, int32_t num_layers,
+                           int32_t num_slots, int32_t num_v_heads, void* base, size_t bytes) {
+  clear_error();
+  if (!pool) return fail(DAMP_ERR_INVALID_ARG, "pool is NULL");
+  TileGeom g;
+  if (!tile_geom(layout, &g)) return DAMP_ERR_INVALID_ARG;
+  if (!base) return fail(DAMP_ERR_INVALID_ARG, "base is NULL");
+  if (reinterpret_cast<uintptr_t>(base) % 256 != 0)
+    return fail(DAMP_ERR_INVALID_ARG, "base is not 256-byte aligned");
+  const size_t need = damp_pool_required_bytes(layout, num_layers, num_slots, num_v_heads);
+  if (need == 0) return fail(DAMP_ERR_INVALID_ARG, "pool counts must be positive");
+  if (bytes < need)
+    return fail(DAMP_ERR_INVALID_ARG, "%zu bytes given, pool needs %zu", bytes, need);
+  std::memset(pool, 0, sizeof *pool);
+  pool->layout = *layout;
+  pool->num_layers = num_layers;
+  pool->num_slots = num_slots;
+  pool->num_v_heads = num_v_heads;
+  pool->base = base;
+  pool->tile_stride = g.stride;
+  pool->bytes = need;
+  return DAMP_OK;
+}
+
+}  // extern "C"

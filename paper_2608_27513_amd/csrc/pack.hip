@@ -1,0 +1,207 @@
+// Pack, unpack and reset of packed pool tiles (section 5.2 and App. A.5,
+// Eq. (17)): conversion between natural-order fp32 states and the persistent
+// mixed-precision representation. Uses the same row encoder as the update.
+#include "device.hpp"
+#include "internal.hpp"
+
+namespace damp {
+namespace {
+
+struct TileParams {
+  uint8_t* layer_base;
+  uint64_t slot_stride;
+  uint64_t tile_stride;
+  uint64_t layer_stride;
+  const int32_t* slot_idx;
+  const uint8_t* perm;
+  float* S;          // [B, HV, D, D] natural order
+  int32_t num_slots;
+  int32_t HV;
+  int32_t k_hi;
+};
+
+template <int D>
+struct Shape {
+  static constexpr int NT = D >= 32 ? 2 * D : 64;
+  static constexpr int CPT = D >= 32 ? 16 : 4;
+  static constexpr int TPR = D / CPT;
+  static constexpr int RG = NT / TPR;
+  static constexpr int RPT = D / RG;
+};
+
+template <int KIND, int D>
+__global__ __launch_bounds__(Shape<D>::NT) void pack_kernel(const TileParams p) {
+  using Sh = Shape<D>;
+  const int t = threadIdx.x, h = blockIdx.x, b = blockIdx.y;
+  const int cg = t % Sh::TPR, rg = t / Sh::TPR, col0 = cg * Sh::CPT;
+  const int slot = p.slot_idx[b];
+  if (slot < 0 || slot >= p.num_slots) return;
+  uint8_t* tile = p.layer_base + static_cast<size_t>(slot) * p.slot_stride +
+                  static_cast<size_t>(h) * p.tile_stride;
+  const int k_hi = KIND == kFp32 ? D : p.k_hi;
+  uint8_t* codes = tile + static_cast<size_t>(k_hi) * D * 2;
+  float2* meta = reinterpret_cast<float2*>(codes + static_cast<size_t>(D - k_hi) * D);
+  const float* src = p.S + (static_cast<size_t>(b) * p.HV + h) * D * D;
+#pragma unroll
+  for (int i = 0; i < Sh::RPT; ++i) {
+    const int r = rg + Sh::RG * i;
+    const int u = p.perm ? (static_cast<int>(p.perm[static_cast<size_t>(h) * D + r]) & (D - 1)) : r;
+    float x[Sh::CPT];
+    uint32_t w[Sh::CPT];
+    load_words<Sh::CPT * 4>(reinterpret_cast<const uint8_t*>(src + static_cast<size_t>(u) * D + col0), w);
+#pragma unroll
+    for (int j = 0; j < Sh::CPT; ++j) x[j] = __uint_as_float(w[j]);
+    encode_row<KIND, D, Sh::CPT, Sh::TPR>(x, r, k_hi, cg, col0, tile, codes, meta);
+  }
+}
+
+template <int KIND, int D>
+__global__ __launch_bounds__(Shape<D>::NT) void unpack_kernel(const TileParams p) {
+  using Sh = Shape<D>;
+  const int t = threadIdx.x, h = blockIdx.x, b = blockIdx.y;
+  const int cg = t % Sh::TPR, rg = t / Sh::TPR, col0 = cg * Sh::CPT;
+  const int slot = p.slot_idx[b];
+  float* dst = p.S + (static_cast<size_t>(b) * p.HV + h) * D * D;
+  const bool live = slot >= 0 && slot < p.num_slots;
+  const uint8_t* tile = p.layer_base + static_cast<size_t>(live ? slot : 0) * p.slot_stride +
+                        static_cast<size_t>(h) * p.tile_stride;
+  const int k_hi = KIND == kFp32 ? D : p.k_hi;
+  const uint8_t* codes = tile + static_cast<size_t>(k_hi) * D * 2;
+  const float2* meta = reinterpret_cast<const float2*>(codes + static_cast<size_t>(D - k_hi) * D);
+#pragma unroll
+  for (int i = 0; i < Sh::RPT; ++i) {
+    const int r = rg + Sh::RG * i;
+    const int u = p.perm ? (static_cast<int>(p.perm[static_cast<size_t>(h) * D + r]) & (D - 1)) : r;
+    uint32_t out[Sh::CPT];
+    if (!live) {
+#pragma unroll
+      for (int j = 0; j < Sh::CPT; ++j) out[j] = 0u;
+    } else if (KIND == kFp32) {
+      load_words<Sh::CPT * 4>(tile + (static_cast<size_t>(r) * D + col0) * 4, out);
+    } else if (r < k_hi) {
+      uint32_t w[Sh::CPT / 2];
+      load_words<Sh::CPT * 2>(tile + (static_cast<size_t>(r) * D + col0) * 2, w);
+#pragma unroll
+      for (int j = 0; j < Sh::CPT / 2; ++j) {
+        out[2 * j] = w[j] << 16;
+        out[2 * j + 1] = w[j] & 0xffff0000u;
+      }
+    } else {
+      uint32_t w[Sh::CPT / 4];
+      load_words<Sh::CPT>(codes + static_cast<size_t>(r - k_hi) * D + col0, w);
+      const float2 sz = meta[r - k_hi];
+      // x_hat = s * (c - z), exactly as Eq. (3) reconstructs
+#pragma unroll
+      for (int j = 0; j < Sh::CPT / 4; ++j) {
+        out[4 * j + 0] = __float_as_uint(__fmul_rn(sz.x, __fsub_rn(ubyte<0>(w[j]), sz.y)));
+        out[4 * j + 1] = __float_as_uint(__fmul_rn(sz.x, __fsub_rn(ubyte<1>(w[j]), sz.y)));
+        out[4 * j + 2] = __float_as_uint(__fmul_rn(sz.x, __fsub_rn(ubyte<2>(w[j]), sz.y)));
+        out[4 * j + 3] = __float_as_uint(__fmul_rn(sz.x, __fsub_rn(ubyte<3>(w[j]), sz.y)));
+      }
+    }
+    store_words<Sh::CPT * 4>(reinterpret_cast<uint8_t*>(dst + static_cast<size_t>(u) * D + col0), out);
+  }
+}
+
+// Packed zero state: zero high tier and codes, (s, z) = (1, 0) per row.
+template <int KIND, int D>
+__global__ __launch_bounds__(Shape<D>::NT) void reset_kernel(const TileParams p) {
+  using Sh = Shape<D>;
+  const int t = threadIdx.x, h = blockIdx.x, i_slot = blockIdx.y, layer = blockIdx.z;
+  const int cg = t % Sh::TPR, rg = t / Sh::TPR, col0 = cg * Sh::CPT;
+  const int slot = p.slot_idx[i_slot];
+  if (slot < 0 || slot >= p.num_slots) return;
+  uint8_t* tile = p.layer_base + static_cast<size_t>(layer) * p.layer_stride +
+                  static_cast<size_t>(slot) * p.slot_stride + static_cast<size_t>(h) * p.tile_stride;
+  const int k_hi = KIND == kFp32 ? D : p.k_hi;
+  uint8_t* codes = tile + static_cast<size_t>(k_hi) * D * 2;
+  float2* meta = reinterpret_cast<float2*>(codes + static_cast<size_t>(D - k_hi) * D);
+  float x[Sh::CPT];
+#pragma unroll
+  for (int j = 0; j < Sh::CPT; ++j) x[j] = 0.0f;
+#pragma unroll
+  for (int i = 0; i < Sh::RPT; ++i)
+    encode_row<KIND, D, Sh::CPT, Sh::TPR>(x, rg + Sh::RG * i, k_hi, cg, col0, tile, codes, meta);
+}
+
+enum class Op { kPack, kUnpack, kReset };
+
+template <int KIND, int D>
+void launch(Op op, const TileParams& p, dim3 grid, hipStream_t s) {
+  const dim3 block(Shape<D>::NT);
+  switch (op) {
+    case Op::kPack: hipLaunchKernelGGL((pack_kernel<KIND, D>), grid, block, 0, s, p); break;
+    case Op::kUnpack: hipLaunchKernelGGL((unpack_kernel<KIND, D>), grid, block, 0, s, p); break;
+    case Op::kReset: hipLaunchKernelGGL((reset_kernel<KIND, D>), grid, block, 0, s, p); break;
+  }
+}
+
+template <int KIND>
+void launch_d(Op op, int D, const TileParams& p, dim3 grid, hipStream_t s) {
+  switch (D) {
+    case 16: launch<KIND, 16>(op, p, grid, s); break;
+    case 32: launch<KIND, 32>(op, p, grid, s); break;
+    case 64: launch<KIND, 64>(op, p, grid, s); break;
+    default: launch<KIND, 128>(op, p, grid, s); break;
+  }
+}
+
+damp_status run(Op op, const char* name, const damp_pool* pool, int32_t layer,
+                const int32_t* slot_idx, int32_t B, const uint8_t* perm, float* S,
+                void* stream) {
+  clear_error();
+  damp_status st = check_pool(pool);
+  if (st != DAMP_OK) return st;
+  const bool all_layers = op == Op::kReset && layer == -1;
+  if (!all_layers && (layer < 0 || layer >= pool->num_layers))
+    return fail(DAMP_ERR_INVALID_ARG, "%s: layer %d outside [0, %d)", name, layer,
+                pool->num_layers);
+  if (B < 0 || B > 65535) return fail(DAMP_ERR_INVALID_ARG, "%s: count %d outside [0, 65535]", name, B);
+  if (B == 0) return DAMP_OK;
+  if (!slot_idx || (op != Op::kReset && !S))
+    return fail(DAMP_ERR_INVALID_ARG, "%s: a required pointer is NULL", name);
+  if (!layout_has_kernels(&pool->layout))
+    return fail(DAMP_ERR_UNSUPPORTED, "%s: no kernel for this layout", name);
+  TileParams p;
+  p.tile_stride = pool->tile_stride;
+  p.slot_stride = pool->tile_stride * static_cast<uint64_t>(pool->num_v_heads);
+  p.layer_stride = p.slot_stride * static_cast<uint64_t>(pool->num_slots);
+  p.layer_base = layer_base(pool, all_layers ? 0 : layer);
+  p.slot_idx = slot_idx;
+  p.perm = perm;
+  p.S = S;
+  p.num_slots = pool->num_slots;
+  p.HV = pool->num_v_heads;
+  p.k_hi = pool->layout.kind == DAMP_STATE_FP32 ? 0 : pool->layout.k_hi;
+  const dim3 grid(pool->num_v_heads, B, all_layers ? pool->num_layers : 1);
+  if (pool->layout.kind == DAMP_STATE_FP32)
+    launch_d<kFp32>(op, pool->layout.d_k, p, grid, as_stream(stream));
+  else
+    launch_d<kMixed>(op, pool->layout.d_k, p, grid, as_stream(stream));
+  return check_launch(name);
+}
+
+}  // namespace
+}  // namespace damp
+
+extern "C" {
+
+damp_status damp_state_pack(const damp_pool* pool, int32_t layer, const int32_t* slot_idx,
+                            int32_t B, const float* S, const uint8_t* perm, void* stream) {
+  return damp::run(damp::Op::kPack, "damp_state_pack", pool, layer, slot_idx, B, perm,
+                   const_cast<float*>(S), stream);
+}
+
+damp_status damp_state_unpack(const damp_pool* pool, int32_t layer, const int32_t* slot_idx,
+                              int32_t B, const uint8_t* perm, float* S_out, void* stream) {
+  return damp::run(damp::Op::kUnpack, "damp_state_unpack", pool, layer, slot_idx, B, perm,
+                   S_out, stream);
+}
+
+damp_status damp_pool_reset_slots(const damp_pool* pool, int32_t layer, const int32_t* slots,
+                                  int32_t n, void* stream) {
+  return damp::run(damp::Op::kReset, "damp_pool_reset_slots", pool, layer, slots, n, nullptr,
+                   nullptr, stream);
+}
+
+}  // extern "C"

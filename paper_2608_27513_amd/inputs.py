@@ -114,3 +114,27 @@ def synthetic_states(seed: int, B: int, HV: int, d: int, rank: int = 16) -> np.n
     S = np.matmul(np.swapaxes(K * w[None, :, None], 1, 2), V)
     S += f(0.01) * rng.standard_normal(S.shape, dtype=f)
     return S.reshape(B, HV, d, d).astype(f)
+
+
+def decode_inputs_device(gen, B: int, HK: int, HV: int, d: int, *, kda: bool = False,
+                         mu=None, device="cuda") -> dict:
+    """One decode step of the same distributions drawn on the GPU with a seeded
+    torch.Generator (used for long warm-up and calibration runs, where moving
+    host arrays would dominate). Returns bf16 device tensors
+    q, k [B, HK, d]; v [B, HV, d]; g [B, HV] or [B, HV, d]; beta [B, HV]."""
+    import torch
+
+    f = torch.float32
+    q = torch.randn((B, HK, d), generator=gen, device=device, dtype=f)
+    k = torch.randn((B, HK, d), generator=gen, device=device, dtype=f)
+    q = q / q.norm(dim=-1, keepdim=True).clamp_min(1e-12)
+    k = k / k.norm(dim=-1, keepdim=True).clamp_min(1e-12)
+    v = torch.randn((B, HV, d), generator=gen, device=device, dtype=f)
+    if kda:
+        x = torch.randn((B, HV, d), generator=gen, device=device, dtype=f) + mu
+    else:
+        x = torch.randn((B, HV), generator=gen, device=device, dtype=f)
+    g = -torch.nn.functional.softplus(x)
+    beta = torch.sigmoid(torch.randn((B, HV), generator=gen, device=device, dtype=f))
+    bf = torch.bfloat16
+    return dict(q=q.to(bf), k=k.to(bf), v=v.to(bf), g=g.to(bf), beta=beta.to(bf))

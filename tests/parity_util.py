@@ -1,0 +1,100 @@
+"""Helpers of the GPU parity tests: moving seeded inputs to the device and
+comparing packed tiles from the HIP path with the oracle's, field by field.
+
+Tolerances (the acceptance bar of the DAMP state update):
+  - FP32-state path: state and o within 1e-5 relative L2;
+  - mixed path: o within 2e-3 relative L2, low-tier codes within 1 LSB on at
+    least 99.9% of entries, high-tier bf16 values within 1 ulp on 99.9%;
+  - channel selection and unpack: bit-exact.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from oracle import oracle as orc
+
+O_TOL_MIXED = 2e-3
+FP32_TOL = 1e-5
+CODE_FRAC = 0.999
+
+
+def dev_bf16(u16: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(u16).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def dev_inputs(step_inp: dict) -> dict:
+    return {k: dev_bf16(v) for k, v in step_inp.items()}
+
+
+def dev_i32(a) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).cuda()
+
+
+def dev_u8(a) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.uint8)).cuda()
+
+
+def rel_l2(x, y) -> float:
+    x = np.asarray(x, np.float64)
+    y = np.asarray(y, np.float64)
+    return float(np.linalg.norm(x - y) / max(np.linalg.norm(y), 1e-300))
+
+
+def _bf16_order(u: np.ndarray) -> np.ndarray:
+    """Monotone integer key of bf16 bit patterns (adjacent values differ by 1)."""
+    u = u.astype(np.int32)
+    return np.where(u & 0x8000, -(u & 0x7FFF), u)
+
+
+def split_tiles(buf: np.ndarray, pool: "orc.Pool"):
+    """(hi bf16 [T, k_hi*dv], codes uint8 [T, nl*dv], s [T, nl], z [T, nl])
+    or the fp32 state [T, dk*dv] for every tile slot of the pool."""
+    tb = orc.tile_bytes(pool.kind, pool.dk, pool.dv, pool.k_hi)
+    tiles = np.ascontiguousarray(buf.reshape(-1, pool.tile_stride)[:, :tb])
+    if pool.kind == orc.KIND_FP32:
+        return tiles.view(np.float32)
+    hb = pool.k_hi * pool.dv * 2
+    nl = pool.dk - pool.k_hi
+    hi = np.ascontiguousarray(tiles[:, :hb]).view(np.uint16)
+    codes = tiles[:, hb:hb + nl * pool.dv]
+    meta = np.ascontiguousarray(tiles[:, hb + nl * pool.dv:]).view(np.float32).reshape(-1, nl, 2)
+    return hi, codes, meta[..., 0], meta[..., 1]
+
+
+def compare_tiles(gpu_buf: np.ndarray, ref: "orc.Pool", label: str = "") -> dict:
+    """Field-by-field comparison; asserts the acceptance bar and returns stats."""
+    if ref.kind == orc.KIND_FP32:
+        a = split_tiles(gpu_buf, ref)
+        b = split_tiles(ref.buf, ref)
+        err = rel_l2(a, b)
+        assert err <= FP32_TOL, f"{label}: fp32 state rel-L2 {err:.3e}"
+        return dict(state_rel=err)
+    ha, ca, sa, za = split_tiles(gpu_buf, ref)
+    hb, cb, sb, zb = split_tiles(ref.buf, ref)
+    stats = {}
+    if ha.size:
+        dh = np.abs(_bf16_order(ha) - _bf16_order(hb))
+        stats["hi_exact"] = float((dh == 0).mean())
+        stats["hi_le1ulp"] = float((dh <= 1).mean())
+        assert stats["hi_le1ulp"] >= CODE_FRAC, f"{label}: hi tier {stats}"
+    if ca.size:
+        dc = np.abs(ca.astype(np.int32) - cb.astype(np.int32))
+        stats["code_exact"] = float((dc == 0).mean())
+        stats["code_le1"] = float((dc <= 1).mean())
+        stats["code_maxdiff"] = int(dc.max())
+        stats["z_le1"] = float((np.abs(za - zb) <= 1).mean())
+        stats["s_rel_max"] = float(np.max(np.abs(sa.astype(np.float64) - sb) / np.abs(sb)))
+        assert stats["code_le1"] >= CODE_FRAC, f"{label}: codes {stats}"
+        assert stats["z_le1"] >= CODE_FRAC, f"{label}: zero points {stats}"
+        assert stats["s_rel_max"] <= 1e-5, f"{label}: scales {stats}"
+    return stats
+
+
+def gpu_pool_from(ref: "orc.Pool", damp_mod, layout=None):
+    """A device pool holding exactly the bytes of an oracle pool."""
+    kind = ref.kind
+    if layout is None:
+        layout = damp_mod.damp_layout_init(ref.dk, ref.dv, ref.k_hi, kind)
+    buf = torch.from_numpy(ref.buf.copy()).cuda()
+    return damp_mod.Pool(layout, ref.num_layers, ref.num_slots, ref.hv, buffer=buf)

@@ -1,0 +1,176 @@
+"""Host-side checks of libdamp: exports, layout arithmetic, argument validation.
+
+No GPU needed: every call here either is pure host arithmetic or fails
+validation before anything is enqueued.
+"""
+import ctypes
+import json
+import os
+import re
+
+import pytest
+
+from oracle import oracle as orc
+from paper_2608_27513_amd import damp as D
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "damp.h")
+GOLDEN = os.path.join(ROOT, "tests", "golden", "paper_numbers.json")
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(D.LIB_PATH):
+        from paper_2608_27513_amd import build
+        build.build()
+    return D.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(damp_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = declared_functions()
+    assert len(names) == 13
+    for n in names:
+        assert hasattr(L, n), n
+    assert sorted(D.EXPORTS) == names
+
+
+@pytest.mark.parametrize("d", [16, 32, 64, 128])
+def test_tile_geometry_matches_oracle(L, d):
+    for kind in (D.DAMP_STATE_FP32, D.DAMP_STATE_MIXED):
+        for k_hi in sorted({0, 1, 4, 8, d // 8, d // 4, d}):
+            lay = D.damp_layout_init(d, d, k_hi, kind)
+            ok = k_hi if kind == D.DAMP_STATE_MIXED else 0
+            assert D.damp_tile_bytes(lay) == orc.tile_bytes(kind, d, d, ok)
+            assert D.damp_tile_stride(lay) == orc.tile_stride(kind, d, d, ok)
+            bits = D.damp_bits_per_value(lay)
+            assert bits == orc.tile_bytes(kind, d, d, ok) * 8 / (d * d)
+
+
+def test_bits_per_value_of_the_paper_layout(L):
+    gold = json.load(open(GOLDEN))["damp_bits_per_value"]
+    lay = D.damp_layout_init(128, 128, 16, D.DAMP_STATE_MIXED)
+    lay.hi_dtype = D.DAMP_DT_FP16
+    lay.group = 32
+    lay.meta_dtype = D.DAMP_DT_FP16
+    lay.hadamard = 1
+    assert D.damp_bits_per_value(lay) == gold["value"]
+    # 16 fp16 rows + 112 code rows + 112 * 4 groups * 2 fp16 words
+    assert D.damp_tile_bytes(lay) == 16 * 256 + 112 * 128 + 112 * 4 * 4 == 20224
+
+
+def test_default_layout_numbers(L):
+    lay = D.damp_layout_init(128, 128, 16)
+    assert D.damp_tile_bytes(lay) == 19328 and D.damp_tile_stride(lay) == 19328
+    assert D.damp_bits_per_value(lay) == 9.4375
+    assert D.damp_pool_required_bytes(lay, 48, 512, 32) == 48 * 512 * 32 * 19328
+    fp = D.damp_layout_init(128, 128, 0, D.DAMP_STATE_FP32)
+    assert D.damp_pool_required_bytes(fp, 30, 256, 32) == 15 * 2 ** 30
+
+
+def _status(fn, *args):
+    st = fn(*args)
+    return st, D.lib().damp_last_error().decode()
+
+
+def test_layout_validation(L):
+    lay = D.damp_layout()
+    st, msg = _status(L.damp_layout_init, ctypes.byref(lay), 128, 128, 129, 1)
+    assert st == D.DAMP_ERR_INVALID_ARG and "k_hi" in msg
+    st, msg = _status(L.damp_layout_init, ctypes.byref(lay), 0, 128, 0, 1)
+    assert st == D.DAMP_ERR_INVALID_ARG
+    st, msg = _status(L.damp_layout_init, ctypes.byref(lay), 128, 128, 0, 7)
+    assert st == D.DAMP_ERR_INVALID_ARG and "kind" in msg
+    assert L.damp_tile_bytes(None) == 0 and L.damp_bits_per_value(None) < 0
+
+
+def test_pool_validation(L):
+    lay = D.damp_layout_init(128, 128, 16)
+    pool = D.damp_pool()
+    need = D.damp_pool_required_bytes(lay, 2, 4, 8)
+    fake = ctypes.c_void_p(0x7f0000000000)  # never dereferenced: every call below fails first
+    st, msg = _status(L.damp_pool_init, ctypes.byref(pool), ctypes.byref(lay), 2, 4, 8, None, need)
+    assert st == D.DAMP_ERR_INVALID_ARG and "NULL" in msg
+    st, msg = _status(L.damp_pool_init, ctypes.byref(pool), ctypes.byref(lay), 2, 4, 8,
+                      ctypes.c_void_p(0x7f0000000010), need)
+    assert st == D.DAMP_ERR_INVALID_ARG and "aligned" in msg
+    st, msg = _status(L.damp_pool_init, ctypes.byref(pool), ctypes.byref(lay), 2, 4, 8, fake,
+                      need - 1)
+    assert st == D.DAMP_ERR_INVALID_ARG and "needs" in msg
+    st, _ = _status(L.damp_pool_init, ctypes.byref(pool), ctypes.byref(lay), 0, 4, 8, fake, need)
+    assert st == D.DAMP_ERR_INVALID_ARG
+    st, _ = _status(L.damp_pool_init, ctypes.byref(pool), ctypes.byref(lay), 2, 4, 8, fake, need)
+    assert st == D.DAMP_OK and pool.tile_stride == 19328 and pool.bytes == need
+
+
+def _fake_pool(L, layout, layers=2, slots=4, hv=8):
+    pool = D.damp_pool()
+    need = D.damp_pool_required_bytes(layout, layers, slots, hv)
+    assert L.damp_pool_init(ctypes.byref(pool), ctypes.byref(layout), layers, slots, hv,
+                            ctypes.c_void_p(0x7f0000000000), need) == 0
+    return pool
+
+
+def test_update_validation_fails_before_launch(L):
+    lay = D.damp_layout_init(128, 128, 16)
+    pool = _fake_pool(L, lay)
+    p = ctypes.c_void_p(0x7f0000100000)  # never dereferenced
+    for fn in (L.damp_state_update_gdn, L.damp_state_update_kda):
+        args = [ctypes.byref(pool), 0, p, 4, 4, p, p, p, p, p, p, 1.0, p, D.DAMP_DT_FP32, None]
+        bad = dict(layer=(1, 2), B=(3, -1), hk=(4, 3), odt=(13, 7))
+        for name, (i, val) in bad.items():
+            a = list(args)
+            a[i] = val
+            st, msg = _status(fn, *a)
+            assert st == D.DAMP_ERR_INVALID_ARG, name
+            assert msg
+        a = list(args)
+        a[3] = 0  # B = 0 is a no-op
+        assert fn(*a) == D.DAMP_OK
+        a = list(args)
+        a[5] = None  # q
+        assert fn(*a) == D.DAMP_ERR_INVALID_ARG
+        assert fn(None, *args[1:]) == D.DAMP_ERR_INVALID_ARG
+
+
+def test_layouts_without_kernels_are_reported(L):
+    lay = D.damp_layout_init(128, 128, 16)
+    lay.group = 32  # the paper's group-32 low tier has no kernel
+    pool = _fake_pool(L, lay)
+    p = ctypes.c_void_p(0x7f0000100000)
+    st, msg = _status(L.damp_state_update_gdn, ctypes.byref(pool), 0, p, 4, 4, p, p, p, p, p,
+                      None, 1.0, p, 0, None)
+    assert st == D.DAMP_ERR_UNSUPPORTED and "no kernel" in msg
+    st, _ = _status(L.damp_state_pack, ctypes.byref(pool), 0, p, 4, p, None, None)
+    assert st == D.DAMP_ERR_UNSUPPORTED
+    lay = D.damp_layout_init(96, 96, 16)  # valid layout, no kernel width
+    pool = _fake_pool(L, lay)
+    st, _ = _status(L.damp_state_unpack, ctypes.byref(pool), 0, p, 4, None, p, None)
+    assert st == D.DAMP_ERR_UNSUPPORTED
+
+
+def test_pack_reset_validation(L):
+    lay = D.damp_layout_init(64, 64, 8)
+    pool = _fake_pool(L, lay)
+    p = ctypes.c_void_p(0x7f0000100000)
+    assert L.damp_state_pack(ctypes.byref(pool), 2, p, 4, p, None, None) == D.DAMP_ERR_INVALID_ARG
+    assert L.damp_state_pack(ctypes.byref(pool), 0, None, 4, p, None, None) == D.DAMP_ERR_INVALID_ARG
+    assert L.damp_state_unpack(ctypes.byref(pool), 0, p, 4, None, None, None) == \
+        D.DAMP_ERR_INVALID_ARG
+    assert L.damp_pool_reset_slots(ctypes.byref(pool), 5, p, 1, None) == D.DAMP_ERR_INVALID_ARG
+    assert L.damp_pool_reset_slots(ctypes.byref(pool), -1, p, 0, None) == D.DAMP_OK
+
+
+def test_select_validation(L):
+    p = ctypes.c_void_p(0x7f0000100000)
+    f = L.damp_select_channels
+    assert f(0, 4, 2, 128, 128, p, p, 129, 1e-4, p, p, None, None) == D.DAMP_ERR_INVALID_ARG
+    assert f(0, 4, 2, 128, 128, p, p, 16, 0.0, p, p, None, None) == D.DAMP_ERR_INVALID_ARG
+    assert f(0, 0, 2, 128, 128, p, p, 16, 1e-4, p, p, None, None) == D.DAMP_ERR_INVALID_ARG
+    assert f(0, 4, 2, 300, 128, p, p, 16, 1e-4, p, p, None, None) == D.DAMP_ERR_INVALID_ARG
+    assert f(0, 4, 2, 128, 128, None, p, 16, 1e-4, p, p, None, None) == D.DAMP_ERR_INVALID_ARG

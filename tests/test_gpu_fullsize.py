@@ -1,0 +1,89 @@
+"""Full-size GPU parity in the launch configuration the benchmark times.
+
+Config 2 (GDN: B=256, 16 key / 32 value heads, d=128, 16 BF16 rows, 8 outlier
+channels per head at 10x) and config 3 (KDA: B=256, 32 heads, per-channel
+decay with ~10% persistent channels, 16 channels chosen by the selection).
+The oracle packs every tile and runs the whole step, so every output and
+every stored byte is compared. Also the largest batch a launch takes and the
+empty batch.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as orc
+from paper_2608_27513_amd import damp as D
+from paper_2608_27513_amd import inputs
+from parity_util import O_TOL_MIXED, compare_tiles, dev_i32, dev_inputs, dev_u8, gpu_pool_from, rel_l2
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+@pytest.mark.parametrize("kda", [False, True])
+def test_full_size_step(kda):
+    B, HV, d, k_hi = 256, 32, 128, 16
+    HK = HV if kda else 16
+    seed = 2 if not kda else 3
+    _say(f"full-size {'KDA' if kda else 'GDN'}: B={B} HK={HK} HV={HV} d={d} k_hi={k_hi}")
+    S = inputs.synthetic_states(seed, B, HV, d)
+    mu = inputs.kda_mu(seed, HV, d) if kda else None
+    if not kda:
+        inputs.scale_channels(S, inputs.outlier_channels(seed, HV, d, 8), 10.0)
+    # channel selection from 64 calibration samples of the same distribution
+    cal = S[:64]
+    if kda:
+        logs = -np.logaddexp(0.0, mu[None] + np.random.default_rng(seed).standard_normal(
+            (64, HV, d))).astype(np.float32)
+    else:
+        logs = np.full((64, HV), -0.5, np.float32)
+    perm = orc.select(kda=kda, states=cal, log_decay=logs, k_hi=k_hi)["perm"]
+    slots = inputs.slot_order(seed, B, B)
+    ref = orc.Pool(orc.KIND_MIXED, d, d, k_hi, 1, B, HV)
+    orc.pack(ref, 0, slots, S, perm)
+    del S, cal
+    gpool = gpu_pool_from(ref, D)
+    inp = inputs.step(inputs.decode_inputs(seed, 1, B, HK, HV, d, kda=kda, mu=mu), 0)
+    di = dev_inputs(inp)
+    o = torch.empty((B, HV, d), dtype=torch.float32, device="cuda")
+    fn = D.damp_state_update_kda if kda else D.damp_state_update_gdn
+    fn(gpool, 0, dev_i32(slots), di["q"], di["k"], di["v"], di["g"], di["beta"],
+       perm=dev_u8(perm), o=o)
+    torch.cuda.synchronize()
+    _say("  gpu step done; running the oracle")
+    o_ref = orc.update(ref, 0, slots, kda=kda, perm=perm, **inp)
+    err = rel_l2(o.cpu().numpy(), o_ref)
+    stats = compare_tiles(gpool.buffer.cpu().numpy(), ref, "full-size")
+    _say(f"  o rel-L2 {err:.2e}  {stats}")
+    assert err <= O_TOL_MIXED and err <= 1e-4
+
+
+def test_largest_batch_and_empty_batch():
+    B, HV, d, k_hi = 65535, 1, 16, 4
+    _say(f"max batch: B={B} HV={HV} d={d}")
+    S = inputs.synthetic_states(4, B, HV, d)
+    slots = np.arange(B, dtype=np.int32)
+    ref = orc.Pool(orc.KIND_MIXED, d, d, k_hi, 1, B, HV)
+    orc.pack(ref, 0, slots, S)
+    gpool = gpu_pool_from(ref, D)
+    inp = inputs.step(inputs.decode_inputs(5, 1, B, 1, HV, d), 0)
+    di = dev_inputs(inp)
+    o = torch.empty((B, HV, d), dtype=torch.float32, device="cuda")
+    D.damp_state_update_gdn(gpool, 0, dev_i32(slots), di["q"], di["k"], di["v"], di["g"],
+                            di["beta"], o=o)
+    torch.cuda.synchronize()
+    o_ref = orc.update(ref, 0, slots, kda=False, **inp)
+    assert rel_l2(o.cpu().numpy(), o_ref) <= 1e-4
+    compare_tiles(gpool.buffer.cpu().numpy(), ref, "max batch")
+    # an empty batch is a no-op
+    before = gpool.buffer.clone()
+    e = torch.empty(0, dtype=torch.int32, device="cuda")
+    z = torch.empty((0, 1, d), dtype=torch.bfloat16, device="cuda")
+    D.damp_state_update_gdn(gpool, 0, e, z, z, z, torch.empty((0, 1), dtype=torch.bfloat16,
+                            device="cuda"), torch.empty((0, 1), dtype=torch.bfloat16,
+                            device="cuda"), o=torch.empty((0, 1, d), device="cuda"))
+    torch.cuda.synchronize()
+    assert torch.equal(before, gpool.buffer)
