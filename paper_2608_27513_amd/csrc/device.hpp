@@ -73,6 +73,19 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
+// Sum over the 64 lanes of a wave with DPP only (no LDS traffic): butterfly
+// within rows of 16 lanes, then row broadcasts; the total ends in lane 63 and
+// is returned to every lane as a wave-uniform value.
+__device__ __forceinline__ float wave_sum_dpp(float x) {
+  x += dpp_mov<0xb1>(x);   // quad_perm [1,0,3,2]
+  x += dpp_mov<0x4e>(x);   // quad_perm [2,3,0,1]
+  x += dpp_mov<0x141>(x);  // row_half_mirror
+  x += dpp_mov<0x140>(x);  // row_mirror: every lane holds its row's sum
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x142, 0xa, 0xf, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x143, 0xc, 0xf, false));
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 63));
+}
+
 // ------------------------------------------------------------- vector I/O
 
 template <int NBYTES>

@@ -20,29 +20,10 @@
 // so no second reduction over S' is needed.
 #include "device.hpp"
 #include "internal.hpp"
+#include "update.hpp"
 
 namespace damp {
 namespace {
-
-struct UpdateParams {
-  uint8_t* layer_base;
-  uint64_t slot_stride;
-  uint64_t tile_stride;
-  const int32_t* slot_idx;
-  const uint16_t* q;
-  const uint16_t* k;
-  const uint16_t* v;
-  const uint16_t* g;
-  const uint16_t* beta;
-  const uint8_t* perm;
-  void* o;
-  float scale;
-  int32_t num_slots;
-  int32_t HK;
-  int32_t HV;
-  int32_t k_hi;
-  int32_t o_bf16;
-};
 
 __device__ __forceinline__ void write_o(const UpdateParams& p, size_t idx, float val) {
   if (p.o_bf16)
@@ -270,6 +251,11 @@ damp_status update(bool kda, const damp_pool* pool, int32_t layer, const int32_t
   p.o_bf16 = o_dtype == DAMP_DT_BF16;
   const int D = pool->layout.d_k;
   hipStream_t s = as_stream(stream);
+  if (pool->layout.kind == DAMP_STATE_MIXED && D == 128 && p.k_hi <= 32) {
+    if (!launch_stream128(kda, p, B, s))
+      return fail(DAMP_ERR_HIP, "%s: occupancy query failed", name);
+    return check_launch(name);
+  }
   if (pool->layout.kind == DAMP_STATE_FP32) {
     if (kda) launch_d<kFp32, true>(D, p, B, s);
     else launch_d<kFp32, false>(D, p, B, s);

@@ -1,0 +1,34 @@
+// Parameters shared by the decode-step update kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace damp {
+
+struct UpdateParams {
+  uint8_t* layer_base;
+  uint64_t slot_stride;
+  uint64_t tile_stride;
+  const int32_t* slot_idx;
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  const uint16_t* g;
+  const uint16_t* beta;
+  const uint8_t* perm;
+  void* o;
+  float scale;
+  int32_t num_slots;
+  int32_t HK;
+  int32_t HV;
+  int32_t k_hi;
+  int32_t o_bf16;
+};
+
+// The streaming kernel for d = 128 mixed tiles with k_hi <= 32 (update_stream.hip).
+// Returns false if it did not launch (a HIP query failed).
+bool launch_stream128(bool kda, const UpdateParams& p, int B, hipStream_t stream);
+
+}  // namespace damp

@@ -1,0 +1,403 @@
+// Persistent, software-pipelined decode-step update for d_k = d_v = 128 mixed
+// tiles with at most 32 high-precision rows (section 3.1 Eq. (1)-(2);
+// section 3.2 Eq. (3); section 5.2 and App. A.5).
+//
+// The state update moves ~2.4 bytes per state value and does ~8 VALU
+// operations per value, so on MI355X the memory time and the VALU time are of
+// the same size; the kernel must overlap them. Each workgroup (4 wave64) is
+// resident for the whole launch and walks the tiles (b, h) with a fixed value
+// head h = blockIdx.x mod HV, so the channel permutation and the row offsets
+// are computed once. While tile k is reduced, updated, re-encoded and
+// stored, the packed bytes of tile k+1 are already in flight into registers.
+//
+// Tiles are read and written through buffer resources whose size is the tile
+// size, or 0 for a padded request: then the loads return zeros and the
+// stores are dropped by the hardware, so every thread issues the same
+// memory instructions for every tile. Loads and stores of the state are
+// non-temporal: each tile is touched once per step.
+//
+// Per tile: thread t (row group rg = t / 8, column group cg = t % 8) holds
+// rows rg, rg+32, rg+64, rg+96, columns 16 cg .. 16 cg + 15. Row 0 of a thread
+// can be in the high (bf16) tier, the others are low (uint8) rows.
+// Operands are staged once per tile by threads t < 128 (one tile row each):
+// k~, q~, the row decay a~ and v, in LDS; q~ . k~ is reduced there too.
+#include "device.hpp"
+#include "internal.hpp"
+#include "update.hpp"
+
+namespace damp {
+namespace {
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kCachePolicyNT = 2;           // non-temporal loads and stores
+constexpr int kBufferConfig = 0x00020000;   // raw 32-bit buffer (gfx9 family)
+
+// Workgroup barrier ordering LDS only (global loads stay in flight). The
+// scheduling fences keep the compiler from hoisting uses of prefetched
+// values above it, which would wait on their latency here.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// voff: per-lane byte offset; soff: wave-uniform byte offset
+__device__ __forceinline__ u32x4 ld16(__amdgpu_buffer_rsrc_t r, int voff, int soff = 0) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kCachePolicyNT);
+}
+__device__ __forceinline__ u32x2 ld8(__amdgpu_buffer_rsrc_t r, int voff, int soff = 0) {
+  return __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, kCachePolicyNT);
+}
+__device__ __forceinline__ void st16(u32x4 v, __amdgpu_buffer_rsrc_t r, int voff, int soff = 0) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, soff, kCachePolicyNT);
+}
+__device__ __forceinline__ void st8(u32x2 v, __amdgpu_buffer_rsrc_t r, int voff, int soff = 0) {
+  __builtin_amdgcn_raw_buffer_store_b64(v, r, voff, soff, kCachePolicyNT);
+}
+
+template <bool KDA>
+__global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, const int ntiles,
+                                                        const int tile_bytes) {
+  constexpr int D = 128, RG = 32, RPT = 4, CPT = 16, TPR = 8;
+  constexpr int kDrop = 0x40000000;  // buffer offset past any tile: the store is dropped
+  __shared__ float red[RG][2 * D + 4];
+  __shared__ float dsh[D];
+  __shared__ float4 opr[2][D];  // per tile parity, row r: (k~_r, q~_r, a~_r, v_r)
+  __shared__ float opsc[2][4];  // per parity: beta, alpha (GDN), two partial sums of q~ . k~
+  __shared__ int next_slot;     // pool slot of the tile after the staged one
+
+  const int t = threadIdx.x;
+  const int cg = t % TPR, rg = t / TPR, col0 = cg * CPT;
+  const int HV = p.HV;
+  const int G = gridDim.x;  // a multiple of HV
+  const int h = blockIdx.x % HV;
+  const int hk = h / (HV / p.HK);
+  const int k_hi = p.k_hi;
+  const bool hi0 = rg < k_hi;  // row slot 0 of this thread is in the bf16 tier
+  const int lo0 = k_hi * D * 2;
+  const int meta0 = lo0 + (D - k_hi) * D;
+  const int o_esize = p.o_bf16 ? 2 : 4;
+
+  // byte offsets of this thread's row slices inside a tile (same for every
+  // tile). Row slot 0 always loads 16 bytes at off_b0: the second half of a
+  // bf16 row, or the (s, z) pair of its low row followed by the next row's.
+  // Rows 1..3 (always low) sit at off_a1 + (i-1) * 32 rows of codes and
+  // off_b1 + (i-1) * 32 pairs of metadata (scalar offsets).
+  const int off_a0 = hi0 ? (rg * D + col0) * 2 : lo0 + (rg - k_hi) * D + col0;
+  const int off_b0 = hi0 ? off_a0 + 16 : meta0 + (rg - k_hi) * 8;
+  const int off_a1 = lo0 + (rg + RG - k_hi) * D + col0;
+  const int off_b1 = meta0 + (rg + RG - k_hi) * 8;
+  constexpr int kStepA = RG * D, kStepB = RG * 8;
+  const int st_b0 = hi0 ? off_b0 : kDrop;                    // second bf16 half
+  const int st_m0 = (cg == 0 && !hi0) ? off_b0 : kDrop;      // (s, z) of row slot 0
+  const int st_m1 = cg == 0 ? off_b1 : kDrop;                // (s, z) of rows 1..3
+  const int st_o = t >= D ? (t - D) * o_esize : kDrop;
+  const int my_u = (t < D && p.perm) ? (static_cast<int>(p.perm[h * D + t]) & (D - 1)) : t;
+
+  int tau = blockIdx.x;
+  if (tau >= ntiles) return;
+
+  // ---- operand staging (threads t < D, i.e. waves 0 and 1) ----------------
+  uint32_t ok = 0, oq = 0, og = 0, ov = 0, obeta = 0, og0 = 0;
+  int oslot = -1;
+  auto issue_ops = [&](int tau_) {  // operands of tile tau_, slot of tile tau_ + G
+    if (t < D) {
+      const int b_ = tau_ / HV;
+      const size_t bh = static_cast<size_t>(b_) * HV + h;
+      const size_t kq = (static_cast<size_t>(b_) * p.HK + hk) * D;
+      ok = p.k[kq + my_u];
+      oq = p.q[kq + my_u];
+      if (KDA) og = p.g[bh * D + my_u];
+      else og0 = p.g[bh];
+      ov = p.v[bh * D + t];
+      obeta = p.beta[bh];
+      oslot = tau_ + G < ntiles ? p.slot_idx[(tau_ + G) / HV] : -1;
+    }
+  };
+  auto publish_ops = [&](int par) {
+    if (t < D) {
+      const float kf = bf16_to_f32(static_cast<uint16_t>(ok));
+      const float qf = bf16_to_f32(static_cast<uint16_t>(oq));
+      const float af = KDA ? __expf(bf16_to_f32(static_cast<uint16_t>(og))) : 1.0f;
+      opr[par][t] = make_float4(kf, qf, af, bf16_to_f32(static_cast<uint16_t>(ov)));
+      const float kq = wave_sum_dpp(kf * qf);
+      if ((t & 63) == 0) opsc[par][2 + (t >> 6)] = kq;
+      if (t == 0) {
+        opsc[par][0] = bf16_to_f32(static_cast<uint16_t>(obeta));
+        opsc[par][1] = KDA ? 1.0f : __expf(bf16_to_f32(static_cast<uint16_t>(og0)));
+        next_slot = oslot;
+      }
+    }
+  };
+
+  // ---- packed tile loads into registers -----------------------------------
+  auto make_rsrc = [&](int slot_) {
+    const bool live = slot_ >= 0 && slot_ < p.num_slots;
+    uint8_t* base = p.layer_base + static_cast<size_t>(live ? slot_ : 0) * p.slot_stride +
+                    static_cast<size_t>(h) * p.tile_stride;
+    return __builtin_amdgcn_make_buffer_rsrc(base, 0, live ? tile_bytes : 0, kBufferConfig);
+  };
+  u32x4 ra[RPT], rb0;
+  u32x2 rb[RPT];
+  auto issue_raw = [&](__amdgpu_buffer_rsrc_t r) {
+    ra[0] = ld16(r, off_a0);
+    rb0 = ld16(r, off_b0);
+#pragma unroll
+    for (int i = 1; i < RPT; ++i) {
+      ra[i] = ld16(r, off_a1, (i - 1) * kStepA);
+      rb[i] = ld8(r, off_b1, (i - 1) * kStepB);
+    }
+  };
+
+  // ---- prologue -------------------------------------------------------------
+  int slot_cur = p.slot_idx[tau / HV];
+  __amdgpu_buffer_rsrc_t rs_cur = make_rsrc(slot_cur);
+  issue_ops(tau);
+  issue_raw(rs_cur);
+  publish_ops(0);
+  // settle the first tile's bytes here, so that the loop head only waits as
+  // far as the stores issued after each prefetch
+  asm volatile("" ::"v"(ra[0]), "v"(rb0), "v"(ra[1]), "v"(rb[1]), "v"(ra[2]), "v"(rb[2]),
+               "v"(ra[3]), "v"(rb[3]));
+  lds_barrier();
+
+  for (int par = 0;; par ^= 1) {
+    const bool live = slot_cur >= 0 && slot_cur < p.num_slots;
+    // -- operands of this tile; dequantize and decay: S_bar = Lambda S
+    float kk[RPT], qq[RPT], aa[RPT];
+    const float alpha = opsc[par][1];
+    const int slot_next = __builtin_amdgcn_readfirstlane(next_slot);
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) {
+      const float4 o4 = opr[par][rg + RG * i];
+      kk[i] = o4.x;
+      qq[i] = o4.y;
+      aa[i] = KDA ? o4.z : alpha;
+    }
+
+    float x[RPT][CPT];
+    if (hi0) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        x[0][2 * j] = aa[0] * bf16_lo(ra[0][j]);
+        x[0][2 * j + 1] = aa[0] * bf16_hi(ra[0][j]);
+        x[0][8 + 2 * j] = aa[0] * bf16_lo(rb0[j]);
+        x[0][8 + 2 * j + 1] = aa[0] * bf16_hi(rb0[j]);
+      }
+    } else {
+      const float A = aa[0] * __uint_as_float(rb0.x);
+      const float B0 = -A * __uint_as_float(rb0.y);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        x[0][4 * j + 0] = fmaf(A, ubyte<0>(ra[0][j]), B0);
+        x[0][4 * j + 1] = fmaf(A, ubyte<1>(ra[0][j]), B0);
+        x[0][4 * j + 2] = fmaf(A, ubyte<2>(ra[0][j]), B0);
+        x[0][4 * j + 3] = fmaf(A, ubyte<3>(ra[0][j]), B0);
+      }
+    }
+#pragma unroll
+    for (int i = 1; i < RPT; ++i) {
+      const float A = aa[i] * __uint_as_float(rb[i].x);
+      const float B0 = -A * __uint_as_float(rb[i].y);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        x[i][4 * j + 0] = fmaf(A, ubyte<0>(ra[i][j]), B0);
+        x[i][4 * j + 1] = fmaf(A, ubyte<1>(ra[i][j]), B0);
+        x[i][4 * j + 2] = fmaf(A, ubyte<2>(ra[i][j]), B0);
+        x[i][4 * j + 3] = fmaf(A, ubyte<3>(ra[i][j]), B0);
+      }
+    }
+
+    // the dequantized tile must exist before the next tile's loads are issued,
+    // so that the waits for this tile's bytes precede the prefetch
+#pragma unroll
+    for (int i = 0; i < RPT; ++i)
+      asm volatile("" ::"v"(x[i][0]), "v"(x[i][1]), "v"(x[i][2]), "v"(x[i][3]), "v"(x[i][4]),
+                   "v"(x[i][5]), "v"(x[i][6]), "v"(x[i][7]), "v"(x[i][8]), "v"(x[i][9]),
+                   "v"(x[i][10]), "v"(x[i][11]), "v"(x[i][12]), "v"(x[i][13]), "v"(x[i][14]),
+                   "v"(x[i][15]));
+
+    // -- prefetch the next tile: operands first, then the packed bytes
+    const int tau_n = tau + G;
+    const bool has_next = tau_n < ntiles;
+    __amdgpu_buffer_rsrc_t rs_next = rs_cur;
+    if (has_next) {
+      issue_ops(tau_n);
+      rs_next = make_rsrc(slot_next);
+      issue_raw(rs_next);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+
+    // -- partial key and query read-outs, reduced over row groups in LDS
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      float pw[8], pq[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        pw[j] = kk[0] * x[0][8 * half + j];
+        pq[j] = qq[0] * x[0][8 * half + j];
+      }
+#pragma unroll
+      for (int i = 1; i < RPT; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          pw[j] = fmaf(kk[i], x[i][8 * half + j], pw[j]);
+          pq[j] = fmaf(qq[i], x[i][8 * half + j], pq[j]);
+        }
+      float* rw = &red[rg][col0 + 8 * half];
+      *reinterpret_cast<float4*>(rw) = make_float4(pw[0], pw[1], pw[2], pw[3]);
+      *reinterpret_cast<float4*>(rw + 4) = make_float4(pw[4], pw[5], pw[6], pw[7]);
+      *reinterpret_cast<float4*>(rw + D) = make_float4(pq[0], pq[1], pq[2], pq[3]);
+      *reinterpret_cast<float4*>(rw + D + 4) = make_float4(pq[4], pq[5], pq[6], pq[7]);
+    }
+    lds_barrier();
+
+    // -- column totals: w = S_bar^T k~ (t < D), S_bar^T q~ (t >= D)
+    float tot;
+    {
+      float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int g = 0; g < RG; ++g) acc[g & 3] += red[g][t];
+      tot = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+    }
+    if (t < D) dsh[t] = opr[par][t].w - tot;  // delta = v - S_bar^T k~
+    if (has_next) publish_ops(par ^ 1);       // next tile's operands (waits only for them)
+    lds_barrier();
+    const float beta = opsc[par][0], qk = opsc[par][2] + opsc[par][3];
+
+    // -- output o = scale (S_bar^T q~ + beta (q~.k~) delta), written by t >= D
+    {
+      const float oval = live ? p.scale * fmaf(beta * qk, dsh[t & (D - 1)], tot) : 0.0f;
+      uint8_t* obase = static_cast<uint8_t*>(p.o) +
+                       (static_cast<size_t>(tau / HV) * HV + h) * D * o_esize;
+      const __amdgpu_buffer_rsrc_t ro =
+          __builtin_amdgcn_make_buffer_rsrc(obase, 0, D * o_esize, kBufferConfig);
+      if (p.o_bf16)
+        __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16(oval), ro, st_o, 0, 0);
+      else
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(oval), ro, st_o, 0, 0);
+    }
+
+    // -- rank-1 update S' = S_bar + beta k~ delta^T, re-encode, store in place
+    float dl[CPT];
+#pragma unroll
+    for (int j = 0; j < CPT; j += 4) {
+      const float4 d4 = *reinterpret_cast<const float4*>(&dsh[col0 + j]);
+      dl[j] = d4.x;
+      dl[j + 1] = d4.y;
+      dl[j + 2] = d4.z;
+      dl[j + 3] = d4.w;
+    }
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) {
+      const float bk = beta * opr[par][rg + RG * i].x;
+#pragma unroll
+      for (int j = 0; j < CPT; ++j) x[i][j] = fmaf(bk, dl[j], x[i][j]);
+    }
+    u32x4 wa[RPT], wb0;
+    u32x2 wm[RPT];
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) {
+      if (i == 0 && hi0) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          wa[0][j] = pack_bf16x2(x[0][2 * j], x[0][2 * j + 1]);
+          wb0[j] = pack_bf16x2(x[0][8 + 2 * j], x[0][8 + 2 * j + 1]);
+        }
+        wm[0] = u32x2{0u, 0u};
+        continue;
+      }
+      float mn = x[i][0], mx = x[i][0];
+#pragma unroll
+      for (int j = 1; j < CPT; ++j) {
+        mn = fminf(mn, x[i][j]);
+        mx = fmaxf(mx, x[i][j]);
+      }
+      group_minmax<TPR>(mn, mx);
+      float s, z, inv;
+      row_qparams(mn, mx, s, z, inv);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        // v_cvt_pk_u8_f32 rounds to nearest even and saturates to [0, 255]
+        uint32_t c = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(x[i][4 * j], inv, z), 0, 0u);
+        c = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(x[i][4 * j + 1], inv, z), 1, c);
+        c = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(x[i][4 * j + 2], inv, z), 2, c);
+        wa[i][j] = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(x[i][4 * j + 3], inv, z), 3, c);
+      }
+      wm[i] = u32x2{__float_as_uint(s), __float_as_uint(z)};
+      if (i == 0) wb0 = u32x4{0u, 0u, 0u, 0u};
+    }
+    // every thread issues the same stores; lanes with nothing to write use
+    // an offset past the buffer, which the hardware drops
+    st16(wa[0], rs_cur, off_a0);
+    st16(wb0, rs_cur, st_b0);
+    st8(wm[0], rs_cur, st_m0);
+#pragma unroll
+    for (int i = 1; i < RPT; ++i) {
+      st16(wa[i], rs_cur, off_a1, (i - 1) * kStepA);
+      st8(wm[i], rs_cur, st_m1, (i - 1) * kStepB);
+    }
+
+    if (!has_next) break;
+    tau = tau_n;
+    slot_cur = slot_next;
+    rs_cur = rs_next;
+  }
+}
+
+struct Occupancy {
+  int cus = 0;
+  int per_cu[2] = {0, 0};
+};
+
+bool occupancy(bool kda, int& cus, int& per_cu) {
+  static Occupancy cache[16];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 16) return false;
+  Occupancy& c = cache[dev];
+  if (c.cus == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      return false;
+    int a = 0, b = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&a, update_stream128<false>, 256, 0) !=
+            hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, update_stream128<true>, 256, 0) !=
+            hipSuccess)
+      return false;
+    c.per_cu[0] = a > 0 ? a : 1;
+    c.per_cu[1] = b > 0 ? b : 1;
+    c.cus = n;
+  }
+  cus = c.cus;
+  per_cu = c.per_cu[kda ? 1 : 0];
+  return true;
+}
+
+}  // namespace
+
+bool launch_stream128(bool kda, const UpdateParams& p, int B, hipStream_t stream) {
+  int cus = 0, per_cu = 0;
+  if (!occupancy(kda, cus, per_cu)) return false;
+  const int ntiles = B * p.HV;
+  // resident workgroups, rounded down to a multiple of HV (at least HV)
+  const long capacity = static_cast<long>(cus) * per_cu;
+  long per_head = capacity / p.HV;
+  if (per_head < 1) per_head = 1;
+  if (per_head > B) per_head = B;
+  const int grid = static_cast<int>(per_head * p.HV);
+  const int tile_bytes = p.k_hi * 128 * 2 + (128 - p.k_hi) * 128 + (128 - p.k_hi) * 8;
+  if (kda)
+    hipLaunchKernelGGL(update_stream128<true>, dim3(grid), dim3(256), 0, stream, p, ntiles,
+                       tile_bytes);
+  else
+    hipLaunchKernelGGL(update_stream128<false>, dim3(grid), dim3(256), 0, stream, p, ntiles,
+                       tile_bytes);
+  return true;
+}
+
+}  // namespace damp

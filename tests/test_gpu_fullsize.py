@@ -87,3 +87,41 @@ def test_largest_batch_and_empty_batch():
                             device="cuda"), o=torch.empty((0, 1, d), device="cuda"))
     torch.cuda.synchronize()
     assert torch.equal(before, gpool.buffer)
+
+
+@pytest.mark.parametrize("kda,k_hi,o_bf16", [(False, 16, False), (True, 8, True), (False, 0, False),
+                                              (True, 32, False), (False, 12, False)])
+def test_many_tiles_per_workgroup_with_padding(kda, k_hi, o_bf16):
+    """B = 600 requests in a 700-slot pool (several tiles per resident
+    workgroup), with padded (-1) and out-of-range slots scattered through the
+    batch: padded requests leave their memory untouched and output zeros."""
+    B, HV, d, num_slots = 600, 32, 128, 700
+    HK = HV if kda else 8
+    seed = 40 + k_hi + kda
+    _say(f"padded batch: kda={kda} k_hi={k_hi} o_bf16={o_bf16}")
+    slots = inputs.slot_order(seed, num_slots, B).copy()
+    rng = np.random.default_rng(seed)
+    pad = rng.choice(B, size=37, replace=False)
+    slots[pad[:30]] = -1
+    slots[pad[30:]] = num_slots + rng.integers(0, 5, 7)
+    S = inputs.synthetic_states(seed, num_slots, HV, d)
+    perm = inputs.random_perms(seed, HV, d)
+    ref = orc.Pool(orc.KIND_MIXED, d, d, k_hi, 2, num_slots, HV)
+    orc.pack(ref, 1, np.arange(num_slots), S, perm)
+    del S
+    gpool = gpu_pool_from(ref, D)
+    inp = inputs.step(inputs.decode_inputs(seed, 1, B, HK, HV, d, kda=kda), 0)
+    di = dev_inputs(inp)
+    o = torch.empty((B, HV, d), dtype=torch.bfloat16 if o_bf16 else torch.float32,
+                    device="cuda")
+    fn = D.damp_state_update_kda if kda else D.damp_state_update_gdn
+    fn(gpool, 1, dev_i32(slots), di["q"], di["k"], di["v"], di["g"], di["beta"],
+       perm=dev_u8(perm), scale=0.5, o=o)
+    torch.cuda.synchronize()
+    o_ref = orc.update(ref, 1, slots, kda=kda, perm=perm, scale=0.5, **inp)
+    o_gpu = o.float().cpu().numpy()
+    assert (o_gpu[pad] == 0).all()
+    tol = 1e-2 if o_bf16 else 1e-4
+    assert rel_l2(o_gpu, o_ref) <= tol
+    stats = compare_tiles(gpool.buffer.cpu().numpy(), ref, "padded batch")
+    _say(f"  o rel-L2 {rel_l2(o_gpu, o_ref):.2e} {stats}")
