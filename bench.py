@@ -35,7 +35,8 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 PROFILE = os.path.join(ROOT, "profiles", "update_gdn_mixed_b256_counters.txt")
-KERNEL_SOURCES = ["paper_2608_27513_amd/csrc/update.hip", "paper_2608_27513_amd/csrc/device.hpp"]
+KERNEL_SOURCES = ["paper_2608_27513_amd/csrc/update_stream.hip", "paper_2608_27513_amd/csrc/update.hpp",
+                  "paper_2608_27513_amd/csrc/device.hpp"]
 
 
 def parse():
@@ -47,7 +48,22 @@ def parse():
     ap.add_argument("--quick", action="store_true", help="headline only: no baselines, no CPU")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device copy (counter calibration)")
     return ap.parse_args()
+
+
+def copy_calibration(torch, reps: int = 5):
+    """A plain device-to-device copy of exactly 1 GiB, `reps` times: the known
+    byte count that HBM counters (FETCH_SIZE, WRITE_SIZE) are scaled by."""
+    n = 1 << 30
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "reps": reps}), flush=True)
 
 
 def kernel_source_hash() -> str:
@@ -189,26 +205,23 @@ class Workload:
 
 
 def time_steps(torch, calls, warmup: int, steps: int):
-    """Wall time of `steps` launches between two synchronisations, then the
-    mean HIP-event duration of each launch in a second pass."""
+    """`steps` back-to-back launches between two synchronisations: wall time,
+    and the HIP-event time over the same region on the launch stream (its
+    mean per launch is the kernel duration the roofline uses)."""
     n = len(calls)
     for i in range(warmup):
         calls[i % n]()
     torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
+    start.record()
     for i in range(steps):
         calls[(warmup + i) % n]()
+    end.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(steps)]
-    for i in range(steps):
-        ev[i][0].record()
-        calls[i % n]()
-        ev[i][1].record()
-    torch.cuda.synchronize()
-    durs = sorted(a.elapsed_time(b) * 1e-3 for a, b in ev)
-    return dict(wall_s=wall, mean_launch_s=sum(durs) / len(durs), median_launch_s=durs[len(durs) // 2])
+    ev = start.elapsed_time(end) * 1e-3
+    return dict(wall_s=wall, mean_launch_s=ev / steps)
 
 
 def measure(torch, D, wl: Workload, kind: int, k_hi: int, rotations: int, warmup: int,
@@ -222,7 +235,6 @@ def measure(torch, D, wl: Workload, kind: int, k_hi: int, rotations: int, warmup
     res = dict(
         us_per_step=1e6 * t["wall_s"] / steps,
         kernel_us=1e6 * t["mean_launch_s"],
-        kernel_us_median=1e6 * t["median_launch_s"],
         bytes_per_step=nbytes,
         gbs=nbytes * steps / t["wall_s"] / 1e9,
         kernel_gbs=nbytes / t["mean_launch_s"] / 1e9,
@@ -281,6 +293,9 @@ def main():
 
     if not torch.cuda.is_available():
         raise SystemExit("no GPU visible")
+    if args.copy_calibration:
+        copy_calibration(torch)
+        return
     D.lib()
     B, HK, HV, d, k_hi = 256, 16, 32, 128, 16
     log("setting up GDN B=256 HK=16 HV=32 d=128 K_hi=16")

@@ -28,9 +28,19 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-ffp-contract
           "-I", INCLUDE, "-I", CSRC, "-Wall", "-Wno-unused-result"]
 
 
+# State values are finite by contract (include/damp.h), so the update and pack
+# kernels may drop NaN-preserving min/max; the selection kernel keeps strict
+# IEEE semantics because its results must be reproducible bit for bit.
+PER_FILE = {
+    "update.hip": ["-fno-honor-nans"],
+    "update_stream.hip": ["-fno-honor-nans"],
+    "pack.hip": ["-fno-honor-nans"],
+}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(OBJDIR, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *COMMON, "-c", src, "-o", obj]
+    cmd = [HIPCC, *COMMON, *PER_FILE.get(os.path.basename(src), []), "-c", src, "-o", obj]
     if src.endswith(".cpp"):
         cmd[1:1] = ["-x", "hip"]
     r = subprocess.run(cmd, capture_output=True, text=True)

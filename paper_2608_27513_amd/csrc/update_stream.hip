@@ -59,6 +59,11 @@ __device__ __forceinline__ void st8(u32x2 v, __amdgpu_buffer_rsrc_t r, int voff,
   __builtin_amdgcn_raw_buffer_store_b64(v, r, voff, soff, kCachePolicyNT);
 }
 
+// Operands of one tile as loaded by threads t < 128 (raw bf16 bits).
+struct OpsRegs {
+  uint32_t k, q, g, v, beta;
+};
+
 template <bool KDA>
 __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, const int ntiles,
                                                         const int tile_bytes) {
@@ -68,7 +73,6 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
   __shared__ float dsh[D];
   __shared__ float4 opr[2][D];  // per tile parity, row r: (k~_r, q~_r, a~_r, v_r)
   __shared__ float opsc[2][4];  // per parity: beta, alpha (GDN), two partial sums of q~ . k~
-  __shared__ int next_slot;     // pool slot of the tile after the staged one
 
   const int t = threadIdx.x;
   const int cg = t % TPR, rg = t / TPR, col0 = cg * CPT;
@@ -81,8 +85,11 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
   const int lo0 = k_hi * D * 2;
   const int meta0 = lo0 + (D - k_hi) * D;
   const int o_esize = p.o_bf16 ? 2 : 4;
+  // slot ids are read-only here: scalar loads through the constant address space
+  const __attribute__((address_space(4))) int32_t* slots =
+      (const __attribute__((address_space(4))) int32_t*)p.slot_idx;
 
-  // byte offsets of this thread's row slices inside a tile (same for every
+  // Byte offsets of this thread's row slices inside a tile (same for every
   // tile). Row slot 0 always loads 16 bytes at off_b0: the second half of a
   // bf16 row, or the (s, z) pair of its low row followed by the next row's.
   // Rows 1..3 (always low) sit at off_a1 + (i-1) * 32 rows of codes and
@@ -98,38 +105,33 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
   const int st_o = t >= D ? (t - D) * o_esize : kDrop;
   const int my_u = (t < D && p.perm) ? (static_cast<int>(p.perm[h * D + t]) & (D - 1)) : t;
 
-  int tau = blockIdx.x;
-  if (tau >= ntiles) return;
+  if (static_cast<int>(blockIdx.x) >= ntiles) return;
 
-  // ---- operand staging (threads t < D, i.e. waves 0 and 1) ----------------
-  uint32_t ok = 0, oq = 0, og = 0, ov = 0, obeta = 0, og0 = 0;
-  int oslot = -1;
-  auto issue_ops = [&](int tau_) {  // operands of tile tau_, slot of tile tau_ + G
+  // ---- operand staging: threads t < D (waves 0 and 1) gather one tile row
+  auto issue_ops = [&](OpsRegs& r, int tau_) {
     if (t < D) {
       const int b_ = tau_ / HV;
       const size_t bh = static_cast<size_t>(b_) * HV + h;
       const size_t kq = (static_cast<size_t>(b_) * p.HK + hk) * D;
-      ok = p.k[kq + my_u];
-      oq = p.q[kq + my_u];
-      if (KDA) og = p.g[bh * D + my_u];
-      else og0 = p.g[bh];
-      ov = p.v[bh * D + t];
-      obeta = p.beta[bh];
-      oslot = tau_ + G < ntiles ? p.slot_idx[(tau_ + G) / HV] : -1;
+      r.k = p.k[kq + my_u];
+      r.q = p.q[kq + my_u];
+      r.g = KDA ? p.g[bh * D + my_u] : p.g[bh];
+      r.v = p.v[bh * D + t];
+      r.beta = p.beta[bh];
     }
   };
-  auto publish_ops = [&](int par) {
+  auto publish_ops = [&](const OpsRegs& r, int par) {
     if (t < D) {
-      const float kf = bf16_to_f32(static_cast<uint16_t>(ok));
-      const float qf = bf16_to_f32(static_cast<uint16_t>(oq));
-      const float af = KDA ? __expf(bf16_to_f32(static_cast<uint16_t>(og))) : 1.0f;
-      opr[par][t] = make_float4(kf, qf, af, bf16_to_f32(static_cast<uint16_t>(ov)));
+      const float kf = bf16_to_f32(static_cast<uint16_t>(r.k));
+      const float qf = bf16_to_f32(static_cast<uint16_t>(r.q));
+      const float gf = bf16_to_f32(static_cast<uint16_t>(r.g));
+      opr[par][t] = make_float4(kf, qf, KDA ? __expf(gf) : 1.0f,
+                                bf16_to_f32(static_cast<uint16_t>(r.v)));
       const float kq = wave_sum_dpp(kf * qf);
       if ((t & 63) == 0) opsc[par][2 + (t >> 6)] = kq;
       if (t == 0) {
-        opsc[par][0] = bf16_to_f32(static_cast<uint16_t>(obeta));
-        opsc[par][1] = KDA ? 1.0f : __expf(bf16_to_f32(static_cast<uint16_t>(og0)));
-        next_slot = oslot;
+        opsc[par][0] = bf16_to_f32(static_cast<uint16_t>(r.beta));
+        opsc[par][1] = KDA ? 1.0f : __expf(gf);
       }
     }
   };
@@ -152,25 +154,31 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
       rb[i] = ld8(r, off_b1, (i - 1) * kStepB);
     }
   };
+  auto slot_of = [&](int tau_) { return tau_ < ntiles ? slots[tau_ / HV] : -1; };
 
-  // ---- prologue -------------------------------------------------------------
-  int slot_cur = p.slot_idx[tau / HV];
+  // ---- one tile: ops of tile tau are in opr[par]; ops of tau + G are in
+  // flight in `pub`; the ops of tau + 2G are loaded into `nxt`
+  int tau = blockIdx.x;
+  int slot_cur = slot_of(tau);
+  int slot_next = slot_of(tau + G);
   __amdgpu_buffer_rsrc_t rs_cur = make_rsrc(slot_cur);
-  issue_ops(tau);
-  issue_raw(rs_cur);
-  publish_ops(0);
-  // settle the first tile's bytes here, so that the loop head only waits as
-  // far as the stores issued after each prefetch
-  asm volatile("" ::"v"(ra[0]), "v"(rb0), "v"(ra[1]), "v"(rb[1]), "v"(ra[2]), "v"(rb[2]),
-               "v"(ra[3]), "v"(rb[3]));
-  lds_barrier();
+  bool done = false;
 
-  for (int par = 0;; par ^= 1) {
+  int turn = static_cast<int>(blockIdx.x) / HV;
+  auto tile = [&](int par, OpsRegs& pub, OpsRegs& nxt) {
+    // The wave arbiter favours older waves, so the workgroups sharing a CU
+    // would otherwise progress at very different rates and the last ones
+    // would finish alone. Rotating the in-kernel wave priority every tile
+    // lets them take turns.
+    switch (turn++ % 3) {
+      case 0: __builtin_amdgcn_s_setprio(0); break;
+      case 1: __builtin_amdgcn_s_setprio(1); break;
+      default: __builtin_amdgcn_s_setprio(2); break;
+    }
     const bool live = slot_cur >= 0 && slot_cur < p.num_slots;
     // -- operands of this tile; dequantize and decay: S_bar = Lambda S
     float kk[RPT], qq[RPT], aa[RPT];
     const float alpha = opsc[par][1];
-    const int slot_next = __builtin_amdgcn_readfirstlane(next_slot);
 #pragma unroll
     for (int i = 0; i < RPT; ++i) {
       const float4 o4 = opr[par][rg + RG * i];
@@ -178,7 +186,6 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
       qq[i] = o4.y;
       aa[i] = KDA ? o4.z : alpha;
     }
-
     float x[RPT][CPT];
     if (hi0) {
 #pragma unroll
@@ -211,9 +218,8 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
         x[i][4 * j + 3] = fmaf(A, ubyte<3>(ra[i][j]), B0);
       }
     }
-
-    // the dequantized tile must exist before the next tile's loads are issued,
-    // so that the waits for this tile's bytes precede the prefetch
+    // the dequantized tile must exist before the next tile's loads are
+    // issued, so that the waits for this tile's bytes precede the prefetch
 #pragma unroll
     for (int i = 0; i < RPT; ++i)
       asm volatile("" ::"v"(x[i][0]), "v"(x[i][1]), "v"(x[i][2]), "v"(x[i][3]), "v"(x[i][4]),
@@ -221,14 +227,16 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
                    "v"(x[i][10]), "v"(x[i][11]), "v"(x[i][12]), "v"(x[i][13]), "v"(x[i][14]),
                    "v"(x[i][15]));
 
-    // -- prefetch the next tile: operands first, then the packed bytes
+    // -- prefetch: packed bytes of the next tile, operands two tiles ahead
     const int tau_n = tau + G;
     const bool has_next = tau_n < ntiles;
     __amdgpu_buffer_rsrc_t rs_next = rs_cur;
+    int slot_nn = -1;
     if (has_next) {
-      issue_ops(tau_n);
       rs_next = make_rsrc(slot_next);
       issue_raw(rs_next);
+      if (tau_n + G < ntiles) issue_ops(nxt, tau_n + G);
+      slot_nn = slot_of(tau_n + G);
     }
     __builtin_amdgcn_sched_barrier(0);
 
@@ -265,7 +273,7 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
       tot = (acc[0] + acc[1]) + (acc[2] + acc[3]);
     }
     if (t < D) dsh[t] = opr[par][t].w - tot;  // delta = v - S_bar^T k~
-    if (has_next) publish_ops(par ^ 1);       // next tile's operands (waits only for them)
+    if (has_next) publish_ops(pub, par ^ 1);  // loaded a whole tile ago
     lds_barrier();
     const float beta = opsc[par][0], qk = opsc[par][2] + opsc[par][3];
 
@@ -342,10 +350,31 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
       st8(wm[i], rs_cur, st_m1, (i - 1) * kStepB);
     }
 
-    if (!has_next) break;
+    done = !has_next;
     tau = tau_n;
     slot_cur = slot_next;
+    slot_next = slot_nn;
     rs_cur = rs_next;
+  };
+
+  // ---- prologue: tile 0's bytes and operands, tile 1's operands in flight
+  OpsRegs ops_a = {0u, 0u, 0u, 0u, 0u}, ops_b = {0u, 0u, 0u, 0u, 0u};
+  issue_ops(ops_a, tau);
+  issue_raw(rs_cur);
+  if (tau + G < ntiles) issue_ops(ops_b, tau + G);
+  publish_ops(ops_a, 0);
+  // settle the first tile's bytes here, so that the loop head only waits as
+  // far as the stores issued after each prefetch
+  asm volatile("" ::"v"(ra[0]), "v"(rb0), "v"(ra[1]), "v"(rb[1]), "v"(ra[2]), "v"(rb[2]),
+               "v"(ra[3]), "v"(rb[3]));
+  lds_barrier();
+
+  // two tiles per trip so the operand register sets alternate without copies
+  for (;;) {
+    tile(0, ops_b, ops_a);
+    if (done) break;
+    tile(1, ops_a, ops_b);
+    if (done) break;
   }
 }
 
