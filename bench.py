@@ -11,8 +11,11 @@ Timing: W untimed steps, then exactly K steps between two synchronisations
 (ms_per_step = wall time / K). The pool holds `--rotations` disjoint copies
 of the batch's slots and consecutive steps use different copies, so the
 state (158 MB per copy) is not served from the 256 MB last-level cache.
-A second pass records a HIP event pair around every launch on the launch
-stream; their mean is the kernel duration the roofline uses.
+Each copy holds the batch in consecutive slots, as a [B, HV, d, d] state
+would be; the same workload with the batch scattered over the whole pool
+in random order is reported beside it (`headline_random_slots`). A HIP
+event pair on the launch stream brackets the timed region; its duration
+over K is the kernel duration the roofline uses.
 
 Also reported: the FP32-state and uniform-INT8 kernels on the same workload,
 KDA decode (B = 256, 32 heads, per-channel decay, selection from a
@@ -48,6 +51,8 @@ def parse():
     ap.add_argument("--quick", action="store_true", help="headline only: no baselines, no CPU")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-multilayer", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration)")
     return ap.parse_args()
@@ -176,14 +181,19 @@ class Workload:
         self.step_inputs = [inputs.decode_inputs_device(gen, B, HK, HV, d, kda=kda, mu=self.mu)
                             for _ in range(4)]
 
-    def make_pool(self, kind: int, k_hi: int, rotations: int):
+    def make_pool(self, kind: int, k_hi: int, rotations: int, scattered: bool = False):
         """A pool with `rotations` disjoint slot sets, each packed with the
-        warm state (permuted by the selection)."""
+        warm state (permuted by the selection). Set r is slots r*B .. r*B+B-1
+        in order, or with `scattered` B slots drawn at random from the whole
+        pool, in random order."""
         torch, D = self.torch, self.D
         B, HV, d = self.B, self.HV, self.d
         layout = D.damp_layout_init(d, d, k_hi, kind)
         pool = D.Pool(layout, 1, B * rotations, HV)
-        order = torch.from_numpy(self.inputs.slot_order(7, B * rotations, B * rotations)).cuda()
+        if scattered:
+            order = torch.from_numpy(self.inputs.slot_order(7, B * rotations, B * rotations)).cuda()
+        else:
+            order = torch.arange(B * rotations, dtype=torch.int32, device="cuda")
         slot_sets = [order[r * B:(r + 1) * B].contiguous() for r in range(rotations)]
         for s in slot_sets:
             D.damp_state_pack(pool, 0, s, self.S, self.perm)
@@ -225,8 +235,8 @@ def time_steps(torch, calls, warmup: int, steps: int):
 
 
 def measure(torch, D, wl: Workload, kind: int, k_hi: int, rotations: int, warmup: int,
-            steps: int, o_dtype):
-    pool, sets, layout = wl.make_pool(kind, k_hi, rotations)
+            steps: int, o_dtype, scattered: bool = False):
+    pool, sets, layout = wl.make_pool(kind, k_hi, rotations, scattered)
     calls = wl.prepared(pool, sets, o_dtype)
     t = time_steps(torch, calls, warmup, steps)
     tb = D.damp_tile_bytes(layout)
@@ -244,6 +254,109 @@ def measure(torch, D, wl: Workload, kind: int, k_hi: int, rotations: int, warmup
     res["kernel_frac_peak"] = res["kernel_gbs"] / HBM_PEAK_GBS
     del pool, calls
     torch.cuda.empty_cache()
+    return res
+
+
+def sweep(torch, D, inputs, steps: int, log=print):
+    """B x high-precision rows x state layout, GDN (16 key heads) and KDA, 32
+    value heads, d = 128. States are random packed tiles (timing does not
+    depend on their values); pools span >= 1 GB so they are not cache
+    resident. Returns one record per point."""
+    out = []
+    d, HV = 128, 32
+    for kda in (False, True):
+        HK = HV if kda else 16
+        for B in (1, 16, 64, 256, 1024):
+            gen = torch.Generator(device="cuda")
+            gen.manual_seed(B)
+            mu = torch.from_numpy(inputs.kda_mu(1, HV, d)).cuda() if kda else None
+            x = inputs.decode_inputs_device(gen, B, HK, HV, d, kda=kda, mu=mu)
+            perm = torch.from_numpy(inputs.random_perms(B, HV, d)).cuda()
+            S = torch.randn((B, HV, d, d), generator=gen, device="cuda") * 0.1
+            o = torch.empty((B, HV, d), dtype=torch.bfloat16, device="cuda")
+            for kind, k_hi in ((D.DAMP_STATE_FP32, 0), (D.DAMP_STATE_MIXED, 0),
+                               (D.DAMP_STATE_MIXED, 8), (D.DAMP_STATE_MIXED, 16),
+                               (D.DAMP_STATE_MIXED, 32)):
+                layout = D.damp_layout_init(d, d, k_hi, kind)
+                tb = D.damp_tile_bytes(layout)
+                rot = max(1, min(16, -(-(1 << 30) // (tb * B * HV))))
+                pool = D.Pool(layout, 1, B * rot, HV)
+                sets = [torch.arange(r * B, (r + 1) * B, dtype=torch.int32, device="cuda")
+                        for r in range(rot)]
+                for sl in sets:
+                    D.damp_state_pack(pool, 0, sl, S, perm)
+                calls = [D.PreparedUpdate(kda, pool, 0, sl, x["q"], x["k"], x["v"], x["g"],
+                                          x["beta"], perm, 1.0, o) for sl in sets]
+                t = time_steps(torch, calls, 10, steps)
+                nbytes = algorithmic_bytes(tb, B, HK, HV, d, kda, 2)
+                out.append(dict(model="KDA" if kda else "GDN", B=B,
+                                layout="fp32" if kind == D.DAMP_STATE_FP32 else
+                                ("int8" if k_hi == 0 else "mixed"), k_hi=k_hi,
+                                kernel_us=round(1e6 * t["mean_launch_s"], 2),
+                                GBs=round(nbytes / t["mean_launch_s"] / 1e9, 1)))
+                del pool, calls
+            del S
+            torch.cuda.empty_cache()
+        log(f"  sweep {'KDA' if kda else 'GDN'} done")
+    return out
+
+
+def multilayer(torch, D, inputs, steps: int, log=print):
+    """48 GDN layers over one slot-indexed pool of 512 requests, 384 of them
+    active in random non-contiguous order (32 value / 16 key heads, d = 128,
+    16 BF16 rows). One decode step = 48 launches, captured once as a HIP
+    graph and replayed; two input sets alternate between steps. Reports the
+    per-step latency for the mixed pool and the FP32-state pool."""
+    L, slots_total, B, HK, HV, d, k_hi = 48, 512, 384, 16, 32, 128, 16
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(5)
+    active = torch.from_numpy(inputs.slot_order(5, slots_total, B)).cuda()
+    perms = [torch.from_numpy(inputs.random_perms(100 + l, HV, d)).cuda() for l in range(L)]
+    sets = [[inputs.decode_inputs_device(gen, B, HK, HV, d) for _ in range(L)] for _ in range(2)]
+    o = torch.empty((B, HV, d), dtype=torch.bfloat16, device="cuda")
+    res = {}
+    for name, kind, kh in (("mixed", D.DAMP_STATE_MIXED, k_hi), ("fp32_state", D.DAMP_STATE_FP32, 0)):
+        layout = D.damp_layout_init(d, d, kh, kind)
+        pool = D.Pool(layout, L, slots_total, HV)
+        for l in range(L):  # random warm states for the active slots of every layer
+            S = torch.randn((B, HV, d, d), generator=gen, device="cuda") * 0.1
+            D.damp_state_pack(pool, l, active, S, perms[l])
+            del S
+        def step(s_):
+            for l, x in enumerate(sets[s_]):  # launches go to the current stream
+                D.damp_state_update_gdn(pool, l, active, x["q"], x["k"], x["v"], x["g"],
+                                        x["beta"], perm=perms[l], o=o)
+
+        graphs = []
+        for s_ in range(2):
+            step(s_)  # warm the launch path before capture
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                step(s_)
+            graphs.append((g, s_))
+        for i in range(4):
+            graphs[i % 2][0].replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        e0.record()
+        for i in range(steps):
+            graphs[i % 2][0].replay()
+        e1.record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        step_s = e0.elapsed_time(e1) * 1e-3 / steps
+        nbytes = L * algorithmic_bytes(D.damp_tile_bytes(layout), B, HK, HV, d, False, 2)
+        res[name] = dict(ms_per_step=round(1e3 * step_s, 4), wall_ms_per_step=round(1e3 * wall / steps, 4),
+                         GBs=round(nbytes / step_s / 1e9, 1), pool_bytes=pool.buffer.numel(),
+                         launches_per_step=L)
+        del graphs, pool
+        torch.cuda.empty_cache()
+        log(f"  48-layer step ({name}): {res[name]['ms_per_step']:.3f} ms")
+    res["speedup_vs_fp32_state"] = round(res["fp32_state"]["ms_per_step"] / res["mixed"]["ms_per_step"], 3)
+    res["config"] = dict(layers=L, pool_slots=slots_total, active=B, HK=HK, HV=HV, d=d, k_hi=k_hi,
+                         steps=steps)
     return res
 
 
@@ -307,6 +420,11 @@ def main():
         f"{head['kernel_gbs']:.0f} GB/s ({100 * head['kernel_frac_peak']:.1f}% of peak)")
     extra = {}
     if not args.quick:
+        scat = measure(torch, D, gdn, D.DAMP_STATE_MIXED, k_hi, args.rotations, args.warmup,
+                       args.steps, torch.bfloat16, scattered=True)
+        log(f"  mixed, slots scattered over the pool: kernel {scat['kernel_us']:.1f} us, "
+            f"{scat['kernel_gbs']:.0f} GB/s")
+        extra["headline_random_slots"] = scat
         rot_fp = max(2, args.rotations // 2)
         fp = measure(torch, D, gdn, D.DAMP_STATE_FP32, 0, rot_fp, args.warmup, args.steps,
                      torch.bfloat16)
@@ -333,6 +451,11 @@ def main():
         del kda
         torch.cuda.empty_cache()
 
+        if not args.no_sweep:
+            extra["sweep"] = sweep(torch, D, inputs, 50, log=log)
+        if not args.no_multilayer:
+            extra["multilayer_48"] = multilayer(torch, D, inputs, 64, log=log)
+
     cpu = None
     if not args.quick and not args.no_cpu:
         cpu = cpu_baseline(args.cpu_seconds, log=log)
@@ -357,6 +480,7 @@ def main():
                                "d_k=d_v=128, 16 of 128 key channels BF16, rest INT8 rows "
                                "with fp32 (s, z); bf16 q/k/v/g/beta in, bf16 o out",
                    "global_batch": B, "layers": 1, "rotations": args.rotations,
+                   "slots": "consecutive per rotation",
                    "bytes_per_step": head["bytes_per_step"]},
         "roofline": {"bound": "hbm", "achieved": round(head["kernel_gbs"], 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",

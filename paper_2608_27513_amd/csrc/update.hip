@@ -251,7 +251,9 @@ damp_status update(bool kda, const damp_pool* pool, int32_t layer, const int32_t
   p.o_bf16 = o_dtype == DAMP_DT_BF16;
   const int D = pool->layout.d_k;
   hipStream_t s = as_stream(stream);
-  if (pool->layout.kind == DAMP_STATE_MIXED && D == 128 && p.k_hi <= 32) {
+  // the persistent kernel numbers the B * HV tiles with 32-bit integers
+  const bool tiles_fit = static_cast<int64_t>(B) * p.HV <= INT32_MAX;
+  if (pool->layout.kind == DAMP_STATE_MIXED && D == 128 && p.k_hi <= 32 && tiles_fit) {
     if (!launch_stream128(kda, p, B, s))
       return fail(DAMP_ERR_HIP, "%s: occupancy query failed", name);
     return check_launch(name);
