@@ -59,6 +59,29 @@ __device__ __forceinline__ void st8(u32x2 v, __amdgpu_buffer_rsrc_t r, int voff,
   __builtin_amdgcn_raw_buffer_store_b64(v, r, voff, soff, kCachePolicyNT);
 }
 
+// Cross-lane sums used by the key-axis reduction. fold32(a, b) returns, on
+// lanes 0..31, a summed over the lane pair (L, L + 32) and, on lanes 32..63,
+// b summed over the pair; fold16 does the same for lane pairs (L, L ^ 16)
+// (even 16-lane rows keep a, odd rows keep b) and fold8 for (L, L ^ 8)
+// (lanes with bit 3 clear keep a). Each halves the number of live partial
+// sums while it halves the number of lanes holding a partial of one value.
+__device__ __forceinline__ float fold32(float a, float b) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float fold16(float a, float b) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(a), __float_as_uint(b), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float fold8(float a, float b, bool upper) {
+  const float send = upper ? a : b, keep = upper ? b : a;
+  // row_ror:8 reads lane L ^ 8 of the same 16-lane row
+  return keep + __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(send), 0x128, 0xf, 0xf,
+                                                        true));
+}
+
 // Operands of one tile as loaded by threads t < 128 (raw bf16 bits).
 struct OpsRegs {
   uint32_t k, q, g, v, beta;
@@ -69,17 +92,28 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
                                                         const int tile_bytes) {
   constexpr int D = 128, RG = 32, RPT = 4, CPT = 16, TPR = 8;
   constexpr int kDrop = 0x40000000;  // buffer offset past any tile: the store is dropped
-  __shared__ float red[RG][2 * D + 4];
-  __shared__ float dsh[D];
-  __shared__ float4 opr[2][D];  // per tile parity, row r: (k~_r, q~_r, a~_r, v_r)
-  __shared__ float opsc[2][4];  // per parity: beta, alpha (GDN), two partial sums of q~ . k~
+  // Per-wave partial column sums of k~ . S_bar (index c) and q~ . S_bar
+  // (index D + c), in the slot order described at the reduction below;
+  // double-buffered by tile parity.
+  __shared__ float4 part[2][4][2 * D / 4];
+  __shared__ float4 dwv[4][D / 4];  // per wave: delta, same slot order
+  // Operands, triple-buffered: row r (k~_r, q~_r, a~_r), column c v_c, and
+  // the scalars beta, alpha (GDN) and two partial sums of q~ . k~.
+  __shared__ float4 opr[3][D];
+  __shared__ float vsh[3][D];
+  __shared__ float opsc[3][4];
 
   const int t = threadIdx.x;
+  const int lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int cg = t % TPR, rg = t / TPR, col0 = cg * CPT;
+  const bool b3 = (lane & 8) != 0, b4 = (lane & 16) != 0, b5 = (lane & 32) != 0;
   const int HV = p.HV;
   const int G = gridDim.x;  // a multiple of HV
   const int h = blockIdx.x % HV;
   const int hk = h / (HV / p.HK);
+  const int B = ntiles / HV;
+  const int b_step = G / HV;
   const int k_hi = p.k_hi;
   const bool hi0 = rg < k_hi;  // row slot 0 of this thread is in the bf16 tier
   const int lo0 = k_hi * D * 2;
@@ -100,17 +134,28 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
   const int off_b1 = meta0 + (rg + RG - k_hi) * 8;
   constexpr int kStepA = RG * D, kStepB = RG * 8;
   const int st_b0 = hi0 ? off_b0 : kDrop;                    // second bf16 half
+  // row slot 0 of every lane of this wave is low (no bf16 second half to
+  // store) or high (no metadata to store): those stores are skipped
+  const bool wave_lo = 8 * wave >= k_hi, wave_hi = 8 * wave + 8 <= k_hi;
   const int st_m0 = (cg == 0 && !hi0) ? off_b0 : kDrop;      // (s, z) of row slot 0
   const int st_m1 = cg == 0 ? off_b1 : kDrop;                // (s, z) of rows 1..3
-  const int st_o = t >= D ? (t - D) * o_esize : kDrop;
   const int my_u = (t < D && p.perm) ? (static_cast<int>(p.perm[h * D + t]) & (D - 1)) : t;
+
+  // Reduction slots: after the in-wave folds, lane (cg, b3, b4, b5) holds the
+  // wave's partial sums of kind b5 (0: k~, 1: q~) for the columns
+  // col0 + 8 hf + 4 b4 + 2 b3 + i, hf, i in {0, 1}; they occupy the four
+  // consecutive floats from slot s0 (position 2 hf + i).
+  const int c_pair = col0 + 4 * (b4 ? 1 : 0) + 2 * (b3 ? 1 : 0);  // first column of hf = 0
+  const int s0q = (b5 ? D / 4 : 0) + cg * 4 + 2 * (b4 ? 1 : 0) + (b3 ? 1 : 0);  // float4 index
+  const int dq = cg * 4 + 2 * (b4 ? 1 : 0) + (b3 ? 1 : 0);  // float4 index of delta in dwv
+  // o: the q-kind lanes of wave 3 write columns c_pair + {0, 1} and c_pair + 8 + {0, 1}
+  const int st_o = (wave == 3 && b5) ? c_pair * o_esize : kDrop;
 
   if (static_cast<int>(blockIdx.x) >= ntiles) return;
 
   // ---- operand staging: threads t < D (waves 0 and 1) gather one tile row
-  auto issue_ops = [&](OpsRegs& r, int tau_) {
+  auto issue_ops = [&](OpsRegs& r, int b_) {
     if (t < D) {
-      const int b_ = tau_ / HV;
       const size_t bh = static_cast<size_t>(b_) * HV + h;
       const size_t kq = (static_cast<size_t>(b_) * p.HK + hk) * D;
       r.k = p.k[kq + my_u];
@@ -120,18 +165,18 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
       r.beta = p.beta[bh];
     }
   };
-  auto publish_ops = [&](const OpsRegs& r, int par) {
+  auto publish_ops = [&](const OpsRegs& r, int buf) {
     if (t < D) {
       const float kf = bf16_to_f32(static_cast<uint16_t>(r.k));
       const float qf = bf16_to_f32(static_cast<uint16_t>(r.q));
       const float gf = bf16_to_f32(static_cast<uint16_t>(r.g));
-      opr[par][t] = make_float4(kf, qf, KDA ? __expf(gf) : 1.0f,
-                                bf16_to_f32(static_cast<uint16_t>(r.v)));
+      opr[buf][t] = make_float4(kf, qf, KDA ? __expf(gf) : 1.0f, 0.0f);
+      vsh[buf][t] = bf16_to_f32(static_cast<uint16_t>(r.v));
       const float kq = wave_sum_dpp(kf * qf);
-      if ((t & 63) == 0) opsc[par][2 + (t >> 6)] = kq;
+      if ((t & 63) == 0) opsc[buf][2 + (t >> 6)] = kq;
       if (t == 0) {
-        opsc[par][0] = bf16_to_f32(static_cast<uint16_t>(r.beta));
-        opsc[par][1] = KDA ? 1.0f : __expf(gf);
+        opsc[buf][0] = bf16_to_f32(static_cast<uint16_t>(r.beta));
+        opsc[buf][1] = KDA ? 1.0f : __expf(gf);
       }
     }
   };
@@ -154,34 +199,38 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
       rb[i] = ld8(r, off_b1, (i - 1) * kStepB);
     }
   };
-  auto slot_of = [&](int tau_) { return tau_ < ntiles ? slots[tau_ / HV] : -1; };
+  auto slot_of = [&](int b_) { return b_ < B ? slots[b_] : -1; };
 
-  // ---- one tile: ops of tile tau are in opr[par]; ops of tau + G are in
-  // flight in `pub`; the ops of tau + 2G are loaded into `nxt`
-  int tau = blockIdx.x;
-  int slot_cur = slot_of(tau);
-  int slot_next = slot_of(tau + G);
+  // ---- one tile (request b): its operands are in buffer `buf`; those of the
+  // next tile are in flight in `pub` and are published into buffer `buf_n`;
+  // those two tiles ahead are loaded into `nxt`
+  int b = blockIdx.x / HV;
+  int slot_cur = slot_of(b);
+  int slot_next = slot_of(b + b_step);
   __amdgpu_buffer_rsrc_t rs_cur = make_rsrc(slot_cur);
   bool done = false;
+  int buf = 0, pb = 0;
+  int turn = b % 3;
 
-  int turn = static_cast<int>(blockIdx.x) / HV;
-  auto tile = [&](int par, OpsRegs& pub, OpsRegs& nxt) {
+  auto tile = [&](OpsRegs& pub, OpsRegs& nxt) {
     // The wave arbiter favours older waves, so the workgroups sharing a CU
     // would otherwise progress at very different rates and the last ones
     // would finish alone. Rotating the in-kernel wave priority every tile
     // lets them take turns.
-    switch (turn++ % 3) {
+    switch (turn) {
       case 0: __builtin_amdgcn_s_setprio(0); break;
       case 1: __builtin_amdgcn_s_setprio(1); break;
       default: __builtin_amdgcn_s_setprio(2); break;
     }
+    turn = turn == 2 ? 0 : turn + 1;
+    const int buf_n = buf == 2 ? 0 : buf + 1;
     const bool live = slot_cur >= 0 && slot_cur < p.num_slots;
     // -- operands of this tile; dequantize and decay: S_bar = Lambda S
     float kk[RPT], qq[RPT], aa[RPT];
-    const float alpha = opsc[par][1];
+    const float alpha = opsc[buf][1];
 #pragma unroll
     for (int i = 0; i < RPT; ++i) {
-      const float4 o4 = opr[par][rg + RG * i];
+      const float4 o4 = opr[buf][rg + RG * i];
       kk[i] = o4.x;
       qq[i] = o4.y;
       aa[i] = KDA ? o4.z : alpha;
@@ -228,81 +277,117 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
                    "v"(x[i][15]));
 
     // -- prefetch: packed bytes of the next tile, operands two tiles ahead
-    const int tau_n = tau + G;
-    const bool has_next = tau_n < ntiles;
+    const int b_n = b + b_step;
+    const bool has_next = b_n < B;
     __amdgpu_buffer_rsrc_t rs_next = rs_cur;
     int slot_nn = -1;
     if (has_next) {
       rs_next = make_rsrc(slot_next);
       issue_raw(rs_next);
-      if (tau_n + G < ntiles) issue_ops(nxt, tau_n + G);
-      slot_nn = slot_of(tau_n + G);
+      if (b_n + b_step < B) issue_ops(nxt, b_n + b_step);
+      slot_nn = slot_of(b_n + b_step);
     }
     __builtin_amdgcn_sched_barrier(0);
 
-    // -- partial key and query read-outs, reduced over row groups in LDS
+    // -- partial key and query read-outs over this thread's 4 rows, folded
+    // over the 8 row groups of the wave (lane bits 5, 4, 3), so each lane
+    // keeps 4 of the wave's 256 partial sums
+    float r3[4];
 #pragma unroll
-    for (int half = 0; half < 2; ++half) {
+    for (int hf = 0; hf < 2; ++hf) {
       float pw[8], pq[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        pw[j] = kk[0] * x[0][8 * half + j];
-        pq[j] = qq[0] * x[0][8 * half + j];
+        pw[j] = kk[0] * x[0][8 * hf + j];
+        pq[j] = qq[0] * x[0][8 * hf + j];
       }
 #pragma unroll
       for (int i = 1; i < RPT; ++i)
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          pw[j] = fmaf(kk[i], x[i][8 * half + j], pw[j]);
-          pq[j] = fmaf(qq[i], x[i][8 * half + j], pq[j]);
+          pw[j] = fmaf(kk[i], x[i][8 * hf + j], pw[j]);
+          pq[j] = fmaf(qq[i], x[i][8 * hf + j], pq[j]);
         }
-      float* rw = &red[rg][col0 + 8 * half];
-      *reinterpret_cast<float4*>(rw) = make_float4(pw[0], pw[1], pw[2], pw[3]);
-      *reinterpret_cast<float4*>(rw + 4) = make_float4(pw[4], pw[5], pw[6], pw[7]);
-      *reinterpret_cast<float4*>(rw + D) = make_float4(pq[0], pq[1], pq[2], pq[3]);
-      *reinterpret_cast<float4*>(rw + D + 4) = make_float4(pq[4], pq[5], pq[6], pq[7]);
-    }
-    lds_barrier();
-
-    // -- column totals: w = S_bar^T k~ (t < D), S_bar^T q~ (t >= D)
-    float tot;
-    {
-      float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      float r1[8], r2[4];
 #pragma unroll
-      for (int g = 0; g < RG; ++g) acc[g & 3] += red[g][t];
-      tot = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+      for (int j = 0; j < 8; ++j) r1[j] = fold32(pw[j], pq[j]);  // kind b5, column 8 hf + j
+#pragma unroll
+      for (int j = 0; j < 4; ++j) r2[j] = fold16(r1[j], r1[j + 4]);  // column 8 hf + 4 b4 + j
+#pragma unroll
+      for (int j = 0; j < 2; ++j) r3[2 * hf + j] = fold8(r2[j], r2[j + 2], b3);
     }
-    if (t < D) dsh[t] = opr[par][t].w - tot;  // delta = v - S_bar^T k~
-    if (has_next) publish_ops(pub, par ^ 1);  // loaded a whole tile ago
+    part[pb][wave][s0q] = make_float4(r3[0], r3[1], r3[2], r3[3]);
+    if (has_next) publish_ops(pub, buf_n);  // loaded a whole tile ago
     lds_barrier();
-    const float beta = opsc[par][0], qk = opsc[par][2] + opsc[par][3];
 
-    // -- output o = scale (S_bar^T q~ + beta (q~.k~) delta), written by t >= D
+    // -- column totals of this lane's 4 slots over the 4 waves; delta = v -
+    // S_bar^T k~ on the k lanes; one swap gives every lane delta and the
+    // q total of its 4 columns
+    float tq[4], dd[4];
     {
-      const float oval = live ? p.scale * fmaf(beta * qk, dsh[t & (D - 1)], tot) : 0.0f;
+      const float4 p0 = part[pb][0][s0q], p1 = part[pb][1][s0q];
+      const float4 p2 = part[pb][2][s0q], p3 = part[pb][3][s0q];
+      const float tot[4] = {(p0.x + p1.x) + (p2.x + p3.x), (p0.y + p1.y) + (p2.y + p3.y),
+                            (p0.z + p1.z) + (p2.z + p3.z), (p0.w + p1.w) + (p2.w + p3.w)};
+      const float2 v0 = *reinterpret_cast<const float2*>(&vsh[buf][c_pair]);
+      const float2 v1 = *reinterpret_cast<const float2*>(&vsh[buf][c_pair + 8]);
+      const float vv[4] = {v0.x, v0.y, v1.x, v1.y};
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const float val = b5 ? tot[m] : vv[m] - tot[m];
+        const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(val),
+                                                        __float_as_uint(val), false, false);
+        dd[m] = __uint_as_float(r[0]);
+        tq[m] = __uint_as_float(r[1]);
+      }
+    }
+    const float beta = opsc[buf][0], qk = opsc[buf][2] + opsc[buf][3];
+
+    // -- output o = scale (S_bar^T q~ + beta (q~.k~) delta), written by the
+    // q lanes of wave 3
+    {
+      float ov[4];
+#pragma unroll
+      for (int m = 0; m < 4; ++m) ov[m] = live ? p.scale * fmaf(beta * qk, dd[m], tq[m]) : 0.0f;
       uint8_t* obase = static_cast<uint8_t*>(p.o) +
-                       (static_cast<size_t>(tau / HV) * HV + h) * D * o_esize;
+                       (static_cast<size_t>(b) * HV + h) * D * o_esize;
       const __amdgpu_buffer_rsrc_t ro =
           __builtin_amdgcn_make_buffer_rsrc(obase, 0, D * o_esize, kBufferConfig);
-      if (p.o_bf16)
-        __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16(oval), ro, st_o, 0, 0);
-      else
-        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(oval), ro, st_o, 0, 0);
+      if (wave != 3) {
+      } else if (p.o_bf16) {
+        __builtin_amdgcn_raw_buffer_store_b32(pack_bf16x2(ov[0], ov[1]), ro, st_o, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b32(pack_bf16x2(ov[2], ov[3]), ro, st_o, 16, 0);
+      } else {
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(ov[0]), __float_as_uint(ov[1])},
+                                              ro, st_o, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(ov[2]), __float_as_uint(ov[3])},
+                                              ro, st_o, 32, 0);
+      }
+    }
+
+    // -- delta of this lane's 16 columns, through the wave's own LDS slice
+    // (a wave's LDS accesses complete in order: no barrier)
+    if (!b5) dwv[wave][dq] = make_float4(dd[0], dd[1], dd[2], dd[3]);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+    float dl[CPT];
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4) {
+      // float4 q4 of the lane's block holds columns 4 (q4 >> 1) + 2 (q4 & 1)
+      // + {0, 1} and the same + 8
+      const float4 d4 = dwv[wave][cg * 4 + q4];
+      const int c = 4 * (q4 >> 1) + 2 * (q4 & 1);
+      dl[c] = d4.x;
+      dl[c + 1] = d4.y;
+      dl[c + 8] = d4.z;
+      dl[c + 9] = d4.w;
     }
 
     // -- rank-1 update S' = S_bar + beta k~ delta^T, re-encode, store in place
-    float dl[CPT];
-#pragma unroll
-    for (int j = 0; j < CPT; j += 4) {
-      const float4 d4 = *reinterpret_cast<const float4*>(&dsh[col0 + j]);
-      dl[j] = d4.x;
-      dl[j + 1] = d4.y;
-      dl[j + 2] = d4.z;
-      dl[j + 3] = d4.w;
-    }
 #pragma unroll
     for (int i = 0; i < RPT; ++i) {
-      const float bk = beta * opr[par][rg + RG * i].x;
+      const float bk = beta * kk[i];
 #pragma unroll
       for (int j = 0; j < CPT; ++j) x[i][j] = fmaf(bk, dl[j], x[i][j]);
     }
@@ -342,8 +427,8 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
     // every thread issues the same stores; lanes with nothing to write use
     // an offset past the buffer, which the hardware drops
     st16(wa[0], rs_cur, off_a0);
-    st16(wb0, rs_cur, st_b0);
-    st8(wm[0], rs_cur, st_m0);
+    if (!wave_lo) st16(wb0, rs_cur, st_b0);
+    if (!wave_hi) st8(wm[0], rs_cur, st_m0);
 #pragma unroll
     for (int i = 1; i < RPT; ++i) {
       st16(wa[i], rs_cur, off_a1, (i - 1) * kStepA);
@@ -351,7 +436,9 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
     }
 
     done = !has_next;
-    tau = tau_n;
+    b = b_n;
+    buf = buf_n;
+    pb ^= 1;
     slot_cur = slot_next;
     slot_next = slot_nn;
     rs_cur = rs_next;
@@ -359,9 +446,9 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
 
   // ---- prologue: tile 0's bytes and operands, tile 1's operands in flight
   OpsRegs ops_a = {0u, 0u, 0u, 0u, 0u}, ops_b = {0u, 0u, 0u, 0u, 0u};
-  issue_ops(ops_a, tau);
+  issue_ops(ops_a, b);
   issue_raw(rs_cur);
-  if (tau + G < ntiles) issue_ops(ops_b, tau + G);
+  if (b + b_step < B) issue_ops(ops_b, b + b_step);
   publish_ops(ops_a, 0);
   // settle the first tile's bytes here, so that the loop head only waits as
   // far as the stores issued after each prefetch
@@ -371,9 +458,9 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
 
   // two tiles per trip so the operand register sets alternate without copies
   for (;;) {
-    tile(0, ops_b, ops_a);
+    tile(ops_b, ops_a);
     if (done) break;
-    tile(1, ops_a, ops_b);
+    tile(ops_a, ops_b);
     if (done) break;
   }
 }
