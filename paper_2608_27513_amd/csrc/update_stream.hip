@@ -82,6 +82,15 @@ __device__ __forceinline__ float fold8(float a, float b, bool upper) {
                                                         true));
 }
 
+// Packed bytes of one tile as loaded by one thread: its four row slices
+// (16 bytes each), the second half of a bf16 row slot 0, and the (s, z) pair
+// of one row of its wave.
+struct RawSet {
+  u32x4 ra[4];
+  u32x4 rb0 = u32x4{0u, 0u, 0u, 0u};
+  u32x2 rm;
+};
+
 // Operands of one tile as loaded by threads t < 128 (raw bf16 bits).
 struct OpsRegs {
   uint32_t k, q, g, v, beta;
@@ -102,6 +111,9 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
   __shared__ float4 opr[3][D];
   __shared__ float vsh[3][D];
   __shared__ float opsc[3][4];
+  // Per wave: the (s, z) pairs of its 32 rows (8 wave + j + 32 i at index
+  // j + 8 i) of the next tile as loaded [0], and as re-encoded [1].
+  __shared__ float2 msh[4][2][32];
 
   const int t = threadIdx.x;
   const int lane = t & 63;
@@ -124,21 +136,25 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
       (const __attribute__((address_space(4))) int32_t*)p.slot_idx;
 
   // Byte offsets of this thread's row slices inside a tile (same for every
-  // tile). Row slot 0 always loads 16 bytes at off_b0: the second half of a
-  // bf16 row, or the (s, z) pair of its low row followed by the next row's.
-  // Rows 1..3 (always low) sit at off_a1 + (i-1) * 32 rows of codes and
-  // off_b1 + (i-1) * 32 pairs of metadata (scalar offsets).
+  // tile). Row slot 0 is a bf16 row (two 16-byte halves at off_a0 and
+  // off_b0) or a row of codes; rows 1..3 (always low) sit at off_a1 +
+  // (i-1) * 32 rows of codes (scalar offsets).
   const int off_a0 = hi0 ? (rg * D + col0) * 2 : lo0 + (rg - k_hi) * D + col0;
-  const int off_b0 = hi0 ? off_a0 + 16 : meta0 + (rg - k_hi) * 8;
+  const int off_b0 = off_a0 + 16;
   const int off_a1 = lo0 + (rg + RG - k_hi) * D + col0;
-  const int off_b1 = meta0 + (rg + RG - k_hi) * 8;
-  constexpr int kStepA = RG * D, kStepB = RG * 8;
+  constexpr int kStepA = RG * D;
   const int st_b0 = hi0 ? off_b0 : kDrop;                    // second bf16 half
-  // row slot 0 of every lane of this wave is low (no bf16 second half to
-  // store) or high (no metadata to store): those stores are skipped
-  const bool wave_lo = 8 * wave >= k_hi, wave_hi = 8 * wave + 8 <= k_hi;
-  const int st_m0 = (cg == 0 && !hi0) ? off_b0 : kDrop;      // (s, z) of row slot 0
-  const int st_m1 = cg == 0 ? off_b1 : kDrop;                // (s, z) of rows 1..3
+  // every lane of this wave has a low row slot 0 (no bf16 second half to
+  // load or store)
+  const bool wave_lo = 8 * wave >= k_hi;
+  // The metadata of the wave's 32 rows moves with one 8-byte access per
+  // lane: lane l < 32 handles row 8 wave + (l & 7) + 32 (l >> 3). Rows of
+  // the high tier have no metadata: their loads read bytes of the tile that
+  // are never used, their stores are dropped.
+  const int mrow = 8 * wave + (lane & 7) + 32 * (lane >> 3);
+  const int off_m = lane < 32 ? meta0 + (mrow - k_hi) * 8 : kDrop;
+  const int st_m = (lane < 32 && mrow >= k_hi) ? off_m : kDrop;
+  const int rgw = lane >> 3;  // row group within the wave
   const int my_u = (t < D && p.perm) ? (static_cast<int>(p.perm[h * D + t]) & (D - 1)) : t;
 
   // Reduction slots: after the in-wave folds, lane (cg, b3, b4, b5) holds the
@@ -188,31 +204,39 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
                     static_cast<size_t>(h) * p.tile_stride;
     return __builtin_amdgcn_make_buffer_rsrc(base, 0, live ? tile_bytes : 0, kBufferConfig);
   };
-  u32x4 ra[RPT], rb0;
-  u32x2 rb[RPT];
-  auto issue_raw = [&](__amdgpu_buffer_rsrc_t r) {
-    ra[0] = ld16(r, off_a0);
-    rb0 = ld16(r, off_b0);
+  auto issue_raw = [&](RawSet& rs, __amdgpu_buffer_rsrc_t r) {
+    rs.rm = ld8(r, off_m);
+    rs.ra[0] = ld16(r, off_a0);
+    if (!wave_lo) rs.rb0 = ld16(r, off_b0);
 #pragma unroll
-    for (int i = 1; i < RPT; ++i) {
-      ra[i] = ld16(r, off_a1, (i - 1) * kStepA);
-      rb[i] = ld8(r, off_b1, (i - 1) * kStepB);
-    }
+    for (int i = 1; i < RPT; ++i) rs.ra[i] = ld16(r, off_a1, (i - 1) * kStepA);
+  };
+  // metadata of a prefetched tile into the wave's LDS slice
+  auto stage_meta = [&](const RawSet& rs) {
+    if (lane < 32)
+      msh[wave][0][lane] = make_float2(__uint_as_float(rs.rm.x), __uint_as_float(rs.rm.y));
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
   };
   auto slot_of = [&](int b_) { return b_ < B ? slots[b_] : -1; };
 
-  // ---- one tile (request b): its operands are in buffer `buf`; those of the
-  // next tile are in flight in `pub` and are published into buffer `buf_n`;
-  // those two tiles ahead are loaded into `nxt`
+  // ---- one tile (request b): its packed bytes are in `cur` and those of the
+  // next tile in flight in `oth`; the bytes two tiles ahead are loaded into
+  // `cur` once it is dequantized. Its operands are in buffer `buf`; those of
+  // the next tile are in flight in `pub` and are published into buffer
+  // `buf_n`; those two tiles ahead are loaded into `nxt`.
   int b = blockIdx.x / HV;
   int slot_cur = slot_of(b);
-  int slot_next = slot_of(b + b_step);
+  int slot_n1 = slot_of(b + b_step);
+  int slot_n2 = slot_of(b + 2 * b_step);
   __amdgpu_buffer_rsrc_t rs_cur = make_rsrc(slot_cur);
+  __amdgpu_buffer_rsrc_t rs_n1 = make_rsrc(slot_n1);
   bool done = false;
   int buf = 0, pb = 0;
   int turn = b % 3;
 
-  auto tile = [&](OpsRegs& pub, OpsRegs& nxt) {
+  auto tile = [&](OpsRegs& pub, OpsRegs& nxt, RawSet& cur, RawSet& oth) {
     // The wave arbiter favours older waves, so the workgroups sharing a CU
     // would otherwise progress at very different rates and the last ones
     // would finish alone. Rotating the in-kernel wave priority every tile
@@ -235,18 +259,22 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
       qq[i] = o4.y;
       aa[i] = KDA ? o4.z : alpha;
     }
+    float2 sz[RPT];
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) sz[i] = msh[wave][0][rgw + 8 * i];
     float x[RPT][CPT];
+    const u32x4* ra = cur.ra;
     if (hi0) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         x[0][2 * j] = aa[0] * bf16_lo(ra[0][j]);
         x[0][2 * j + 1] = aa[0] * bf16_hi(ra[0][j]);
-        x[0][8 + 2 * j] = aa[0] * bf16_lo(rb0[j]);
-        x[0][8 + 2 * j + 1] = aa[0] * bf16_hi(rb0[j]);
+        x[0][8 + 2 * j] = aa[0] * bf16_lo(cur.rb0[j]);
+        x[0][8 + 2 * j + 1] = aa[0] * bf16_hi(cur.rb0[j]);
       }
     } else {
-      const float A = aa[0] * __uint_as_float(rb0.x);
-      const float B0 = -A * __uint_as_float(rb0.y);
+      const float A = aa[0] * sz[0].x;
+      const float B0 = -A * sz[0].y;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         x[0][4 * j + 0] = fmaf(A, ubyte<0>(ra[0][j]), B0);
@@ -257,8 +285,8 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
     }
 #pragma unroll
     for (int i = 1; i < RPT; ++i) {
-      const float A = aa[i] * __uint_as_float(rb[i].x);
-      const float B0 = -A * __uint_as_float(rb[i].y);
+      const float A = aa[i] * sz[i].x;
+      const float B0 = -A * sz[i].y;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         x[i][4 * j + 0] = fmaf(A, ubyte<0>(ra[i][j]), B0);
@@ -276,16 +304,16 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
                    "v"(x[i][10]), "v"(x[i][11]), "v"(x[i][12]), "v"(x[i][13]), "v"(x[i][14]),
                    "v"(x[i][15]));
 
-    // -- prefetch: packed bytes of the next tile, operands two tiles ahead
+    // -- prefetch: packed bytes and operands two tiles ahead
     const int b_n = b + b_step;
     const bool has_next = b_n < B;
-    __amdgpu_buffer_rsrc_t rs_next = rs_cur;
-    int slot_nn = -1;
-    if (has_next) {
-      rs_next = make_rsrc(slot_next);
-      issue_raw(rs_next);
-      if (b_n + b_step < B) issue_ops(nxt, b_n + b_step);
-      slot_nn = slot_of(b_n + b_step);
+    __amdgpu_buffer_rsrc_t rs_n2 = rs_n1;
+    int slot_n3 = -1;
+    if (b_n + b_step < B) {
+      rs_n2 = make_rsrc(slot_n2);
+      issue_raw(cur, rs_n2);
+      issue_ops(nxt, b_n + b_step);
+      slot_n3 = slot_of(b_n + 2 * b_step);
     }
     __builtin_amdgcn_sched_barrier(0);
 
@@ -392,7 +420,7 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
       for (int j = 0; j < CPT; ++j) x[i][j] = fmaf(bk, dl[j], x[i][j]);
     }
     u32x4 wa[RPT], wb0;
-    u32x2 wm[RPT];
+    float2 wm[RPT];
 #pragma unroll
     for (int i = 0; i < RPT; ++i) {
       if (i == 0 && hi0) {
@@ -401,7 +429,7 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
           wa[0][j] = pack_bf16x2(x[0][2 * j], x[0][2 * j + 1]);
           wb0[j] = pack_bf16x2(x[0][8 + 2 * j], x[0][8 + 2 * j + 1]);
         }
-        wm[0] = u32x2{0u, 0u};
+        wm[0] = make_float2(0.0f, 0.0f);
         continue;
       }
       float mn = x[i][0], mx = x[i][0];
@@ -421,46 +449,57 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
         c = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(x[i][4 * j + 2], inv, z), 2, c);
         wa[i][j] = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(x[i][4 * j + 3], inv, z), 3, c);
       }
-      wm[i] = u32x2{__float_as_uint(s), __float_as_uint(z)};
+      wm[i] = make_float2(s, z);
       if (i == 0) wb0 = u32x4{0u, 0u, 0u, 0u};
     }
-    // every thread issues the same stores; lanes with nothing to write use
-    // an offset past the buffer, which the hardware drops
+    // metadata of the wave's rows, gathered through its LDS slice
+    if (cg == 0) {
+#pragma unroll
+      for (int i = 0; i < RPT; ++i) msh[wave][1][rgw + 8 * i] = wm[i];
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+    const float2 mo = msh[wave][1][lane & 31];
+    // every lane issues the same stores; lanes with nothing to write use an
+    // offset past the buffer, which the hardware drops
     st16(wa[0], rs_cur, off_a0);
     if (!wave_lo) st16(wb0, rs_cur, st_b0);
-    if (!wave_hi) st8(wm[0], rs_cur, st_m0);
 #pragma unroll
-    for (int i = 1; i < RPT; ++i) {
-      st16(wa[i], rs_cur, off_a1, (i - 1) * kStepA);
-      st8(wm[i], rs_cur, st_m1, (i - 1) * kStepB);
-    }
+    for (int i = 1; i < RPT; ++i) st16(wa[i], rs_cur, off_a1, (i - 1) * kStepA);
+    st8(u32x2{__float_as_uint(mo.x), __float_as_uint(mo.y)}, rs_cur, st_m);
+    if (has_next) stage_meta(oth);
 
     done = !has_next;
     b = b_n;
     buf = buf_n;
     pb ^= 1;
-    slot_cur = slot_next;
-    slot_next = slot_nn;
-    rs_cur = rs_next;
+    slot_cur = slot_n1;
+    slot_n1 = slot_n2;
+    slot_n2 = slot_n3;
+    rs_cur = rs_n1;
+    rs_n1 = rs_n2;
   };
 
-  // ---- prologue: tile 0's bytes and operands, tile 1's operands in flight
+  // ---- prologue: the bytes of tiles 0 and 1 and the operands of tile 0 in
+  // flight, tile 1's operands in flight
   OpsRegs ops_a = {0u, 0u, 0u, 0u, 0u}, ops_b = {0u, 0u, 0u, 0u, 0u};
+  RawSet set_a, set_b;
   issue_ops(ops_a, b);
-  issue_raw(rs_cur);
-  if (b + b_step < B) issue_ops(ops_b, b + b_step);
+  issue_raw(set_a, rs_cur);
+  if (b + b_step < B) {
+    issue_raw(set_b, rs_n1);
+    issue_ops(ops_b, b + b_step);
+  }
   publish_ops(ops_a, 0);
-  // settle the first tile's bytes here, so that the loop head only waits as
-  // far as the stores issued after each prefetch
-  asm volatile("" ::"v"(ra[0]), "v"(rb0), "v"(ra[1]), "v"(rb[1]), "v"(ra[2]), "v"(rb[2]),
-               "v"(ra[3]), "v"(rb[3]));
+  stage_meta(set_a);
   lds_barrier();
 
   // two tiles per trip so the operand register sets alternate without copies
   for (;;) {
-    tile(ops_b, ops_a);
+    tile(ops_b, ops_a, set_a, set_b);
     if (done) break;
-    tile(ops_a, ops_b);
+    tile(ops_a, ops_b, set_b, set_a);
     if (done) break;
   }
 }
