@@ -23,6 +23,15 @@
  *    stored as fp32; the high tier is bf16 with round-to-nearest-even.
  *  - GDN's per-head decay is applied as the same a for every row, so KDA with
  *    a channel-constant g reproduces GDN exactly.
+ *  - The paper's own low tier (App. A.1 format table; Eq. (17)) is available
+ *    as a storage format: groups of 32 values along d_v with FP16 (s, z),
+ *    an optional normalized block-32 Hadamard transform applied before
+ *    quantization and again after reconstruction (it is its own inverse),
+ *    and an FP16 high tier. s follows Eq. (3) in fp32 and is stored in FP16
+ *    (round to nearest even, kept within the positive finite FP16 range);
+ *    z = round(-min / s) uses the stored s and is stored in FP16 (within the
+ *    finite range); codes use the stored (s, z), so the encoder and the
+ *    reconstruction agree.
  */
 #include <float.h>
 #include <math.h>
@@ -74,6 +83,63 @@ void orc_bf16_widen(const uint16_t* x, float* out, int64_t n) {
   for (int64_t i = 0; i < n; ++i) out[i] = orc_from_bf16(x[i]);
 }
 
+/* fp32 -> IEEE binary16 bits, round to nearest even (overflow -> inf). The
+ * rounding is done on exact double quotients: subnormals count in units of
+ * 2^-24, normals carry 11 significant bits. */
+static uint16_t orc_to_fp16(float f) {
+  uint32_t bits;
+  memcpy(&bits, &f, 4);
+  uint16_t sign = (uint16_t)((bits >> 16) & 0x8000u);
+  double a = fabs((double)f);
+  if (a != a) return (uint16_t)(sign | 0x7E00u);           /* NaN */
+  if (a >= 65520.0) return (uint16_t)(sign | 0x7C00u);     /* rounds past the largest */
+  if (a < 6.103515625e-05) {                               /* below 2^-14: subnormal */
+    double m = rint(a * 16777216.0);                        /* units of 2^-24 */
+    return (uint16_t)(sign | (uint16_t)m);                  /* 1024 is the first normal */
+  }
+  int e2;
+  frexp(a, &e2);                                            /* a = f 2^e2, f in [0.5, 1) */
+  int e = e2 - 1;                                           /* a in [2^e, 2^(e+1)) */
+  double m = rint(ldexp(a, 10 - e));                        /* in [1024, 2048] */
+  if (m == 2048.0) {
+    m = 1024.0;
+    e += 1;
+  }
+  if (e > 15) return (uint16_t)(sign | 0x7C00u);
+  return (uint16_t)(sign | (uint16_t)((e + 15) << 10) | (uint16_t)(m - 1024.0));
+}
+
+static float orc_from_fp16(uint16_t h) {
+  int e = (h >> 10) & 0x1F, m = h & 0x3FF;
+  double v;
+  if (e == 0) v = ldexp((double)m, -24);
+  else if (e == 31) v = m ? NAN : INFINITY;
+  else v = ldexp((double)(1024 + m), e - 25);
+  return (float)((h & 0x8000u) ? -v : v);
+}
+
+void orc_fp16_round(const float* x, uint16_t* out, int64_t n) {
+  for (int64_t i = 0; i < n; ++i) out[i] = orc_to_fp16(x[i]);
+}
+void orc_fp16_widen(const uint16_t* x, float* out, int64_t n) {
+  for (int64_t i = 0; i < n; ++i) out[i] = orc_from_fp16(x[i]);
+}
+
+/* Normalized block-32 Hadamard transform (App. A.1): y_i = 32^(-1/2)
+ * sum_j (-1)^popcount(i & j) x_j, summed in fp32 in ascending j. The matrix
+ * is symmetric and orthogonal, so the same call inverts it. */
+void orc_hadamard32(const float* x, float* y) {
+  const float norm = 0.17677669529663687f; /* 1 / sqrt(32) */
+  for (int i = 0; i < 32; ++i) {
+    float acc = 0.0f;
+    for (int j = 0; j < 32; ++j) {
+      if (__builtin_popcount((unsigned)(i & j)) & 1) acc = acc - x[j];
+      else acc = acc + x[j];
+    }
+    y[i] = acc * norm;
+  }
+}
+
 /* ------------------------------------------------- Eq. (3): one-row INT8 */
 
 /* Scale and zero point of a row (Eq. (3) with b = 8). */
@@ -112,12 +178,59 @@ void orc_dequant_row(const uint8_t* codes, int n, float s, float z, float* out) 
   for (int j = 0; j < n; ++j) out[j] = orc_decode(codes[j], s, z);
 }
 
+/* One group with FP16 metadata (App. A.1, integer formats): s from Eq. (3) in
+ * fp32, stored in FP16; z from the stored s, stored in FP16; codes from the
+ * stored pair. s and z are returned widened to fp32. */
+void orc_quant_group_fp16(const float* x, int n, uint8_t* codes, float* s_out, float* z_out) {
+  float s, z;
+  orc_quant_params(x, n, &s, &z);
+  float lo = x[0];
+  for (int j = 1; j < n; ++j)
+    if (x[j] < lo) lo = x[j];
+  float s16 = orc_from_fp16(orc_to_fp16(s));
+  if (!(s16 > 0.0f)) s16 = orc_from_fp16(0x0001u);   /* smallest positive FP16 */
+  if (s16 > 65504.0f) s16 = 65504.0f;
+  float zf = rintf(-lo / s16);
+  if (zf > 65504.0f) zf = 65504.0f;
+  if (zf < -65504.0f) zf = -65504.0f;
+  float z16 = orc_from_fp16(orc_to_fp16(zf));
+  for (int j = 0; j < n; ++j) codes[j] = orc_code(x[j], s16, z16);
+  *s_out = s16;
+  *z_out = z16;
+}
+
 /* ------------------------------------------------------- layout (Eq. 17) */
 
-/* Bytes of one tile: high tier, codes, then per-row (s, z) metadata. */
-int64_t orc_tile_bytes(int kind, int dk, int dv, int k_hi) {
+/* Storage format: fmt[0] high-tier type (1 BF16, 2 FP16), fmt[1] values per
+ * (s, z) pair along d_v, fmt[2] metadata type (0 FP32, 2 FP16), fmt[3] 1 for
+ * the block-32 Hadamard transform of the low tier. NULL: BF16, one pair per
+ * row, FP32 metadata, no transform. */
+typedef struct {
+  int hi_fp16, group, meta_fp16, hadamard;
+} orc_fmt_t;
+
+static orc_fmt_t orc_fmt(const int32_t* f, int dv) {
+  orc_fmt_t r = {0, dv, 0, 0};
+  if (f) {
+    r.hi_fp16 = f[0] == 2;
+    r.group = f[1];
+    r.meta_fp16 = f[2] == 2;
+    r.hadamard = f[3] != 0;
+  }
+  return r;
+}
+
+static int64_t orc_meta_row_bytes(orc_fmt_t f, int dv) {
+  return (int64_t)(dv / f.group) * 2 * (f.meta_fp16 ? 2 : 4);
+}
+
+/* Bytes of one tile: high tier, codes, then the (s, z) metadata of each low
+ * row, group by group. */
+int64_t orc_tile_bytes(int kind, const int32_t* fmt, int dk, int dv, int k_hi) {
   if (kind == ORC_KIND_FP32) return (int64_t)dk * dv * 4;
-  return (int64_t)k_hi * dv * 2 + (int64_t)(dk - k_hi) * dv + (int64_t)(dk - k_hi) * 8;
+  orc_fmt_t f = orc_fmt(fmt, dv);
+  return (int64_t)k_hi * dv * 2 + (int64_t)(dk - k_hi) * dv +
+         (int64_t)(dk - k_hi) * orc_meta_row_bytes(f, dv);
 }
 
 /* Storage bits per value of a mixed layout, general form of Eq. (7): the low
@@ -130,8 +243,8 @@ double orc_bits_per_value(int dk, int k_hi, int hi_bits, int code_bits, int grou
 }
 
 /* Decode tile rows (in tile order) into S[dk][dv]. */
-static void orc_tile_decode(int kind, int dk, int dv, int k_hi, const uint8_t* tile,
-                            float* S) {
+static void orc_tile_decode(int kind, orc_fmt_t f, int dk, int dv, int k_hi,
+                            const uint8_t* tile, float* S) {
   if (kind == ORC_KIND_FP32) {
     memcpy(S, tile, (size_t)dk * dv * sizeof(float));
     return;
@@ -139,24 +252,42 @@ static void orc_tile_decode(int kind, int dk, int dv, int k_hi, const uint8_t* t
   const uint8_t* hi = tile;
   const uint8_t* codes = tile + (size_t)k_hi * dv * 2;
   const uint8_t* meta = codes + (size_t)(dk - k_hi) * dv;
+  const int64_t mrow = orc_meta_row_bytes(f, dv);
   for (int r = 0; r < dk; ++r) {
+    float* x = S + (size_t)r * dv;
     if (r < k_hi) {
       for (int j = 0; j < dv; ++j) {
         uint16_t h;
         memcpy(&h, hi + ((size_t)r * dv + j) * 2, 2);
-        S[(size_t)r * dv + j] = orc_from_bf16(h);
+        x[j] = f.hi_fp16 ? orc_from_fp16(h) : orc_from_bf16(h);
       }
-    } else {
-      int l = r - k_hi;
+      continue;
+    }
+    int l = r - k_hi;
+    for (int g = 0; g < dv / f.group; ++g) {
       float sz[2];
-      memcpy(sz, meta + (size_t)l * 8, 8);
-      orc_dequant_row(codes + (size_t)l * dv, dv, sz[0], sz[1], S + (size_t)r * dv);
+      const uint8_t* m = meta + (size_t)l * mrow;
+      if (f.meta_fp16) {
+        uint16_t h[2];
+        memcpy(h, m + (size_t)g * 4, 4);
+        sz[0] = orc_from_fp16(h[0]);
+        sz[1] = orc_from_fp16(h[1]);
+      } else {
+        memcpy(sz, m + (size_t)g * 8, 8);
+      }
+      float* xg = x + (size_t)g * f.group;
+      orc_dequant_row(codes + (size_t)l * dv + (size_t)g * f.group, f.group, sz[0], sz[1], xg);
+      if (f.hadamard) {
+        float y[32];
+        orc_hadamard32(xg, y);
+        memcpy(xg, y, sizeof y);
+      }
     }
   }
 }
 
 /* Encode S[dk][dv] (tile order) into the tile. */
-static void orc_tile_encode(int kind, int dk, int dv, int k_hi, const float* S,
+static void orc_tile_encode(int kind, orc_fmt_t f, int dk, int dv, int k_hi, const float* S,
                             uint8_t* tile) {
   if (kind == ORC_KIND_FP32) {
     memcpy(tile, S, (size_t)dk * dv * sizeof(float));
@@ -165,17 +296,35 @@ static void orc_tile_encode(int kind, int dk, int dv, int k_hi, const float* S,
   uint8_t* hi = tile;
   uint8_t* codes = tile + (size_t)k_hi * dv * 2;
   uint8_t* meta = codes + (size_t)(dk - k_hi) * dv;
+  const int64_t mrow = orc_meta_row_bytes(f, dv);
   for (int r = 0; r < dk; ++r) {
+    const float* x = S + (size_t)r * dv;
     if (r < k_hi) {
       for (int j = 0; j < dv; ++j) {
-        uint16_t h = orc_to_bf16(S[(size_t)r * dv + j]);
+        uint16_t h = f.hi_fp16 ? orc_to_fp16(x[j]) : orc_to_bf16(x[j]);
         memcpy(hi + ((size_t)r * dv + j) * 2, &h, 2);
       }
-    } else {
-      int l = r - k_hi;
+      continue;
+    }
+    int l = r - k_hi;
+    for (int g = 0; g < dv / f.group; ++g) {
+      const float* xg = x + (size_t)g * f.group;
+      float y[32];
+      if (f.hadamard) {
+        orc_hadamard32(xg, y);
+        xg = y;
+      }
+      uint8_t* c = codes + (size_t)l * dv + (size_t)g * f.group;
+      uint8_t* m = meta + (size_t)l * mrow;
       float sz[2];
-      orc_quant_row(S + (size_t)r * dv, dv, codes + (size_t)l * dv, &sz[0], &sz[1]);
-      memcpy(meta + (size_t)l * 8, sz, 8);
+      if (f.meta_fp16) {
+        orc_quant_group_fp16(xg, f.group, c, &sz[0], &sz[1]);
+        uint16_t h[2] = {orc_to_fp16(sz[0]), orc_to_fp16(sz[1])};
+        memcpy(m + (size_t)g * 4, h, 4);
+      } else {
+        orc_quant_row(xg, f.group, c, &sz[0], &sz[1]);
+        memcpy(m + (size_t)g * 8, sz, 8);
+      }
     }
   }
 }
@@ -188,9 +337,10 @@ static int orc_perm_at(const uint8_t* perm, int h, int dk, int r) {
 
 /* Pool addressing: tile of (slot, head) at pool + slot*slot_stride +
  * head*tile_stride (pool already offset to the layer). */
-void orc_pack(int kind, int dk, int dv, int k_hi, uint8_t* pool, int64_t slot_stride,
-              int64_t tile_stride, int num_slots, const int32_t* slot_idx, int B, int HV,
-              const float* S, const uint8_t* perm) {
+void orc_pack(int kind, const int32_t* fmt, int dk, int dv, int k_hi, uint8_t* pool,
+              int64_t slot_stride, int64_t tile_stride, int num_slots, const int32_t* slot_idx,
+              int B, int HV, const float* S, const uint8_t* perm) {
+  const orc_fmt_t f = orc_fmt(fmt, dv);
   int64_t ntiles = (int64_t)B * HV;
 #pragma omp parallel for schedule(static)
   for (int64_t t = 0; t < ntiles; ++t) {
@@ -202,15 +352,16 @@ void orc_pack(int kind, int dk, int dv, int k_hi, uint8_t* pool, int64_t slot_st
     for (int r = 0; r < dk; ++r)
       memcpy(W + (size_t)r * dv, src + (size_t)orc_perm_at(perm, h, dk, r) * dv,
              (size_t)dv * sizeof(float));
-    orc_tile_encode(kind, dk, dv, k_hi, W,
+    orc_tile_encode(kind, f, dk, dv, k_hi, W,
                     pool + (size_t)slot * slot_stride + (size_t)h * tile_stride);
     free(W);
   }
 }
 
-void orc_unpack(int kind, int dk, int dv, int k_hi, const uint8_t* pool,
+void orc_unpack(int kind, const int32_t* fmt, int dk, int dv, int k_hi, const uint8_t* pool,
                 int64_t slot_stride, int64_t tile_stride, int num_slots,
                 const int32_t* slot_idx, int B, int HV, const uint8_t* perm, float* S) {
+  const orc_fmt_t f = orc_fmt(fmt, dv);
   int64_t ntiles = (int64_t)B * HV;
 #pragma omp parallel for schedule(static)
   for (int64_t t = 0; t < ntiles; ++t) {
@@ -222,7 +373,7 @@ void orc_unpack(int kind, int dk, int dv, int k_hi, const uint8_t* pool,
       continue;
     }
     float* W = (float*)malloc((size_t)dk * dv * sizeof(float));
-    orc_tile_decode(kind, dk, dv, k_hi,
+    orc_tile_decode(kind, f, dk, dv, k_hi,
                     pool + (size_t)slot * slot_stride + (size_t)h * tile_stride, W);
     for (int r = 0; r < dk; ++r)
       memcpy(dst + (size_t)orc_perm_at(perm, h, dk, r) * dv, W + (size_t)r * dv,
@@ -244,12 +395,13 @@ void orc_unpack(int kind, int dk, int dv, int k_hi, const uint8_t* pool,
  * If pre_out is not NULL it receives the updated state before re-encoding,
  * [B, HV, dk, dv] in tile-row order (used for the error analysis of Eq. (5)).
  */
-void orc_update(int is_kda, int kind, int dk, int dv, int k_hi, uint8_t* pool,
-                int64_t slot_stride, int64_t tile_stride, int num_slots,
+void orc_update(int is_kda, int kind, const int32_t* fmt, int dk, int dv, int k_hi,
+                uint8_t* pool, int64_t slot_stride, int64_t tile_stride, int num_slots,
                 const int32_t* slot_idx, int B, int HK, int HV, const uint16_t* q,
                 const uint16_t* k, const uint16_t* v, const uint16_t* g,
                 const uint16_t* beta, const uint8_t* perm, float scale, float* o,
                 float* pre_out) {
+  const orc_fmt_t f = orc_fmt(fmt, dv);
   int64_t ntiles = (int64_t)B * HV;
   int group = HV / HK;
 #pragma omp parallel for schedule(dynamic, 4)
@@ -285,7 +437,7 @@ void orc_update(int is_kda, int kind, int dk, int dv, int k_hi, uint8_t* pool,
     const uint16_t* vb = v + ((size_t)b * HV + h) * dv;
 
     /* dequantize, then decay: S_bar = Lambda S */
-    orc_tile_decode(kind, dk, dv, k_hi, tile, S);
+    orc_tile_decode(kind, f, dk, dv, k_hi, tile, S);
     for (int r = 0; r < dk; ++r)
       for (int j = 0; j < dv; ++j) S[(size_t)r * dv + j] = a[r] * S[(size_t)r * dv + j];
 
@@ -312,21 +464,23 @@ void orc_update(int is_kda, int kind, int dk, int dv, int k_hi, uint8_t* pool,
 
     if (pre_out) memcpy(pre_out + (size_t)t * dk * dv, S, (size_t)dk * dv * sizeof(float));
 
-    /* store: bf16 for the high tier, Eq. (3) per low-tier row */
-    orc_tile_encode(kind, dk, dv, k_hi, S, tile);
+    /* store: the high tier rounded, Eq. (3) per low-tier group */
+    orc_tile_encode(kind, f, dk, dv, k_hi, S, tile);
 
     free(S); free(kp); free(qp); free(a); free(w); free(delta);
   }
 }
 
 /* Packed zero state for every head of the listed slots. */
-void orc_reset(int kind, int dk, int dv, int k_hi, uint8_t* pool, int64_t slot_stride,
-               int64_t tile_stride, int num_slots, const int32_t* slots, int n, int HV) {
+void orc_reset(int kind, const int32_t* fmt, int dk, int dv, int k_hi, uint8_t* pool,
+               int64_t slot_stride, int64_t tile_stride, int num_slots, const int32_t* slots,
+               int n, int HV) {
+  const orc_fmt_t f = orc_fmt(fmt, dv);
   float* Z = (float*)calloc((size_t)dk * dv, sizeof(float));
   for (int i = 0; i < n; ++i) {
     if (slots[i] < 0 || slots[i] >= num_slots) continue;
     for (int h = 0; h < HV; ++h)
-      orc_tile_encode(kind, dk, dv, k_hi, Z,
+      orc_tile_encode(kind, f, dk, dv, k_hi, Z,
                       pool + (size_t)slots[i] * slot_stride + (size_t)h * tile_stride);
   }
   free(Z);

@@ -11,7 +11,7 @@ marshals numpy arrays. It also keeps its own description of the packed pool
 Every function cites the passage it follows:
   update      section 3.1 Eq. (1)-(2); section 3.2; App. A.5 (fused executor)
   quant_row   section 3.2 Eq. (3); App. A.1 (integer formats)
-  pack/unpack section 5.2; App. A.5 Eq. (17)
+  pack/unpack section 5.2; App. A.5 Eq. (17); App. A.1 (storage formats)
   select      section 5.1 Eq. (8)-(10); App. A.2 Eq. (13)-(15); Alg. 1
   bits        section 5.1 Eq. (7); App. A.1 Eq. (12) and the format table
 """
@@ -29,6 +29,12 @@ LIB = os.path.join(HERE, "liboracle.so")
 
 KIND_FP32 = 0
 KIND_MIXED = 1
+
+# Storage formats (high-tier type, values per (s, z) pair, metadata type,
+# Hadamard): types 1 = BF16, 2 = FP16, 0 = FP32. None is the default format:
+# BF16 high tier, one fp32 (s, z) pair per row, no transform.
+FMT_PAPER = (2, 32, 2, 1)        # App. A.1: INT8 + H32, FP16 (s, z) per 32; FP16 tier
+FMT_PAPER_PLAIN = (2, 32, 2, 0)  # the same without the transform
 
 _lib = None
 
@@ -59,18 +65,22 @@ def lib():
         L.orc_max_threads.restype = i32
         L.orc_bf16_round.argtypes = [vp, vp, i64]
         L.orc_bf16_widen.argtypes = [vp, vp, i64]
+        L.orc_fp16_round.argtypes = [vp, vp, i64]
+        L.orc_fp16_widen.argtypes = [vp, vp, i64]
+        L.orc_hadamard32.argtypes = [vp, vp]
+        L.orc_quant_group_fp16.argtypes = [vp, i32, vp, vp, vp]
         L.orc_quant_params.argtypes = [vp, i32, vp, vp]
         L.orc_quant_row.argtypes = [vp, i32, vp, vp, vp]
         L.orc_dequant_row.argtypes = [vp, i32, f32, f32, vp]
-        L.orc_tile_bytes.argtypes = [i32, i32, i32, i32]
+        L.orc_tile_bytes.argtypes = [i32, vp, i32, i32, i32]
         L.orc_tile_bytes.restype = i64
         L.orc_bits_per_value.argtypes = [i32, i32, i32, i32, i32, i32]
         L.orc_bits_per_value.restype = f64
-        L.orc_pack.argtypes = [i32, i32, i32, i32, vp, i64, i64, i32, vp, i32, i32, vp, vp]
-        L.orc_unpack.argtypes = [i32, i32, i32, i32, vp, i64, i64, i32, vp, i32, i32, vp, vp]
-        L.orc_update.argtypes = [i32, i32, i32, i32, i32, vp, i64, i64, i32, vp, i32, i32, i32,
-                                 vp, vp, vp, vp, vp, vp, f32, vp, vp]
-        L.orc_reset.argtypes = [i32, i32, i32, i32, vp, i64, i64, i32, vp, i32, i32]
+        L.orc_pack.argtypes = [i32, vp, i32, i32, i32, vp, i64, i64, i32, vp, i32, i32, vp, vp]
+        L.orc_unpack.argtypes = [i32, vp, i32, i32, i32, vp, i64, i64, i32, vp, i32, i32, vp, vp]
+        L.orc_update.argtypes = [i32, i32, vp, i32, i32, i32, vp, i64, i64, i32, vp, i32, i32,
+                                 i32, vp, vp, vp, vp, vp, vp, f32, vp, vp]
+        L.orc_reset.argtypes = [i32, vp, i32, i32, i32, vp, i64, i64, i32, vp, i32, i32]
         L.orc_select.argtypes = [i32, i32, i32, i32, i32, vp, vp, i32, f64, vp, vp, vp, vp, vp]
         L.orc_select.restype = i32
         _lib = L
@@ -99,6 +109,50 @@ def bf16_widen(u) -> np.ndarray:
     return out
 
 
+def fp16_round(x) -> np.ndarray:
+    """fp32 -> IEEE binary16 bit patterns, round-to-nearest-even."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    out = np.empty(x.shape, np.uint16)
+    lib().orc_fp16_round(_p(x), _p(out), x.size)
+    return out
+
+
+def fp16_widen(u) -> np.ndarray:
+    u = np.ascontiguousarray(u, dtype=np.uint16)
+    out = np.empty(u.shape, np.float32)
+    lib().orc_fp16_widen(_p(u), _p(out), u.size)
+    return out
+
+
+def hadamard32(x) -> np.ndarray:
+    """Normalized block-32 Hadamard transform of one group (App. A.1)."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    assert x.shape == (32,)
+    y = np.empty(32, np.float32)
+    lib().orc_hadamard32(_p(x), _p(y))
+    return y
+
+
+def quant_group_fp16(x):
+    """Eq. (3) on one group with FP16 metadata (App. A.1): (codes, s, z), with
+    s and z the stored FP16 values widened to fp32."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    codes = np.empty(x.shape, np.uint8)
+    s = ctypes.c_float()
+    z = ctypes.c_float()
+    lib().orc_quant_group_fp16(_p(x), x.size, _p(codes), ctypes.byref(s), ctypes.byref(z))
+    return codes, np.float32(s.value), np.float32(z.value)
+
+
+def _fmt_arr(fmt):
+    if fmt is None:
+        return None
+    hi, group, meta, had = fmt
+    assert hi in (1, 2) and meta in (0, 2) and group > 0
+    assert not had or group == 32
+    return np.ascontiguousarray(fmt, dtype=np.int32)
+
+
 def quant_row(x):
     """Eq. (3) on one row: returns (codes uint8, s, z)."""
     x = np.ascontiguousarray(x, dtype=np.float32)
@@ -124,12 +178,15 @@ def qdq_row(x) -> np.ndarray:
 
 # ------------------------------------------------------------------- layout
 
-def tile_bytes(kind: int, dk: int, dv: int, k_hi: int) -> int:
-    return int(lib().orc_tile_bytes(kind, dk, dv, k_hi))
+def tile_bytes(kind: int, dk: int, dv: int, k_hi: int, fmt=None) -> int:
+    f = _fmt_arr(fmt)
+    if f is not None:
+        assert dv % fmt[1] == 0
+    return int(lib().orc_tile_bytes(kind, _p(f), dk, dv, k_hi))
 
 
-def tile_stride(kind: int, dk: int, dv: int, k_hi: int) -> int:
-    tb = tile_bytes(kind, dk, dv, k_hi)
+def tile_stride(kind: int, dk: int, dv: int, k_hi: int, fmt=None) -> int:
+    tb = tile_bytes(kind, dk, dv, k_hi, fmt)
     return (tb + 127) // 128 * 128
 
 
@@ -142,10 +199,12 @@ class Pool:
     """Host byte image of a slot-indexed pool, laid out as the library's."""
 
     def __init__(self, kind: int, dk: int, dv: int, k_hi: int, num_layers: int,
-                 num_slots: int, num_v_heads: int):
+                 num_slots: int, num_v_heads: int, fmt=None):
         self.kind, self.dk, self.dv, self.k_hi = kind, dk, dv, k_hi
         self.num_layers, self.num_slots, self.hv = num_layers, num_slots, num_v_heads
-        self.tile_stride = tile_stride(kind, dk, dv, k_hi)
+        self.fmt = None if kind == KIND_FP32 else fmt
+        self._fmt = _fmt_arr(self.fmt)
+        self.tile_stride = tile_stride(kind, dk, dv, k_hi, self.fmt)
         self.slot_stride = self.tile_stride * num_v_heads
         self.layer_stride = self.slot_stride * num_slots
         self.buf = np.zeros(self.layer_stride * num_layers, np.uint8)
@@ -155,7 +214,7 @@ class Pool:
 
     def tile(self, layer: int, slot: int, head: int) -> np.ndarray:
         o = layer * self.layer_stride + slot * self.slot_stride + head * self.tile_stride
-        return self.buf[o:o + tile_bytes(self.kind, self.dk, self.dv, self.k_hi)]
+        return self.buf[o:o + tile_bytes(self.kind, self.dk, self.dv, self.k_hi, self.fmt)]
 
     def copy(self) -> "Pool":
         c = Pool.__new__(Pool)
@@ -175,7 +234,7 @@ def pack(pool: Pool, layer: int, slot_idx, S, perm=None) -> None:
     perm = None if perm is None else np.ascontiguousarray(perm, dtype=np.uint8)
     B = slot_idx.size
     assert S.shape == (B, pool.hv, pool.dk, pool.dv)
-    lib().orc_pack(pool.kind, pool.dk, pool.dv, pool.k_hi, pool.layer_ptr(layer),
+    lib().orc_pack(pool.kind, _p(pool._fmt), pool.dk, pool.dv, pool.k_hi, pool.layer_ptr(layer),
                    pool.slot_stride, pool.tile_stride, pool.num_slots, _p(slot_idx), B,
                    pool.hv, _p(S), _p(perm))
 
@@ -185,7 +244,7 @@ def unpack(pool: Pool, layer: int, slot_idx, perm=None) -> np.ndarray:
     perm = None if perm is None else np.ascontiguousarray(perm, dtype=np.uint8)
     B = slot_idx.size
     S = np.empty((B, pool.hv, pool.dk, pool.dv), np.float32)
-    lib().orc_unpack(pool.kind, pool.dk, pool.dv, pool.k_hi, pool.layer_ptr(layer),
+    lib().orc_unpack(pool.kind, _p(pool._fmt), pool.dk, pool.dv, pool.k_hi, pool.layer_ptr(layer),
                      pool.slot_stride, pool.tile_stride, pool.num_slots, _p(slot_idx), B,
                      pool.hv, _p(perm), _p(S))
     return S
@@ -195,7 +254,7 @@ def reset(pool: Pool, layer: int, slots) -> None:
     slots = _i32(slots)
     layers = range(pool.num_layers) if layer < 0 else [layer]
     for l in layers:
-        lib().orc_reset(pool.kind, pool.dk, pool.dv, pool.k_hi, pool.layer_ptr(l),
+        lib().orc_reset(pool.kind, _p(pool._fmt), pool.dk, pool.dv, pool.k_hi, pool.layer_ptr(l),
                         pool.slot_stride, pool.tile_stride, pool.num_slots, _p(slots),
                         slots.size, pool.hv)
 
@@ -219,7 +278,8 @@ def update(pool: Pool, layer: int, slot_idx, *, kda: bool, q, k, v, g, beta, per
     perm = None if perm is None else np.ascontiguousarray(perm, dtype=np.uint8)
     o = np.empty((B, pool.hv, pool.dv), np.float32)
     pre = np.empty((B, pool.hv, pool.dk, pool.dv), np.float32) if want_pre else None
-    lib().orc_update(int(kda), pool.kind, pool.dk, pool.dv, pool.k_hi, pool.layer_ptr(layer),
+    lib().orc_update(int(kda), pool.kind, _p(pool._fmt), pool.dk, pool.dv, pool.k_hi,
+                     pool.layer_ptr(layer),
                      pool.slot_stride, pool.tile_stride, pool.num_slots, _p(slot_idx), B, HK,
                      pool.hv, _p(q), _p(k), _p(v), _p(g), _p(beta), _p(perm), float(scale),
                      _p(o), _p(pre))
