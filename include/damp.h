@@ -25,15 +25,22 @@
  * State orientation (paper section 3.1): one head's state S has d_k rows
  * (key channels u) and d_v columns. The read-out is o = S^T q.
  *
- * Packed tile (paper section 5.2 and App. A.5, Eq. (17), with the per-row
- * low tier used here): one tile holds the state of one (layer, request slot,
- * value head). Its rows are in the calibrated order pi: tile row r holds key
- * channel pi[r]; rows 0..k_hi-1 are the protected channels. Bytes, in order:
+ * Packed tile (paper section 5.2 and App. A.5, Eq. (17)): one tile holds the
+ * state of one (layer, request slot, value head). Its rows are in the
+ * calibrated order pi: tile row r holds key channel pi[r]; rows 0..k_hi-1
+ * are the protected channels. Bytes, in order:
  *
- *   DAMP_STATE_MIXED:
+ *   DAMP_STATE_MIXED, default tiers (damp_layout_init):
  *     [hi]   k_hi x d_v bf16, row-major
  *     [code] (d_k - k_hi) x d_v uint8 codes, row-major
  *     [meta] (d_k - k_hi) x {s, z} fp32 (8 bytes per low-tier row)
+ *   DAMP_STATE_MIXED, the paper's tiers (App. A.1 format table; set
+ *   hi_dtype = meta_dtype = DAMP_DT_FP16, group = 32, hadamard = 0 or 1):
+ *     [hi]   k_hi x d_v FP16, row-major
+ *     [code] (d_k - k_hi) x d_v uint8 codes, row-major; with hadamard = 1
+ *            the codes of each group of 32 are those of its normalized
+ *            Hadamard transform
+ *     [meta] (d_k - k_hi) x (d_v / 32) x {s, z} FP16 (4 bytes per group)
  *   DAMP_STATE_FP32:
  *     d_k x d_v fp32, row-major
  *
@@ -44,6 +51,12 @@
  * with round = round-half-to-even. A row whose s is not a normal fp32 number
  * (a constant row) uses s = |min x| / 255, or s = 1 if that is not normal
  * either, so the all-zero row is stored as codes 0, s = 1, z = 0.
+ * The paper's tiers apply the same rule per group of 32 values (after the
+ * transform when hadamard = 1; the transform is y = H x / sqrt(32) with the
+ * Sylvester matrix H, its own inverse), then round s to FP16 (kept within
+ * [2^-24, 65504]), compute z = round(-min / s) from the stored s, round it
+ * to FP16 (within +-65504), and code with the stored pair; reconstruction is
+ * s * (c - z) followed by the inverse transform.
  * The tile stride in a pool is the tile size rounded up to 128 bytes.
  */
 #ifndef DAMP_H
@@ -77,16 +90,19 @@ typedef struct {
   int32_t d_v;        /* value channels (columns) */
   int32_t k_hi;       /* protected rows held in the high-precision tier */
   int32_t kind;       /* damp_state_kind */
-  int32_t hi_dtype;   /* damp_dtype of the high tier (BF16 has kernels) */
+  int32_t hi_dtype;   /* damp_dtype of the high tier (BF16, or FP16 with the paper's tiers) */
   int32_t group;      /* values per (s, z) pair along d_v; d_v = one per row */
-  int32_t meta_dtype; /* damp_dtype of s and z (FP32 has kernels) */
-  int32_t hadamard;   /* 1 = block-32 Hadamard before quantization (no kernels) */
+  int32_t meta_dtype; /* damp_dtype of s and z (FP32 per row, or FP16 per group of 32) */
+  int32_t hadamard;   /* 1 = block-32 Hadamard before quantization (paper's tiers) */
 } damp_layout;
 
 /* Fills `out` with the default layout: BF16 high tier, one fp32 (s, z) pair
  * per low-tier row, no Hadamard. Kernels exist for d_k == d_v in
- * {16, 32, 64, 128}. Returns DAMP_ERR_INVALID_ARG if out is NULL,
- * d_k or d_v is not positive, or k_hi is outside [0, d_k]. */
+ * {16, 32, 64, 128}, and for the paper's tiers (FP16 high tier and FP16
+ * (s, z) per group of 32, with or without the transform) for d_k == d_v in
+ * {32, 64, 128}; other layouts are valid for the size queries but calls that
+ * move state return DAMP_ERR_UNSUPPORTED. Returns DAMP_ERR_INVALID_ARG if
+ * out is NULL, d_k or d_v is not positive, or k_hi is outside [0, d_k]. */
 damp_status damp_layout_init(damp_layout* out, int32_t d_k, int32_t d_v,
                              int32_t k_hi, int32_t kind);
 

@@ -9,7 +9,11 @@
 namespace damp {
 
 constexpr int kFp32 = 0;   // DAMP_STATE_FP32
-constexpr int kMixed = 1;  // DAMP_STATE_MIXED
+constexpr int kMixed = 1;  // DAMP_STATE_MIXED with the default tiers
+// DAMP_STATE_MIXED with the paper's tiers (App. A.1, Eq. (17)): FP16 high
+// rows; low rows in groups of 32 values with FP16 (s, z), optionally after
+// the normalized block-32 Hadamard transform.
+constexpr int kPaper = 2;
 
 // ------------------------------------------------------------ conversions
 
@@ -29,6 +33,24 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
 
 __device__ __forceinline__ uint16_t f32_to_bf16(float a) {
   return static_cast<uint16_t>(pack_bf16x2(a, 0.0f) & 0xffffu);
+}
+
+// FP16 halves of a word, and two fp32 -> packed FP16 pair (round to nearest
+// even, IEEE overflow to infinity).
+__device__ __forceinline__ float f16_lo(uint32_t w) {
+  return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(w & 0xffffu)));
+}
+__device__ __forceinline__ float f16_hi(uint32_t w) {
+  return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(w >> 16)));
+}
+__device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
+  typedef float f2 __attribute__((ext_vector_type(2)));
+  typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+  f2 v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, h2));
+}
+__device__ __forceinline__ float round_f16(float a) {
+  return static_cast<float>(static_cast<_Float16>(a));
 }
 
 // Byte i of w as a float (v_cvt_f32_ubyte{i}).
@@ -167,6 +189,53 @@ __device__ __forceinline__ uint32_t pack_codes4(float c0, float c1, float c2, fl
   return __builtin_amdgcn_cvt_pk_u8_f32(c3, 3, w);
 }
 
+// -------------------------------------- paper low tier (App. A.1, Eq. 17)
+
+constexpr float kInvSqrt32 = 0.17677669529663687f;
+
+// Unnormalized Hadamard transform (Sylvester order) of the 32 values of a
+// group held as 16 per lane by the lane pair (L, L ^ 1); `upper` is true on
+// the lane holding values 16..31. Four butterfly stages in the lane, the
+// fifth across the pair.
+__device__ __forceinline__ void fwht32_pair(float (&x)[16], bool upper) {
+#pragma unroll
+  for (int m = 1; m < 16; m <<= 1)
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+      if (!(j & m)) {
+        const float a = x[j], b = x[j | m];
+        x[j] = a + b;
+        x[j | m] = a - b;
+      }
+  const float sgn = upper ? -1.0f : 1.0f;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) x[j] = fmaf(sgn, x[j], dpp_mov<0xb1>(x[j]));
+}
+
+// Stored (s, z) of one group of 32 values held by a lane pair, given the
+// lane's extrema, and the reciprocal of the stored scale: s from Eq. (3) in
+// fp32 (constant groups as for rows), rounded to FP16 and kept positive and
+// finite; z = round(-min / s) from the stored s, within FP16's finite range,
+// rounded to FP16. Divisions are IEEE (a few per group).
+__device__ __forceinline__ void group_qparams_f16(float mn, float mx, float& s16, float& z16,
+                                                  float& inv) {
+  mn = fminf(mn, dpp_mov<0xb1>(mn));
+  mx = fmaxf(mx, dpp_mov<0xb1>(mx));
+  float s = (mx - mn) / 255.0f;
+  if (!(s >= FLT_MIN)) {
+    s = fabsf(mn) / 255.0f;
+    if (!(s >= FLT_MIN)) s = 1.0f;
+  }
+  s16 = round_f16(s);
+  if (!(s16 > 0.0f)) s16 = 5.9604644775390625e-08f;  // smallest positive FP16
+  if (s16 > 65504.0f) s16 = 65504.0f;
+  float zf = rintf(-mn / s16);
+  zf = fminf(fmaxf(zf, -65504.0f), 65504.0f);
+  z16 = round_f16(zf);
+  const float rc = __builtin_amdgcn_rcpf(s16);
+  inv = fmaf(fmaf(-rc, s16, 1.0f), rc, rc);
+}
+
 // ------------------------------------------------------------- row encode
 
 // Stores one row slice of CPT values (columns col0..col0+CPT of tile row r)
@@ -175,7 +244,49 @@ __device__ __forceinline__ uint32_t pack_codes4(float c0, float c1, float c2, fl
 // branch on r is uniform across the TPR lanes of the row.
 template <int KIND, int D, int CPT, int TPR>
 __device__ __forceinline__ void encode_row(const float* x, int r, int k_hi, int cg, int col0,
-                                           uint8_t* tile, uint8_t* codes, float2* meta) {
+                                           uint8_t* tile, uint8_t* codes, uint8_t* meta_bytes,
+                                           bool had = false) {
+  if constexpr (KIND == kPaper) {
+    static_assert(CPT == 16, "a lane pair holds one group of 32");
+    if (r < k_hi) {
+      uint32_t w[CPT / 2];
+#pragma unroll
+      for (int j = 0; j < CPT / 2; ++j) w[j] = pack_f16x2(x[2 * j], x[2 * j + 1]);
+      store_words<CPT * 2>(tile + (static_cast<size_t>(r) * D + col0) * 2, w);
+      return;
+    }
+    float y[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) y[j] = x[j];
+    if (had) {
+      fwht32_pair(y, (cg & 1) != 0);
+#pragma unroll
+      for (int j = 0; j < 16; ++j) y[j] *= kInvSqrt32;
+    }
+    float mn = y[0], mx = y[0];
+#pragma unroll
+    for (int j = 1; j < 16; ++j) {
+      mn = fminf(mn, y[j]);
+      mx = fmaxf(mx, y[j]);
+    }
+    float s16, z16, inv;
+    group_qparams_f16(mn, mx, s16, z16, inv);
+    uint32_t w[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      uint32_t c = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(y[4 * j], inv, z16), 0, 0u);
+      c = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(y[4 * j + 1], inv, z16), 1, c);
+      c = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(y[4 * j + 2], inv, z16), 2, c);
+      w[j] = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(y[4 * j + 3], inv, z16), 3, c);
+    }
+    const int l = r - k_hi;
+    store_words<16>(codes + static_cast<size_t>(l) * D + col0, w);
+    if ((cg & 1) == 0)
+      reinterpret_cast<uint32_t*>(meta_bytes)[static_cast<size_t>(l) * (D / 32) + (col0 >> 5)] =
+          pack_f16x2(s16, z16);
+    return;
+  }
+  float2* meta = reinterpret_cast<float2*>(meta_bytes);
   if (KIND == kFp32) {
     uint32_t w[CPT];
 #pragma unroll

@@ -24,8 +24,17 @@ struct TileGeom {
 // not one the layout math accepts.
 bool tile_geom(const damp_layout* layout, TileGeom* g);
 
-// True if the layout has kernels: BF16 high tier, one fp32 (s, z) pair per
-// row, no Hadamard, d_k == d_v in {16, 32, 64, 128}.
+// True for the paper's tiers (App. A.1, Eq. (17)): FP16 high tier, groups
+// of 32 with FP16 (s, z), with or without the block-32 Hadamard transform.
+bool layout_is_paper(const damp_layout* layout);
+
+// True for the default tiers: BF16 high tier, one fp32 (s, z) pair per row,
+// no transform.
+bool layout_is_default(const damp_layout* layout);
+
+// True if the layout has kernels: d_k == d_v in {16, 32, 64, 128} with the
+// FP32 state or the default tiers, or d_k == d_v in {32, 64, 128} with the
+// paper's tiers.
 bool layout_has_kernels(const damp_layout* layout);
 
 // Validates a pool descriptor (non-null, consistent strides and counts).

@@ -86,12 +86,22 @@ bool tile_geom(const damp_layout* L, TileGeom* g) {
   return true;
 }
 
+bool layout_is_paper(const damp_layout* L) {
+  return L->kind == DAMP_STATE_MIXED && L->hi_dtype == DAMP_DT_FP16 &&
+         L->meta_dtype == DAMP_DT_FP16 && L->group == 32 && (L->hadamard == 0 || L->hadamard == 1);
+}
+
+bool layout_is_default(const damp_layout* L) {
+  return L->kind == DAMP_STATE_MIXED && L->hi_dtype == DAMP_DT_BF16 &&
+         L->meta_dtype == DAMP_DT_FP32 && L->group == L->d_v && L->hadamard == 0;
+}
+
 bool layout_has_kernels(const damp_layout* L) {
   if (L->d_k != L->d_v) return false;
   if (L->d_k != 16 && L->d_k != 32 && L->d_k != 64 && L->d_k != 128) return false;
   if (L->kind == DAMP_STATE_FP32) return true;
-  return L->hi_dtype == DAMP_DT_BF16 && L->meta_dtype == DAMP_DT_FP32 && L->group == L->d_v &&
-         L->hadamard == 0;
+  if (layout_is_paper(L)) return L->d_k >= 32;
+  return layout_is_default(L);
 }
 
 damp_status check_pool(const damp_pool* pool) {

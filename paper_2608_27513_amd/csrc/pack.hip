@@ -18,6 +18,7 @@ struct TileParams {
   int32_t num_slots;
   int32_t HV;
   int32_t k_hi;
+  int32_t had;  // block-32 Hadamard on the low tier (paper layout only)
 };
 
 template <int D>
@@ -40,7 +41,7 @@ __global__ __launch_bounds__(Shape<D>::NT) void pack_kernel(const TileParams p) 
                   static_cast<size_t>(h) * p.tile_stride;
   const int k_hi = KIND == kFp32 ? D : p.k_hi;
   uint8_t* codes = tile + static_cast<size_t>(k_hi) * D * 2;
-  float2* meta = reinterpret_cast<float2*>(codes + static_cast<size_t>(D - k_hi) * D);
+  uint8_t* meta = codes + static_cast<size_t>(D - k_hi) * D;
   const float* src = p.S + (static_cast<size_t>(b) * p.HV + h) * D * D;
 #pragma unroll
   for (int i = 0; i < Sh::RPT; ++i) {
@@ -51,7 +52,7 @@ __global__ __launch_bounds__(Shape<D>::NT) void pack_kernel(const TileParams p) 
     load_words<Sh::CPT * 4>(reinterpret_cast<const uint8_t*>(src + static_cast<size_t>(u) * D + col0), w);
 #pragma unroll
     for (int j = 0; j < Sh::CPT; ++j) x[j] = __uint_as_float(w[j]);
-    encode_row<KIND, D, Sh::CPT, Sh::TPR>(x, r, k_hi, cg, col0, tile, codes, meta);
+    encode_row<KIND, D, Sh::CPT, Sh::TPR>(x, r, k_hi, cg, col0, tile, codes, meta, p.had != 0);
   }
 }
 
@@ -68,12 +69,45 @@ __global__ __launch_bounds__(Shape<D>::NT) void unpack_kernel(const TileParams p
   const int k_hi = KIND == kFp32 ? D : p.k_hi;
   const uint8_t* codes = tile + static_cast<size_t>(k_hi) * D * 2;
   const float2* meta = reinterpret_cast<const float2*>(codes + static_cast<size_t>(D - k_hi) * D);
+  const uint32_t* meta16 = reinterpret_cast<const uint32_t*>(codes + static_cast<size_t>(D - k_hi) * D);
 #pragma unroll
   for (int i = 0; i < Sh::RPT; ++i) {
     const int r = rg + Sh::RG * i;
     const int u = p.perm ? (static_cast<int>(p.perm[static_cast<size_t>(h) * D + r]) & (D - 1)) : r;
     uint32_t out[Sh::CPT];
-    if (!live) {
+    if constexpr (KIND == kPaper) {
+      // FP16 rows; low rows: s * (c - z) per group of 32, then the inverse
+      // transform (the lane pair holds the group)
+      float y[Sh::CPT];
+      if (r < k_hi) {
+        uint32_t w[Sh::CPT / 2];
+        load_words<Sh::CPT * 2>(tile + (static_cast<size_t>(r) * D + col0) * 2, w);
+#pragma unroll
+        for (int j = 0; j < Sh::CPT / 2; ++j) {
+          y[2 * j] = f16_lo(w[j]);
+          y[2 * j + 1] = f16_hi(w[j]);
+        }
+      } else {
+        uint32_t w[Sh::CPT / 4];
+        load_words<Sh::CPT>(codes + static_cast<size_t>(r - k_hi) * D + col0, w);
+        const uint32_t m = meta16[static_cast<size_t>(r - k_hi) * (D / 32) + (col0 >> 5)];
+        const float s16 = f16_lo(m), z16 = f16_hi(m);
+#pragma unroll
+        for (int j = 0; j < Sh::CPT / 4; ++j) {
+          y[4 * j + 0] = __fmul_rn(s16, __fsub_rn(ubyte<0>(w[j]), z16));
+          y[4 * j + 1] = __fmul_rn(s16, __fsub_rn(ubyte<1>(w[j]), z16));
+          y[4 * j + 2] = __fmul_rn(s16, __fsub_rn(ubyte<2>(w[j]), z16));
+          y[4 * j + 3] = __fmul_rn(s16, __fsub_rn(ubyte<3>(w[j]), z16));
+        }
+        if (p.had) {
+          fwht32_pair(y, (cg & 1) != 0);
+#pragma unroll
+          for (int j = 0; j < Sh::CPT; ++j) y[j] *= kInvSqrt32;
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < Sh::CPT; ++j) out[j] = live ? __float_as_uint(y[j]) : 0u;
+    } else if (!live) {
 #pragma unroll
       for (int j = 0; j < Sh::CPT; ++j) out[j] = 0u;
     } else if (KIND == kFp32) {
@@ -103,7 +137,7 @@ __global__ __launch_bounds__(Shape<D>::NT) void unpack_kernel(const TileParams p
   }
 }
 
-// Packed zero state: zero high tier and codes, (s, z) = (1, 0) per row.
+// Packed zero state: zero high tier and codes, (s, z) = (1, 0) per row or group.
 template <int KIND, int D>
 __global__ __launch_bounds__(Shape<D>::NT) void reset_kernel(const TileParams p) {
   using Sh = Shape<D>;
@@ -115,13 +149,14 @@ __global__ __launch_bounds__(Shape<D>::NT) void reset_kernel(const TileParams p)
                   static_cast<size_t>(slot) * p.slot_stride + static_cast<size_t>(h) * p.tile_stride;
   const int k_hi = KIND == kFp32 ? D : p.k_hi;
   uint8_t* codes = tile + static_cast<size_t>(k_hi) * D * 2;
-  float2* meta = reinterpret_cast<float2*>(codes + static_cast<size_t>(D - k_hi) * D);
+  uint8_t* meta = codes + static_cast<size_t>(D - k_hi) * D;
   float x[Sh::CPT];
 #pragma unroll
   for (int j = 0; j < Sh::CPT; ++j) x[j] = 0.0f;
 #pragma unroll
   for (int i = 0; i < Sh::RPT; ++i)
-    encode_row<KIND, D, Sh::CPT, Sh::TPR>(x, rg + Sh::RG * i, k_hi, cg, col0, tile, codes, meta);
+    encode_row<KIND, D, Sh::CPT, Sh::TPR>(x, rg + Sh::RG * i, k_hi, cg, col0, tile, codes, meta,
+                                          p.had != 0);
 }
 
 enum class Op { kPack, kUnpack, kReset };
@@ -139,7 +174,9 @@ void launch(Op op, const TileParams& p, dim3 grid, hipStream_t s) {
 template <int KIND>
 void launch_d(Op op, int D, const TileParams& p, dim3 grid, hipStream_t s) {
   switch (D) {
-    case 16: launch<KIND, 16>(op, p, grid, s); break;
+    case 16:
+      if constexpr (KIND != kPaper) launch<KIND, 16>(op, p, grid, s);  // groups need d_v >= 32
+      break;
     case 32: launch<KIND, 32>(op, p, grid, s); break;
     case 64: launch<KIND, 64>(op, p, grid, s); break;
     default: launch<KIND, 128>(op, p, grid, s); break;
@@ -173,9 +210,12 @@ damp_status run(Op op, const char* name, const damp_pool* pool, int32_t layer,
   p.num_slots = pool->num_slots;
   p.HV = pool->num_v_heads;
   p.k_hi = pool->layout.kind == DAMP_STATE_FP32 ? 0 : pool->layout.k_hi;
+  p.had = pool->layout.hadamard;
   const dim3 grid(pool->num_v_heads, B, all_layers ? pool->num_layers : 1);
   if (pool->layout.kind == DAMP_STATE_FP32)
     launch_d<kFp32>(op, pool->layout.d_k, p, grid, as_stream(stream));
+  else if (layout_is_paper(&pool->layout))
+    launch_d<kPaper>(op, pool->layout.d_k, p, grid, as_stream(stream));
   else
     launch_d<kMixed>(op, pool->layout.d_k, p, grid, as_stream(stream));
   return check_launch(name);

@@ -62,7 +62,10 @@ __global__ __launch_bounds__(NT) void update_kernel(const UpdateParams p) {
                   static_cast<size_t>(h) * p.tile_stride;
   const int k_hi = KIND == kFp32 ? D : p.k_hi;
   uint8_t* codes = tile + static_cast<size_t>(k_hi) * D * 2;
-  float2* meta = reinterpret_cast<float2*>(codes + static_cast<size_t>(D - k_hi) * D);
+  uint8_t* meta_bytes = codes + static_cast<size_t>(D - k_hi) * D;
+  const float2* meta = reinterpret_cast<const float2*>(meta_bytes);
+  // paper tiers: one word (FP16 s, FP16 z) per row and group of 32
+  const uint32_t* meta16 = reinterpret_cast<const uint32_t*>(meta_bytes);
 
   // ---- issue the tile loads (the dominant HBM traffic) ---------------------
   uint32_t raw[RPT][CPT * EB / 4];
@@ -75,7 +78,12 @@ __global__ __launch_bounds__(NT) void update_kernel(const UpdateParams p) {
       sz[i] = make_float2(0.0f, 0.0f);
     } else {
       load_words<CPT>(codes + static_cast<size_t>(r - k_hi) * D + col0, raw[i]);
-      sz[i] = meta[r - k_hi];
+      if constexpr (KIND == kPaper) {
+        const uint32_t m = meta16[static_cast<size_t>(r - k_hi) * (D / 32) + (col0 >> 5)];
+        sz[i] = make_float2(f16_lo(m), f16_hi(m));
+      } else {
+        sz[i] = meta[r - k_hi];
+      }
     }
   }
 
@@ -109,6 +117,12 @@ __global__ __launch_bounds__(NT) void update_kernel(const UpdateParams p) {
       if (KIND == kFp32) {
 #pragma unroll
         for (int j = 0; j < CPT; ++j) x[i][j] = aa[i] * __uint_as_float(raw[i][j]);
+      } else if (KIND == kPaper) {
+#pragma unroll
+        for (int j = 0; j < CPT / 2; ++j) {
+          x[i][2 * j] = aa[i] * f16_lo(raw[i][j]);
+          x[i][2 * j + 1] = aa[i] * f16_hi(raw[i][j]);
+        }
       } else {
 #pragma unroll
         for (int j = 0; j < CPT / 2; ++j) {
@@ -117,8 +131,9 @@ __global__ __launch_bounds__(NT) void update_kernel(const UpdateParams p) {
         }
       }
     } else {
-      // a * s * (c - z) as one FMA per value: (a s) c + (-(a s) z)
-      const float A = aa[i] * sz[i].x;
+      // a * s * (c - z) as one FMA per value: (a s) c + (-(a s) z); with the
+      // transform, its normalization folds into the same factor
+      const float A = aa[i] * sz[i].x * ((KIND == kPaper && p.had) ? kInvSqrt32 : 1.0f);
       const float B0 = -A * sz[i].y;
 #pragma unroll
       for (int j = 0; j < CPT / 4; ++j) {
@@ -126,6 +141,9 @@ __global__ __launch_bounds__(NT) void update_kernel(const UpdateParams p) {
         x[i][4 * j + 1] = fmaf(A, ubyte<1>(raw[i][j]), B0);
         x[i][4 * j + 2] = fmaf(A, ubyte<2>(raw[i][j]), B0);
         x[i][4 * j + 3] = fmaf(A, ubyte<3>(raw[i][j]), B0);
+      }
+      if constexpr (KIND == kPaper) {
+        if (p.had) fwht32_pair(reinterpret_cast<float(&)[16]>(x[i]), (cg & 1) != 0);
       }
     }
   }
@@ -186,7 +204,7 @@ __global__ __launch_bounds__(NT) void update_kernel(const UpdateParams p) {
     const float bk = beta * kk[i];
 #pragma unroll
     for (int j = 0; j < CPT; ++j) x[i][j] = fmaf(bk, dl[j], x[i][j]);
-    encode_row<KIND, D, CPT, TPR>(x[i], r, k_hi, cg, col0, tile, codes, meta);
+    encode_row<KIND, D, CPT, TPR>(x[i], r, k_hi, cg, col0, tile, codes, meta_bytes, p.had != 0);
   }
 }
 
@@ -201,7 +219,9 @@ void launch(const UpdateParams& p, int B, hipStream_t stream) {
 template <int KIND, bool KDA>
 void launch_d(int D, const UpdateParams& p, int B, hipStream_t stream) {
   switch (D) {
-    case 16: launch<KIND, KDA, 16>(p, B, stream); break;
+    case 16:
+      if constexpr (KIND != kPaper) launch<KIND, KDA, 16>(p, B, stream);  // groups need d_v >= 32
+      break;
     case 32: launch<KIND, KDA, 32>(p, B, stream); break;
     case 64: launch<KIND, KDA, 64>(p, B, stream); break;
     default: launch<KIND, KDA, 128>(p, B, stream); break;
@@ -249,11 +269,12 @@ damp_status update(bool kda, const damp_pool* pool, int32_t layer, const int32_t
   p.HV = pool->num_v_heads;
   p.k_hi = pool->layout.kind == DAMP_STATE_FP32 ? 0 : pool->layout.k_hi;
   p.o_bf16 = o_dtype == DAMP_DT_BF16;
+  p.had = pool->layout.hadamard;
   const int D = pool->layout.d_k;
   hipStream_t s = as_stream(stream);
   // the persistent kernel numbers the B * HV tiles with 32-bit integers
   const bool tiles_fit = static_cast<int64_t>(B) * p.HV <= INT32_MAX;
-  if (pool->layout.kind == DAMP_STATE_MIXED && D == 128 && p.k_hi <= 32 && tiles_fit) {
+  if (layout_is_default(&pool->layout) && D == 128 && p.k_hi <= 32 && tiles_fit) {
     if (!launch_stream128(kda, p, B, s))
       return fail(DAMP_ERR_HIP, "%s: occupancy query failed", name);
     return check_launch(name);
@@ -261,6 +282,9 @@ damp_status update(bool kda, const damp_pool* pool, int32_t layer, const int32_t
   if (pool->layout.kind == DAMP_STATE_FP32) {
     if (kda) launch_d<kFp32, true>(D, p, B, s);
     else launch_d<kFp32, false>(D, p, B, s);
+  } else if (layout_is_paper(&pool->layout)) {
+    if (kda) launch_d<kPaper, true>(D, p, B, s);
+    else launch_d<kPaper, false>(D, p, B, s);
   } else {
     if (kda) launch_d<kMixed, true>(D, p, B, s);
     else launch_d<kMixed, false>(D, p, B, s);

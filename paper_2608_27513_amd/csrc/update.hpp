@@ -25,6 +25,7 @@ struct UpdateParams {
   int32_t HV;
   int32_t k_hi;
   int32_t o_bf16;
+  int32_t had;  // block-32 Hadamard on the low tier (paper tiers only)
 };
 
 // The streaming kernel for d = 128 mixed tiles with k_hi <= 32 (update_stream.hip).

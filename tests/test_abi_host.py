@@ -50,6 +50,14 @@ def test_tile_geometry_matches_oracle(L, d):
             assert D.damp_tile_stride(lay) == orc.tile_stride(kind, d, d, ok)
             bits = D.damp_bits_per_value(lay)
             assert bits == orc.tile_bytes(kind, d, d, ok) * 8 / (d * d)
+    if d >= 32:  # the paper's tiers: groups of 32 along d_v
+        for k_hi in sorted({0, 8, d // 4, d}):
+            lay = D.damp_layout_init(d, d, k_hi, D.DAMP_STATE_MIXED)
+            lay.hi_dtype, lay.group, lay.meta_dtype, lay.hadamard = orc.FMT_PAPER
+            assert D.damp_tile_bytes(lay) == orc.tile_bytes(D.DAMP_STATE_MIXED, d, d, k_hi,
+                                                            orc.FMT_PAPER)
+            assert D.damp_tile_stride(lay) == orc.tile_stride(D.DAMP_STATE_MIXED, d, d, k_hi,
+                                                              orc.FMT_PAPER)
 
 
 def test_bits_per_value_of_the_paper_layout(L):
@@ -140,7 +148,7 @@ def test_update_validation_fails_before_launch(L):
 
 def test_layouts_without_kernels_are_reported(L):
     lay = D.damp_layout_init(128, 128, 16)
-    lay.group = 32  # the paper's group-32 low tier has no kernel
+    lay.group = 32  # groups of 32 with a BF16 tier and fp32 metadata: no kernel
     pool = _fake_pool(L, lay)
     p = ctypes.c_void_p(0x7f0000100000)
     st, msg = _status(L.damp_state_update_gdn, ctypes.byref(pool), 0, p, 4, 4, p, p, p, p, p,
@@ -151,6 +159,11 @@ def test_layouts_without_kernels_are_reported(L):
     lay = D.damp_layout_init(96, 96, 16)  # valid layout, no kernel width
     pool = _fake_pool(L, lay)
     st, _ = _status(L.damp_state_unpack, ctypes.byref(pool), 0, p, 4, None, p, None)
+    assert st == D.DAMP_ERR_UNSUPPORTED
+    lay = D.damp_layout_init(16, 16, 4)  # the paper's tiers need d_v >= 32
+    lay.hi_dtype, lay.group, lay.meta_dtype, lay.hadamard = (D.DAMP_DT_FP16, 16, D.DAMP_DT_FP16, 0)
+    pool = _fake_pool(L, lay)
+    st, _ = _status(L.damp_state_pack, ctypes.byref(pool), 0, p, 4, p, None, None)
     assert st == D.DAMP_ERR_UNSUPPORTED
 
 
