@@ -181,14 +181,18 @@ class Workload:
         self.step_inputs = [inputs.decode_inputs_device(gen, B, HK, HV, d, kda=kda, mu=self.mu)
                             for _ in range(4)]
 
-    def make_pool(self, kind: int, k_hi: int, rotations: int, scattered: bool = False):
+    def make_pool(self, kind: int, k_hi: int, rotations: int, scattered: bool = False,
+                  tiers=None):
         """A pool with `rotations` disjoint slot sets, each packed with the
         warm state (permuted by the selection). Set r is slots r*B .. r*B+B-1
         in order, or with `scattered` B slots drawn at random from the whole
-        pool, in random order."""
+        pool, in random order. `tiers` = (hi_dtype, group, meta_dtype,
+        hadamard) selects another storage format than the default."""
         torch, D = self.torch, self.D
         B, HV, d = self.B, self.HV, self.d
         layout = D.damp_layout_init(d, d, k_hi, kind)
+        if tiers is not None:
+            layout.hi_dtype, layout.group, layout.meta_dtype, layout.hadamard = tiers
         pool = D.Pool(layout, 1, B * rotations, HV)
         if scattered:
             order = torch.from_numpy(self.inputs.slot_order(7, B * rotations, B * rotations)).cuda()
@@ -235,8 +239,8 @@ def time_steps(torch, calls, warmup: int, steps: int):
 
 
 def measure(torch, D, wl: Workload, kind: int, k_hi: int, rotations: int, warmup: int,
-            steps: int, o_dtype, scattered: bool = False):
-    pool, sets, layout = wl.make_pool(kind, k_hi, rotations, scattered)
+            steps: int, o_dtype, scattered: bool = False, tiers=None):
+    pool, sets, layout = wl.make_pool(kind, k_hi, rotations, scattered, tiers)
     calls = wl.prepared(pool, sets, o_dtype)
     t = time_steps(torch, calls, warmup, steps)
     tb = D.damp_tile_bytes(layout)
@@ -435,6 +439,16 @@ def main():
         log(f"  uniform int8: {i8['us_per_step']:.1f} us/step, kernel {i8['kernel_us']:.1f} us")
         extra["baselines_gdn"] = {"fp32_state": fp, "uniform_int8": i8,
                                   "speedup_vs_fp32_state": fp["kernel_us"] / head["kernel_us"]}
+        # the paper's own tiers: FP16 rows, INT8 groups of 32 with FP16 (s, z)
+        paper = {}
+        for name, had in (("int8_h32", 1), ("int8_g32", 0)):
+            r = measure(torch, D, gdn, D.DAMP_STATE_MIXED, k_hi, args.rotations, args.warmup,
+                        args.steps, torch.bfloat16,
+                        tiers=(D.DAMP_DT_FP16, 32, D.DAMP_DT_FP16, had))
+            log(f"  paper tiers ({name}): kernel {r['kernel_us']:.1f} us, "
+                f"{r['kernel_gbs']:.0f} GB/s, {r['bits_per_value']} bits/value")
+            paper[name] = r
+        extra["paper_tiers_gdn"] = paper
         del gdn
         torch.cuda.empty_cache()
         log("setting up KDA B=256 H=32 d=128 K_hi=16")
