@@ -385,15 +385,62 @@ void orc_unpack(int kind, const int32_t* fmt, int dk, int dv, int k_hi, const ui
 /* ------------------------------------------------- decode-step update */
 
 /*
- * One decode step of one layer for B requests (section 3.1, Eq. (1)):
+ * One token of Eq. (1) on an fp32 state S[dk][dv] in tile-row order (row r
+ * holds key channel perm[h][r]):
  *   S_bar = Lambda S;  delta = v - S_bar^T k;  S = S_bar + beta k delta^T;
- *   o = scale * S^T q,  then S is stored per its tier (section 3.2).
- * GDN (is_kda = 0): Lambda = exp(g[b,h]) I. KDA: Lambda = diag(exp(g[b,h,:])).
- * All operands arrive in natural channel order; row r of a tile holds key
- * channel perm[h][r], so k, q and g are read through the permutation
- * (section 5.2). q, k, v, g, beta are bf16 bit patterns. o is fp32.
- * If pre_out is not NULL it receives the updated state before re-encoding,
- * [B, HV, dk, dv] in tile-row order (used for the error analysis of Eq. (5)).
+ *   o = scale * S^T q.
+ * GDN (is_kda = 0): Lambda = exp(g) I with one g. KDA: Lambda = diag(exp(g)).
+ * kb, qb, gb (KDA) are the d_k bf16 operands in natural channel order, so they
+ * are read through the permutation (section 5.2); vb has d_v values.
+ */
+static void orc_step(int is_kda, int dk, int dv, const uint8_t* perm, int h, float* S,
+                     const uint16_t* kb, const uint16_t* qb, const uint16_t* gb,
+                     uint16_t beta_bits, const uint16_t* vb, float scale, float* ob) {
+  float* kp = (float*)malloc((size_t)dk * sizeof(float));
+  float* qp = (float*)malloc((size_t)dk * sizeof(float));
+  float* a = (float*)malloc((size_t)dk * sizeof(float));
+  float* delta = (float*)malloc((size_t)dv * sizeof(float));
+  for (int r = 0; r < dk; ++r) {
+    int u = orc_perm_at(perm, h, dk, r);
+    kp[r] = orc_from_bf16(kb[u]);
+    qp[r] = orc_from_bf16(qb[u]);
+    a[r] = expf(orc_from_bf16(is_kda ? gb[u] : gb[0]));
+  }
+  float bt = orc_from_bf16(beta_bits);
+
+  /* decay: S_bar = Lambda S */
+  for (int r = 0; r < dk; ++r)
+    for (int j = 0; j < dv; ++j) S[(size_t)r * dv + j] = a[r] * S[(size_t)r * dv + j];
+
+  /* key read-out and residual: delta = v - S_bar^T k */
+  for (int j = 0; j < dv; ++j) {
+    float acc = 0.0f;
+    for (int r = 0; r < dk; ++r) acc = acc + kp[r] * S[(size_t)r * dv + j];
+    delta[j] = orc_from_bf16(vb[j]) - acc;
+  }
+
+  /* rank-1 delta update: S = S_bar + beta k delta^T */
+  for (int r = 0; r < dk; ++r) {
+    float bk = bt * kp[r];
+    for (int j = 0; j < dv; ++j) S[(size_t)r * dv + j] = S[(size_t)r * dv + j] + bk * delta[j];
+  }
+
+  /* read-out of the updated state: o = scale * S^T q */
+  for (int j = 0; j < dv; ++j) {
+    float acc = 0.0f;
+    for (int r = 0; r < dk; ++r) acc = acc + qp[r] * S[(size_t)r * dv + j];
+    ob[j] = scale * acc;
+  }
+  free(kp); free(qp); free(a); free(delta);
+}
+
+/*
+ * One decode step of one layer for B requests (section 3.1, Eq. (1)): the
+ * tile is decoded, updated by one token (orc_step) and stored per its tier
+ * (section 3.2). q, k: bf16 [B, HK, dk]; v: [B, HV, dv]; g: [B, HV] (GDN) or
+ * [B, HV, dk] (KDA); beta: [B, HV]; o fp32 [B, HV, dv]. If pre_out is not
+ * NULL it receives the updated state before re-encoding, [B, HV, dk, dv] in
+ * tile-row order (used for the error analysis of Eq. (5)).
  */
 void orc_update(int is_kda, int kind, const int32_t* fmt, int dk, int dv, int k_hi,
                 uint8_t* pool, int64_t slot_stride, int64_t tile_stride, int num_slots,
@@ -416,58 +463,55 @@ void orc_update(int is_kda, int kind, const int32_t* fmt, int dk, int dv, int k_
     }
     uint8_t* tile = pool + (size_t)slot * slot_stride + (size_t)h * tile_stride;
     float* S = (float*)malloc((size_t)dk * dv * sizeof(float));
-    float* kp = (float*)malloc((size_t)dk * sizeof(float));
-    float* qp = (float*)malloc((size_t)dk * sizeof(float));
-    float* a = (float*)malloc((size_t)dk * sizeof(float));
-    float* w = (float*)malloc((size_t)dv * sizeof(float));
-    float* delta = (float*)malloc((size_t)dv * sizeof(float));
-
-    /* operands in tile-row order */
-    const uint16_t* kb = k + ((size_t)b * HK + hk) * dk;
-    const uint16_t* qb = q + ((size_t)b * HK + hk) * dk;
-    for (int r = 0; r < dk; ++r) {
-      int u = orc_perm_at(perm, h, dk, r);
-      kp[r] = orc_from_bf16(kb[u]);
-      qp[r] = orc_from_bf16(qb[u]);
-      float gu = is_kda ? orc_from_bf16(g[((size_t)b * HV + h) * dk + u])
-                        : orc_from_bf16(g[(size_t)b * HV + h]);
-      a[r] = expf(gu);
-    }
-    float bt = orc_from_bf16(beta[(size_t)b * HV + h]);
-    const uint16_t* vb = v + ((size_t)b * HV + h) * dv;
-
-    /* dequantize, then decay: S_bar = Lambda S */
     orc_tile_decode(kind, f, dk, dv, k_hi, tile, S);
-    for (int r = 0; r < dk; ++r)
-      for (int j = 0; j < dv; ++j) S[(size_t)r * dv + j] = a[r] * S[(size_t)r * dv + j];
-
-    /* key read-out and residual: delta = v - S_bar^T k */
-    for (int j = 0; j < dv; ++j) {
-      float acc = 0.0f;
-      for (int r = 0; r < dk; ++r) acc = acc + kp[r] * S[(size_t)r * dv + j];
-      w[j] = acc;
-      delta[j] = orc_from_bf16(vb[j]) - w[j];
-    }
-
-    /* rank-1 delta update: S = S_bar + beta k delta^T */
-    for (int r = 0; r < dk; ++r) {
-      float bk = bt * kp[r];
-      for (int j = 0; j < dv; ++j) S[(size_t)r * dv + j] = S[(size_t)r * dv + j] + bk * delta[j];
-    }
-
-    /* read-out of the updated state: o = scale * S^T q */
-    for (int j = 0; j < dv; ++j) {
-      float acc = 0.0f;
-      for (int r = 0; r < dk; ++r) acc = acc + qp[r] * S[(size_t)r * dv + j];
-      ob[j] = scale * acc;
-    }
-
+    const uint16_t* gb = is_kda ? g + ((size_t)b * HV + h) * dk : g + (size_t)b * HV + h;
+    orc_step(is_kda, dk, dv, perm, h, S, k + ((size_t)b * HK + hk) * dk,
+             q + ((size_t)b * HK + hk) * dk, gb, beta[(size_t)b * HV + h],
+             v + ((size_t)b * HV + h) * dv, scale, ob);
     if (pre_out) memcpy(pre_out + (size_t)t * dk * dv, S, (size_t)dk * dv * sizeof(float));
-
     /* store: the high tier rounded, Eq. (3) per low-tier group */
     orc_tile_encode(kind, f, dk, dv, k_hi, S, tile);
+    free(S);
+  }
+}
 
-    free(S); free(kp); free(qp); free(a); free(w); free(delta);
+/*
+ * Prefill of one chunk of T tokens per request (App. A.5, prefill path): the
+ * tile is decoded once, the recurrence runs in fp32 for t = 0 .. T-1
+ * (orc_step, o_t from the state updated by token t), and only the state after
+ * the last token is stored per its tier. Inputs carry a token axis after the
+ * request axis: q, k [B, T, HK, dk]; v [B, T, HV, dv]; g [B, T, HV] (GDN) or
+ * [B, T, HV, dk] (KDA); beta [B, T, HV]; o fp32 [B, T, HV, dv].
+ */
+void orc_prefill(int is_kda, int kind, const int32_t* fmt, int dk, int dv, int k_hi,
+                 uint8_t* pool, int64_t slot_stride, int64_t tile_stride, int num_slots,
+                 const int32_t* slot_idx, int B, int T, int HK, int HV, const uint16_t* q,
+                 const uint16_t* k, const uint16_t* v, const uint16_t* g,
+                 const uint16_t* beta, const uint8_t* perm, float scale, float* o) {
+  const orc_fmt_t f = orc_fmt(fmt, dv);
+  int64_t ntiles = (int64_t)B * HV;
+  int group = HV / HK;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t ti = 0; ti < ntiles; ++ti) {
+    int b = (int)(ti / HV), h = (int)(ti % HV);
+    int hk = h / group;
+    int slot = slot_idx[b];
+    if (slot < 0 || slot >= num_slots) {
+      for (int t = 0; t < T; ++t)
+        memset(o + (((size_t)b * T + t) * HV + h) * dv, 0, (size_t)dv * sizeof(float));
+      continue;
+    }
+    uint8_t* tile = pool + (size_t)slot * slot_stride + (size_t)h * tile_stride;
+    float* S = (float*)malloc((size_t)dk * dv * sizeof(float));
+    orc_tile_decode(kind, f, dk, dv, k_hi, tile, S);
+    for (int t = 0; t < T; ++t) {
+      size_t bt = (size_t)b * T + t;
+      const uint16_t* gb = is_kda ? g + (bt * HV + h) * dk : g + bt * HV + h;
+      orc_step(is_kda, dk, dv, perm, h, S, k + (bt * HK + hk) * dk, q + (bt * HK + hk) * dk, gb,
+               beta[bt * HV + h], v + (bt * HV + h) * dv, scale, o + (bt * HV + h) * dv);
+    }
+    orc_tile_encode(kind, f, dk, dv, k_hi, S, tile);
+    free(S);
   }
 }
 

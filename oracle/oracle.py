@@ -10,6 +10,7 @@ marshals numpy arrays. It also keeps its own description of the packed pool
 
 Every function cites the passage it follows:
   update      section 3.1 Eq. (1)-(2); section 3.2; App. A.5 (fused executor)
+  prefill     App. A.5 (prefill path); section 3.1 Eq. (1)
   quant_row   section 3.2 Eq. (3); App. A.1 (integer formats)
   pack/unpack section 5.2; App. A.5 Eq. (17); App. A.1 (storage formats)
   select      section 5.1 Eq. (8)-(10); App. A.2 Eq. (13)-(15); Alg. 1
@@ -81,6 +82,8 @@ def lib():
         L.orc_update.argtypes = [i32, i32, vp, i32, i32, i32, vp, i64, i64, i32, vp, i32, i32,
                                  i32, vp, vp, vp, vp, vp, vp, f32, vp, vp]
         L.orc_reset.argtypes = [i32, vp, i32, i32, i32, vp, i64, i64, i32, vp, i32, i32]
+        L.orc_prefill.argtypes = [i32, i32, vp, i32, i32, i32, vp, i64, i64, i32, vp, i32, i32,
+                                  i32, i32, vp, vp, vp, vp, vp, vp, f32, vp]
         L.orc_select.argtypes = [i32, i32, i32, i32, i32, vp, vp, i32, f64, vp, vp, vp, vp, vp]
         L.orc_select.restype = i32
         _lib = L
@@ -284,6 +287,30 @@ def update(pool: Pool, layer: int, slot_idx, *, kda: bool, q, k, v, g, beta, per
                      pool.hv, _p(q), _p(k), _p(v), _p(g), _p(beta), _p(perm), float(scale),
                      _p(o), _p(pre))
     return (o, pre) if want_pre else o
+
+
+def prefill(pool: Pool, layer: int, slot_idx, *, kda: bool, q, k, v, g, beta, perm=None,
+            scale: float = 1.0):
+    """One chunk of T tokens per request (App. A.5, prefill path), in place:
+    decode once, T fp32 steps of Eq. (1), encode once. q, k: bf16 bits
+    [B, T, HK, dk]; v: [B, T, HV, dv]; g: [B, T, HV] (GDN) or [B, T, HV, dk]
+    (KDA); beta: [B, T, HV]. Returns o fp32 [B, T, HV, dv]."""
+    slot_idx = _i32(slot_idx)
+    B = slot_idx.size
+    u16 = lambda a: np.ascontiguousarray(a, dtype=np.uint16)
+    q, k, v, g, beta = u16(q), u16(k), u16(v), u16(g), u16(beta)
+    T, HK = q.shape[1], q.shape[2]
+    assert q.shape == (B, T, HK, pool.dk) and k.shape == q.shape
+    assert v.shape == (B, T, pool.hv, pool.dv) and beta.shape == (B, T, pool.hv)
+    assert g.shape == ((B, T, pool.hv, pool.dk) if kda else (B, T, pool.hv))
+    assert pool.hv % HK == 0
+    perm = None if perm is None else np.ascontiguousarray(perm, dtype=np.uint8)
+    o = np.empty((B, T, pool.hv, pool.dv), np.float32)
+    lib().orc_prefill(int(kda), pool.kind, _p(pool._fmt), pool.dk, pool.dv, pool.k_hi,
+                      pool.layer_ptr(layer), pool.slot_stride, pool.tile_stride, pool.num_slots,
+                      _p(slot_idx), B, T, HK, pool.hv, _p(q), _p(k), _p(v), _p(g), _p(beta),
+                      _p(perm), float(scale), _p(o))
+    return o
 
 
 def select(*, kda: bool, states, log_decay, k_hi: int, tau: float = 1e-4) -> dict:

@@ -74,6 +74,12 @@ def step(inp: dict, t: int) -> dict:
     return {name: np.ascontiguousarray(a[t]) for name, a in inp.items()}
 
 
+def as_prefill(inp: dict) -> dict:
+    """Step-major inputs [T, B, ...] as one prefill chunk per request
+    [B, T, ...] (the same values)."""
+    return {name: np.ascontiguousarray(np.swapaxes(a, 0, 1)) for name, a in inp.items()}
+
+
 def outlier_channels(seed: int, hv: int, d: int, n: int = 8) -> np.ndarray:
     """n distinct key channels per head, int32 [hv, n], ascending."""
     rng = np.random.default_rng([seed, 0x6f75])
