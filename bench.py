@@ -364,6 +364,44 @@ def multilayer(torch, D, inputs, steps: int, log=print):
     return res
 
 
+def prefill_bench(torch, D, inputs, steps: int, log=print, T: int = 64):
+    """Prefill of one T-token chunk per request (App. A.5, prefill path) on
+    the B=256 GDN workload (16 key / 32 value heads, d=128, 16 BF16 rows):
+    decode the stored state once, T fp32 steps, store once. Reports tokens per
+    second and the fp32 rate (7 flops per state value and token: decay, two
+    read-outs, the update), against the vector fp32 peak."""
+    B, HK, HV, d, k_hi = 256, 16, 32, 128, 16
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(11)
+    steps_in = [inputs.decode_inputs_device(gen, B, HK, HV, d) for _ in range(T)]
+    x = {name: torch.stack([s_[name] for s_ in steps_in], dim=1).contiguous()
+         for name in steps_in[0]}
+    del steps_in
+    perm = torch.from_numpy(inputs.random_perms(12, HV, d)).cuda()
+    layout = D.damp_layout_init(d, d, k_hi)
+    rot = 2
+    pool = D.Pool(layout, 1, B * rot, HV)
+    S = torch.randn((B, HV, d, d), generator=gen, device="cuda") * 0.1
+    sets = [torch.arange(r * B, (r + 1) * B, dtype=torch.int32, device="cuda") for r in range(rot)]
+    for sl in sets:
+        D.damp_state_pack(pool, 0, sl, S, perm)
+    del S
+    o = torch.empty((B, T, HV, d), dtype=torch.bfloat16, device="cuda")
+    calls = [lambda sl=sl: D.damp_state_prefill_gdn(pool, 0, sl, x["q"], x["k"], x["v"], x["g"],
+                                                    x["beta"], perm=perm, o=o) for sl in sets]
+    t = time_steps(torch, calls, 3, steps)
+    sec = t["mean_launch_s"]
+    flops = 7.0 * d * d * B * HV * T
+    res = dict(B=B, T=T, HK=HK, HV=HV, d=d, k_hi=k_hi, chunk_us=round(1e6 * sec, 1),
+               tokens_per_s=round(B * T / sec), tflops=round(flops / sec / 1e12, 2),
+               frac_fp32_vector_peak=round(flops / sec / 157.3e12, 4))
+    log(f"  prefill T={T}: {res['chunk_us']} us per chunk, {res['tokens_per_s']:.3g} tokens/s, "
+        f"{res['tflops']} TFLOP/s")
+    del pool, x, o
+    torch.cuda.empty_cache()
+    return res
+
+
 def cpu_baseline(seconds: float, log=print):
     """The CPU oracle on config 2 (B=256, 16/32 heads, d=128, 16 BF16 rows),
     timed on the host: as many whole decode steps as fit in `seconds`."""
@@ -469,6 +507,7 @@ def main():
             extra["sweep"] = sweep(torch, D, inputs, 50, log=log)
         if not args.no_multilayer:
             extra["multilayer_48"] = multilayer(torch, D, inputs, 64, log=log)
+        extra["prefill_gdn"] = prefill_bench(torch, D, inputs, 10, log=log)
 
     cpu = None
     if not args.quick and not args.no_cpu:

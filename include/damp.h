@@ -207,6 +207,37 @@ damp_status damp_state_update_kda(const damp_pool* pool, int32_t layer,
                                   const uint8_t* perm, float scale, void* o,
                                   int32_t o_dtype, void* stream);
 
+/* Prefill of one chunk of T tokens per request (App. A.5, prefill path): the
+ * stored state of every (request, value head) is decoded once, the
+ * recurrence of Eq. (1) runs in fp32 for the T tokens in order (o of each
+ * token read from the state that token updated, as in the decode step), and
+ * only the chunk-final state is stored back per the layout, so the chunk's
+ * intermediate states are never quantized. Arguments as for
+ * damp_state_update_gdn, with a token axis after the request axis:
+ *  T          tokens per request in this chunk (0 is a no-op).
+ *  q, k       bf16 [B, T, HK, d_k];  v  bf16 [B, T, HV, d_v];
+ *  g          bf16 [B, T, HV] (GDN) or [B, T, HV, d_k] (KDA): log-decay;
+ *  beta       bf16 [B, T, HV];  o  [B, T, HV, d_v] in o_dtype.
+ * A padded request (slot outside the pool) gets o = 0 for every token.
+ * DAMP_ERR_INVALID_ARG also for T < 0. */
+damp_status damp_state_prefill_gdn(const damp_pool* pool, int32_t layer,
+                                   const int32_t* slot_idx, int32_t B, int32_t T,
+                                   int32_t num_k_heads, const uint16_t* q,
+                                   const uint16_t* k, const uint16_t* v,
+                                   const uint16_t* g, const uint16_t* beta,
+                                   const uint8_t* perm, float scale, void* o,
+                                   int32_t o_dtype, void* stream);
+
+/* KDA prefill: as damp_state_prefill_gdn with the per-key-channel decay of
+ * damp_state_update_kda (g is [B, T, HV, d_k]). */
+damp_status damp_state_prefill_kda(const damp_pool* pool, int32_t layer,
+                                   const int32_t* slot_idx, int32_t B, int32_t T,
+                                   int32_t num_k_heads, const uint16_t* q,
+                                   const uint16_t* k, const uint16_t* v,
+                                   const uint16_t* g, const uint16_t* beta,
+                                   const uint8_t* perm, float scale, void* o,
+                                   int32_t o_dtype, void* stream);
+
 /* Packs natural-order fp32 states into pool tiles (the persistent
  * representation of Eq. (17)): tile row r receives S[b,h,perm[h,r],:],
  * stored in the tier row r belongs to.

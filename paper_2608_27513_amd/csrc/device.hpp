@@ -318,4 +318,61 @@ __device__ __forceinline__ void encode_row(const float* x, int r, int k_hi, int 
   }
 }
 
+// ------------------------------------------------------------- row decode
+
+// Loads and decodes one row slice (columns col0 .. col0 + CPT of tile row r)
+// into fp32: the high tier widened, the low tier as s * (c - z) (then the
+// inverse transform for the paper tiers with had). Lanes of a row take the
+// same branch (r is uniform across them).
+template <int KIND, int D, int CPT>
+__device__ __forceinline__ void decode_row(const uint8_t* tile, const uint8_t* codes,
+                                           const uint8_t* meta_bytes, int r, int k_hi, int cg,
+                                           int col0, bool had, float* x) {
+  if (KIND == kFp32) {
+    uint32_t w[CPT];
+    load_words<CPT * 4>(tile + (static_cast<size_t>(r) * D + col0) * 4, w);
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) x[j] = __uint_as_float(w[j]);
+    return;
+  }
+  if (r < k_hi) {
+    uint32_t w[CPT / 2];
+    load_words<CPT * 2>(tile + (static_cast<size_t>(r) * D + col0) * 2, w);
+#pragma unroll
+    for (int j = 0; j < CPT / 2; ++j) {
+      x[2 * j] = KIND == kPaper ? f16_lo(w[j]) : bf16_lo(w[j]);
+      x[2 * j + 1] = KIND == kPaper ? f16_hi(w[j]) : bf16_hi(w[j]);
+    }
+    return;
+  }
+  const int l = r - k_hi;
+  uint32_t w[CPT / 4];
+  load_words<CPT>(codes + static_cast<size_t>(l) * D + col0, w);
+  float s, z;
+  if constexpr (KIND == kPaper) {
+    const uint32_t m =
+        reinterpret_cast<const uint32_t*>(meta_bytes)[static_cast<size_t>(l) * (D / 32) + (col0 >> 5)];
+    s = f16_lo(m);
+    z = f16_hi(m);
+  } else {
+    const float2 sz = reinterpret_cast<const float2*>(meta_bytes)[l];
+    s = sz.x;
+    z = sz.y;
+  }
+  // s * (c - z) as one FMA per value, with the transform's normalization
+  // folded into the factor
+  const float A = s * ((KIND == kPaper && had) ? kInvSqrt32 : 1.0f);
+  const float B0 = -A * z;
+#pragma unroll
+  for (int j = 0; j < CPT / 4; ++j) {
+    x[4 * j + 0] = fmaf(A, ubyte<0>(w[j]), B0);
+    x[4 * j + 1] = fmaf(A, ubyte<1>(w[j]), B0);
+    x[4 * j + 2] = fmaf(A, ubyte<2>(w[j]), B0);
+    x[4 * j + 3] = fmaf(A, ubyte<3>(w[j]), B0);
+  }
+  if constexpr (KIND == kPaper && CPT == 16) {
+    if (had) fwht32_pair(reinterpret_cast<float(&)[16]>(*x), (cg & 1) != 0);
+  }
+}
+
 }  // namespace damp

@@ -41,8 +41,9 @@ class damp_pool(ctypes.Structure):
 
 EXPORTS = ("damp_layout_init", "damp_tile_bytes", "damp_tile_stride", "damp_bits_per_value",
            "damp_pool_required_bytes", "damp_pool_init", "damp_pool_reset_slots",
-           "damp_state_update_gdn", "damp_state_update_kda", "damp_state_pack",
-           "damp_state_unpack", "damp_select_channels", "damp_last_error")
+           "damp_state_update_gdn", "damp_state_update_kda", "damp_state_prefill_gdn",
+           "damp_state_prefill_kda", "damp_state_pack", "damp_state_unpack",
+           "damp_select_channels", "damp_last_error")
 
 _lib = None
 
@@ -69,6 +70,10 @@ def lib() -> ctypes.CDLL:
         "damp_pool_reset_slots": (st, [PP, i32, P, i32, P]),
         "damp_state_update_gdn": (st, [PP, i32, P, i32, i32, P, P, P, P, P, P, f32, P, i32, P]),
         "damp_state_update_kda": (st, [PP, i32, P, i32, i32, P, P, P, P, P, P, f32, P, i32, P]),
+        "damp_state_prefill_gdn": (st, [PP, i32, P, i32, i32, i32, P, P, P, P, P, P, f32, P, i32,
+                                        P]),
+        "damp_state_prefill_kda": (st, [PP, i32, P, i32, i32, i32, P, P, P, P, P, P, f32, P, i32,
+                                        P]),
         "damp_state_pack": (st, [PP, i32, P, i32, P, P, P]),
         "damp_state_unpack": (st, [PP, i32, P, i32, P, P, P]),
         "damp_select_channels": (st, [i32, i32, i32, i32, i32, P, P, i32, f64, P, P, P, P]),
@@ -224,6 +229,51 @@ def damp_state_update_kda(pool: Pool, layer: int, slot_idx, q, k, v, g, beta, pe
         o = torch.empty((slot_idx.numel(), pool.num_v_heads, pool.d), dtype=torch.float32,
                         device=pool.buffer.device)
     return _update(True, pool, layer, slot_idx, q, k, v, g, beta, perm, scale, o, stream)
+
+
+def _prefill(kda: bool, pool: Pool, layer: int, slot_idx, q, k, v, g, beta, perm, scale, o,
+             stream):
+    d = pool.d
+    HV = pool.num_v_heads
+    slot_idx = _dev(slot_idx, torch.int32, "slot_idx")
+    B = slot_idx.numel()
+    if q.dim() != 4:
+        raise ValueError("q must be [B, T, HK, d]")
+    T, HK = q.shape[1], q.shape[2]
+    _dev(q, torch.bfloat16, "q", (B, T, HK, d))
+    _dev(k, torch.bfloat16, "k", (B, T, HK, d))
+    _dev(v, torch.bfloat16, "v", (B, T, HV, d))
+    _dev(g, torch.bfloat16, "g", (B, T, HV, d) if kda else (B, T, HV))
+    _dev(beta, torch.bfloat16, "beta", (B, T, HV))
+    if perm is not None:
+        _dev(perm, torch.uint8, "perm", (HV, d))
+    if o is None:
+        o = torch.empty((B, T, HV, d), dtype=torch.float32, device=pool.buffer.device)
+    if o.dtype == torch.float32:
+        o_dt = DAMP_DT_FP32
+    elif o.dtype == torch.bfloat16:
+        o_dt = DAMP_DT_BF16
+    else:
+        raise ValueError("o must be float32 or bfloat16")
+    _dev(o, o.dtype, "o", (B, T, HV, d))
+    fn = lib().damp_state_prefill_kda if kda else lib().damp_state_prefill_gdn
+    _check(fn(ctypes.byref(pool.desc), layer, _ptr(slot_idx), B, T, HK, _ptr(q), _ptr(k), _ptr(v),
+              _ptr(g), _ptr(beta), _ptr(perm), float(scale), _ptr(o), o_dt, _stream(stream)))
+    return o
+
+
+def damp_state_prefill_gdn(pool: Pool, layer: int, slot_idx, q, k, v, g, beta, perm=None,
+                           scale: float = 1.0, o=None, stream=None):
+    """One GDN prefill chunk in place on the pool (inputs [B, T, ...]);
+    returns o [B, T, HV, d]."""
+    return _prefill(False, pool, layer, slot_idx, q, k, v, g, beta, perm, scale, o, stream)
+
+
+def damp_state_prefill_kda(pool: Pool, layer: int, slot_idx, q, k, v, g, beta, perm=None,
+                           scale: float = 1.0, o=None, stream=None):
+    """One KDA prefill chunk in place on the pool (inputs [B, T, ...]);
+    returns o [B, T, HV, d]."""
+    return _prefill(True, pool, layer, slot_idx, q, k, v, g, beta, perm, scale, o, stream)
 
 
 # ----------------------------------------------------------- pack / unpack

@@ -69,8 +69,12 @@ def split_tiles(buf: np.ndarray, pool: "orc.Pool"):
     return hi, codes, meta[..., 0], meta[..., 1]
 
 
-def compare_tiles(gpu_buf: np.ndarray, ref: "orc.Pool", label: str = "") -> dict:
-    """Field-by-field comparison; asserts the acceptance bar and returns stats."""
+def compare_tiles(gpu_buf: np.ndarray, ref: "orc.Pool", label: str = "",
+                  s16_exact_min: float = CODE_FRAC) -> dict:
+    """Field-by-field comparison; asserts the acceptance bar and returns stats.
+    s16_exact_min: fraction of FP16 scales that must match exactly (the rest
+    within one FP16 step); lower after several fp32 steps, whose rounding
+    differences move more scales across an FP16 rounding boundary."""
     if ref.kind == orc.KIND_FP32:
         a = split_tiles(gpu_buf, ref)
         b = split_tiles(ref.buf, ref)
@@ -104,7 +108,7 @@ def compare_tiles(gpu_buf: np.ndarray, ref: "orc.Pool", label: str = "") -> dict
             # its FP16 rounding, by one FP16 step (2^-10 relative)
             stats["s_exact"] = float((sa[live] == sb[live]).mean()) if rel.size else 1.0
             assert stats["s_rel_max"] <= 2.0 ** -10 * 1.0001, f"{label}: scales {stats}"
-            assert stats["s_exact"] >= CODE_FRAC, f"{label}: scales {stats}"
+            assert stats["s_exact"] >= s16_exact_min, f"{label}: scales {stats}"
     return stats
 
 

@@ -34,7 +34,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = declared_functions()
-    assert len(names) == 13
+    assert len(names) == 15
     for n in names:
         assert hasattr(L, n), n
     assert sorted(D.EXPORTS) == names
@@ -144,6 +144,28 @@ def test_update_validation_fails_before_launch(L):
         a[5] = None  # q
         assert fn(*a) == D.DAMP_ERR_INVALID_ARG
         assert fn(None, *args[1:]) == D.DAMP_ERR_INVALID_ARG
+
+
+def test_prefill_validation_fails_before_launch(L):
+    lay = D.damp_layout_init(64, 64, 8)
+    pool = _fake_pool(L, lay)
+    p = ctypes.c_void_p(0x7f0000100000)  # never dereferenced
+    for fn in (L.damp_state_prefill_gdn, L.damp_state_prefill_kda):
+        args = [ctypes.byref(pool), 0, p, 4, 3, 4, p, p, p, p, p, p, 1.0, p, D.DAMP_DT_FP32, None]
+        bad = dict(layer=(1, 2), B=(3, -1), T=(4, -2), hk=(5, 3), odt=(14, 7))
+        for name, (i, val) in bad.items():
+            a = list(args)
+            a[i] = val
+            st, msg = _status(fn, *a)
+            assert st == D.DAMP_ERR_INVALID_ARG, name
+            assert msg
+        for i in (3, 4):  # B = 0 or T = 0 is a no-op
+            a = list(args)
+            a[i] = 0
+            assert fn(*a) == D.DAMP_OK
+        a = list(args)
+        a[10] = None  # beta
+        assert fn(*a) == D.DAMP_ERR_INVALID_ARG
 
 
 def test_layouts_without_kernels_are_reported(L):
