@@ -403,7 +403,7 @@ def prefill_bench(torch, D, inputs, steps: int, log=print, T: int = 64):
 
 
 def cpu_baseline(seconds: float, log=print):
-    """The CPU oracle on config 2 (B=256, 16/32 heads, d=128, 16 BF16 rows),
+    """The CPU oracle on the GDN workload (B=256, 16/32 heads, d=128, 16 BF16 rows),
     timed on the host: as many whole decode steps as fit in `seconds`."""
     import numpy as np
 
@@ -438,7 +438,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the state update has no "
-              "cross-GPU step; see DESIGN.md for how it shards.", file=sys.stderr)
+              "cross-GPU step (tiles shard by value heads or request slots with no collective).", file=sys.stderr)
         sys.exit(2)
     log = lambda *a: print(*a, file=sys.stderr, flush=True)
     import torch

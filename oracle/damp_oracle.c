@@ -13,7 +13,7 @@
  * App. A.2 in double on the host. An independent fp64 brute force of the
  * recurrence lives in brute.py and pins this file.
  *
- * Readings taken where the paper is silent (each is listed in the design doc):
+ * Readings taken where the paper is silent:
  *  - round() in Eq. (3) is round-half-to-even (rintf), for z and for codes;
  *    codes saturate to [0, 255] (App. A.1); z is not clamped.
  *  - A row whose scale s is not a normal fp32 number (a constant row) uses

@@ -1,7 +1,7 @@
 """Full-size GPU parity in the launch configuration the benchmark times.
 
-Config 2 (GDN: B=256, 16 key / 32 value heads, d=128, 16 BF16 rows, 8 outlier
-channels per head at 10x) and config 3 (KDA: B=256, 32 heads, per-channel
+The GDN workload (B=256, 16 key / 32 value heads, d=128, 16 BF16 rows, 8
+outlier channels per head at 10x) and the KDA workload (B=256, 32 heads, per-channel
 decay with ~10% persistent channels, 16 channels chosen by the selection).
 The oracle packs every tile and runs the whole step, so every output and
 every stored byte is compared. Also the largest batch a launch takes and the
