@@ -402,6 +402,54 @@ def prefill_bench(torch, D, inputs, steps: int, log=print, T: int = 64):
     return res
 
 
+def calibration_bench(torch, D, inputs, log=print, T: int = 2048, stride: int = 8):
+    """On-device calibration on the KDA workload (App. A.2-A.4): a T-token
+    FP32 calibration sequence per split (one request, 32 heads, d=128), the
+    state write after every `stride` tokens folded into the accumulators,
+    then Alg. 1. Two disjoint splits (different sequences) give the
+    calibration-split agreement of App. B: mean top-16 overlap and mean
+    Spearman correlation of the scores over heads."""
+    HV, d, k_hi = 32, 128, 16
+    dev = "cuda"
+    mu = torch.from_numpy(inputs.kda_mu(1, HV, d)).to(dev)
+    res = {}
+    for name, tiers in (("int8_h32", (D.DAMP_DT_FP16, 32, D.DAMP_DT_FP16, 1)),
+                        ("int8_rows", None)):
+        lo = D.damp_layout_init(d, d, 0)
+        if tiers is not None:
+            lo.hi_dtype, lo.group, lo.meta_dtype, lo.hadamard = tiers
+        picks, scores, times = [], [], []
+        for split in range(2):
+            gen = torch.Generator(device=dev)
+            gen.manual_seed(100 + split)
+            steps = [inputs.decode_inputs_device(gen, 1, HV, HV, d, kda=True, mu=mu)
+                     for _ in range(T)]
+            x = {n: torch.stack([st[n] for st in steps], dim=1).contiguous() for n in steps[0]}
+            del steps
+            pool = D.Pool(D.damp_layout_init(d, d, 0, D.DAMP_STATE_FP32), 1, 1, HV)
+            slots = torch.zeros(1, dtype=torch.int32, device=dev)
+            cal = D.Calib(lo, kda=True, num_heads=HV)
+            D.damp_pool_reset_slots(pool, 0, slots)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            D.damp_calibrate_sequence(cal, 0, pool, 0, slots, x["q"], x["k"], x["v"], x["g"],
+                                      x["beta"], stride=stride)
+            r = D.damp_calib_finalize(cal, k_hi)  # synchronises
+            times.append(time.perf_counter() - t0)
+            picks.append(r["sel"].numpy())
+            scores.append(r["score"].numpy())
+            del pool, cal, x
+        overlap = float(sum(D.damp_topk_overlap(picks[0][h], picks[1][h]) for h in range(HV)) / HV)
+        rho = float(sum(D.damp_spearman(scores[0][h], scores[1][h]) for h in range(HV)) / HV)
+        res[name] = dict(T=T, stride=stride, samples=T // stride, heads=HV, d=d,
+                         ms=round(1e3 * min(times), 2), split_overlap=round(overlap, 4),
+                         split_spearman=round(rho, 4))
+        log(f"  calibration ({name}): {res[name]['ms']} ms for {T} tokens x {HV} heads, "
+            f"split overlap {overlap:.3f}, Spearman {rho:.3f}")
+    torch.cuda.empty_cache()
+    return res
+
+
 def cpu_baseline(seconds: float, log=print):
     """The CPU oracle on the GDN workload (B=256, 16/32 heads, d=128, 16 BF16 rows),
     timed on the host: as many whole decode steps as fit in `seconds`."""
@@ -508,6 +556,7 @@ def main():
         if not args.no_multilayer:
             extra["multilayer_48"] = multilayer(torch, D, inputs, 64, log=log)
         extra["prefill_gdn"] = prefill_bench(torch, D, inputs, 10, log=log)
+        extra["calibration_kda"] = calibration_bench(torch, D, inputs, log=log)
 
     cpu = None
     if not args.quick and not args.no_cpu:

@@ -13,7 +13,8 @@
  *    damp_select_channels (freed before it returns).
  *  - Calls taking `stream` (a hipStream_t passed as void*, NULL = the null
  *    stream) only enqueue work and return without synchronising, except
- *    damp_select_channels, which synchronises `stream`.
+ *    damp_select_channels and damp_calib_finalize, which synchronise
+ *    `stream`.
  *  - Arguments are validated on the host before anything is enqueued. A
  *    failed validation returns DAMP_ERR_INVALID_ARG (or DAMP_ERR_UNSUPPORTED
  *    for a valid layout that has no kernel) and touches no memory; the
@@ -285,6 +286,135 @@ damp_status damp_select_channels(int32_t is_kda, int32_t N, int32_t H,
                                  double tau, int32_t* sel_out,
                                  uint8_t* perm_out, double* score_out,
                                  void* stream);
+
+/* ------------------------------------------------------------------------
+ * On-device calibration (App. A.2, Eq. (13)-(15); Alg. 1 in App. A.4; the
+ * key-channel selector ablation of section 6; the calibration-split
+ * agreement of App. B).
+ *
+ * The reference (FP32) trajectory runs in an FP32 pool; every sampled state
+ * write is folded into double accumulators, one set per calibration domain,
+ * for each head h and key channel u:
+ *   err  += || Q_lo(S[h,u,:]) - S[h,u,:] ||^2     (Eq. (14))
+ *   en   += || S[h,u,:] ||^2                      (the state-energy selector)
+ *   loga += log a[h,u] of the sampled token       (Eq. (15))
+ *   count += 1 per sampled request
+ * Q_lo is the low tier of `lo` (default tiers: one fp32 (s, z) per row;
+ * the paper's tiers: groups of 32 with FP16 (s, z), optionally after the
+ * block-32 transform). Every sum runs in the order of its definition:
+ * columns ascending within a row (IEEE operations, no contraction), samples
+ * in the order they are accumulated. Finalization forms, per head and
+ * channel, the domain-balanced mean of Eq. (13) (the mean over domains of
+ * each domain's mean), a_eff = exp(mean log a), P = 1 / max(1 - a_eff^2,
+ * tau) and the chosen selector's score, then keeps the k_hi largest scores
+ * (ties to the lower channel) and returns the stable partition of Alg. 1.
+ * ---------------------------------------------------------------------- */
+
+#define DAMP_CALIB_MAX_DOMAINS 64
+
+/* Selectors of the ablation in section 6: the product C = E P, the error
+ * energy E alone, the persistence P alone, the mean squared key-channel
+ * norm, or caller-supplied scores (Random: draw them uniformly). */
+typedef enum {
+  DAMP_SEL_DAMP = 0,
+  DAMP_SEL_ERROR = 1,
+  DAMP_SEL_PERSISTENCE = 2,
+  DAMP_SEL_STATE_ENERGY = 3,
+  DAMP_SEL_RANDOM = 4
+} damp_selector;
+
+/* Accumulator descriptor (plain data; filled by damp_calib_init). The
+ * accumulators are caller-owned device memory: per domain d, three
+ * [num_heads, d_k] double arrays (err, en, loga), followed by num_domains
+ * double sample counts. */
+typedef struct {
+  damp_layout lo;       /* Q_lo is this layout's low tier; k_hi is not used */
+  int32_t is_kda;       /* 1: log-decay per key channel (KDA); 0: per head */
+  int32_t num_heads;
+  int32_t num_domains;
+  double* sums;         /* device */
+  size_t bytes;
+} damp_calib;
+
+/* 8 * num_domains * (3 * num_heads * d_k + 1); 0 for non-positive sizes. */
+size_t damp_calib_required_bytes(int32_t num_domains, int32_t num_heads,
+                                 int32_t d_k);
+
+/* Fills *calib and zeroes the accumulators (a fill kernel on `stream`).
+ *  lo           a DAMP_STATE_MIXED layout with d_k == d_v <= 256 whose low
+ *               tier has kernels (default or paper tiers; else
+ *               DAMP_ERR_UNSUPPORTED).
+ *  num_domains  in [1, DAMP_CALIB_MAX_DOMAINS].
+ *  sums, bytes  device memory, 8-byte aligned, at least
+ *               damp_calib_required_bytes(num_domains, num_heads, lo->d_k). */
+damp_status damp_calib_init(damp_calib* calib, const damp_layout* lo,
+                            int32_t is_kda, int32_t num_heads,
+                            int32_t num_domains, void* sums, size_t bytes,
+                            void* stream);
+
+/* Adds one sampled state write of B requests to domain `domain`.
+ *  pool      a DAMP_STATE_FP32 pool of the calibration trajectory with
+ *            d_k, d_v and num_v_heads equal to the calib's.
+ *  slot_idx  int32 [B]; requests whose slot is outside [0, num_slots) are
+ *            skipped and not counted.
+ *  perm      uint8 [num_heads, d_k]: tile row r holds key channel
+ *            perm[h, r]; NULL = identity.
+ *  g         bf16 log-decay of the sampled token: [B, num_heads] (GDN) or
+ *            [B, num_heads, d_k] in natural channel order (KDA).
+ * Calls on one calib must not overlap (they read and write the same
+ * accumulators); they accumulate in call order. */
+damp_status damp_calib_accumulate(const damp_calib* calib, int32_t domain,
+                                  const damp_pool* pool, int32_t layer,
+                                  const int32_t* slot_idx, int32_t B,
+                                  const uint8_t* perm, const uint16_t* g,
+                                  void* stream);
+
+/* Runs a calibration sequence of T tokens for B requests on the FP32 pool
+ * (its tiles hold the starting states in natural channel order, e.g. the
+ * zero state after damp_pool_reset_slots) and samples every `stride`
+ * tokens: after tokens stride, 2 stride, ... the state write is
+ * accumulated into `domain`, with the log-decay of that token (App. A.3:
+ * states sampled every eight tokens). A trailing partial stride is run but
+ * not sampled. The recurrence is the prefill path's, `stride` tokens per
+ * launch; no outputs are written. Inputs as for damp_state_prefill_gdn /
+ * _kda (num_k_heads == num_heads for KDA). The pool holds the final states
+ * afterwards. */
+damp_status damp_calibrate_sequence(const damp_calib* calib, int32_t domain,
+                                    const damp_pool* pool, int32_t layer,
+                                    const int32_t* slot_idx, int32_t B,
+                                    int32_t T, int32_t stride,
+                                    int32_t num_k_heads, const uint16_t* q,
+                                    const uint16_t* k, const uint16_t* v,
+                                    const uint16_t* g, const uint16_t* beta,
+                                    void* stream);
+
+/* Selection from the accumulated statistics (Alg. 1). Synchronises `stream`.
+ *  selector     a damp_selector.
+ *  k_hi         in [0, d_k]; tau > 0 (the paper uses 1e-4).
+ *  rand_scores  host double [num_heads, d_k] for DAMP_SEL_RANDOM, else
+ *               unused.
+ *  sel_out      host int32 [num_heads, k_hi], ascending per head.
+ *  perm_out     host uint8 [num_heads, d_k].
+ *  score_out    host double [num_heads, d_k]: the selector's score, or NULL.
+ *  stats_out    host double [4, num_heads, d_k]: E, P, mean squared norm,
+ *               mean log a; or NULL.
+ * DAMP_ERR_INVALID_ARG if a domain has no samples. */
+damp_status damp_calib_finalize(const damp_calib* calib, int32_t selector,
+                                int32_t k_hi, double tau,
+                                const double* rand_scores, int32_t* sel_out,
+                                uint8_t* perm_out, double* score_out,
+                                double* stats_out, void* stream);
+
+/* Calibration-split agreement (App. B), host only. Top-k overlap
+ * |A intersect B| / k of two selections of k distinct channels each; NaN for
+ * NULL or k <= 0. */
+double damp_topk_overlap(const int32_t* sel_a, const int32_t* sel_b,
+                         int32_t k);
+
+/* Spearman rank correlation of two score vectors of length n (ties get
+ * their average rank; Pearson correlation of the ranks); NaN for n < 2, a
+ * NULL pointer, or a constant vector. Host only. */
+double damp_spearman(const double* a, const double* b, int32_t n);
 
 /* Message describing the last failure on the calling thread ("" if none). */
 const char* damp_last_error(void);

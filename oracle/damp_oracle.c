@@ -617,3 +617,134 @@ int orc_select(int is_kda, int N, int H, int dk, int dv, const float* states,
   free(err);
   return 0;
 }
+
+/* ------------------------------------------- calibration over a trajectory */
+
+/* ||Q_lo(x) - x||^2 of one row of n values, for the low tier of format f: one
+ * (s, z) per row (Eq. (3)), or groups of f.group values with FP16 (s, z), in
+ * the block-32 transformed domain when f.hadamard (App. A.1). The
+ * reconstruction is taken back to the state's domain before the difference;
+ * squared differences are summed in double over ascending columns. */
+static double orc_row_error_fmt(const float* x, int n, orc_fmt_t f) {
+  if (!f.meta_fp16) return orc_row_error(x, n);
+  double acc = 0.0;
+  for (int g0 = 0; g0 < n; g0 += f.group) {
+    const float* xg = x + g0;
+    float y[256], yq[256], xr[256];
+    uint8_t c[256];
+    if (f.hadamard) orc_hadamard32(xg, y);
+    else memcpy(y, xg, (size_t)f.group * sizeof(float));
+    float s, z;
+    orc_quant_group_fp16(y, f.group, c, &s, &z);
+    orc_dequant_row(c, f.group, s, z, yq);
+    if (f.hadamard) orc_hadamard32(yq, xr);
+    else memcpy(xr, yq, (size_t)f.group * sizeof(float));
+    for (int j = 0; j < f.group; ++j) {
+      double e = (double)xr[j] - (double)xg[j];
+      acc = acc + e * e;
+    }
+  }
+  return acc;
+}
+
+/*
+ * One sampled state write (App. A.2): for each of the B requests in turn and
+ * each head h and key channel u, adds to the running sums
+ *   err[h,u]  += ||Q_lo(S_b[h,u,:]) - S_b[h,u,:]||^2        (Eq. (14))
+ *   en[h,u]   += ||S_b[h,u,:]||^2                            (state energy)
+ *   loga[h,u] += log a_b[h,u] (the bf16 log-decay g widened) (Eq. (15))
+ * and 1 to *count. states: fp32 [B, H, dk, dv] in natural channel order;
+ * g: bf16 [B, H] (GDN) or [B, H, dk] (KDA). fmt as for orc_pack (NULL: one
+ * fp32 (s, z) per row).
+ */
+void orc_calib_accumulate(int is_kda, const int32_t* fmt, int B, int H, int dk, int dv,
+                          const float* states, const uint16_t* g, double* err, double* en,
+                          double* loga, double* count) {
+  orc_fmt_t f = orc_fmt(fmt, dv);
+  for (int b = 0; b < B; ++b) {
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < (int64_t)H * dk; ++i) {
+      const int h = (int)(i / dk), u = (int)(i % dk);
+      const float* x = states + (((size_t)b * H + h) * dk + u) * dv;
+      double e2 = 0.0;
+      for (int j = 0; j < dv; ++j) e2 = e2 + (double)x[j] * (double)x[j];
+      const uint16_t gb = is_kda ? g[((size_t)b * H + h) * dk + u] : g[(size_t)b * H + h];
+      err[i] = err[i] + orc_row_error_fmt(x, dv, f);
+      en[i] = en[i] + e2;
+      loga[i] = loga[i] + (double)orc_from_bf16(gb);
+    }
+    *count = *count + 1.0;
+  }
+}
+
+/*
+ * Selection from accumulated statistics (Alg. 1 with App. A.2's estimates and
+ * the domain-balanced mean of Eq. (13)): for each head and key channel the
+ * mean over domains (ascending) of each domain's mean, then
+ *   a_eff = exp(mean log a),  P = 1 / max(1 - a_eff^2, tau)   (Eq. (15))
+ * and the score of the selector: 0 C = E P, 1 E, 2 P, 3 the mean squared
+ * row norm, 4 the caller's rand [H, dk]. The k_hi largest scores are kept
+ * (ties to the lower channel); perm is the stable partition.
+ * sums: [D][3][H][dk] (err, en, loga); counts: [D]. stats (nullable):
+ * [4][H][dk] = E, P, mean squared norm, mean log a. Returns nonzero if a
+ * domain has no samples or an argument is out of range.
+ */
+int orc_calib_finalize(int D, int H, int dk, const double* sums, const double* counts,
+                       int selector, int k_hi, double tau, const double* rand, int32_t* sel,
+                       uint8_t* perm, double* score, double* stats) {
+  if (D <= 0 || H <= 0 || dk <= 0 || dk > 256 || k_hi < 0 || k_hi > dk || selector < 0 ||
+      selector > 4 || (selector == 4 && !rand))
+    return 1;
+  for (int d = 0; d < D; ++d)
+    if (!(counts[d] > 0.0)) return 1;
+  const size_t hk = (size_t)H * dk;
+  orc_ranked* rk = (orc_ranked*)malloc((size_t)dk * sizeof(orc_ranked));
+  unsigned char* keep = (unsigned char*)malloc((size_t)dk);
+  for (int h = 0; h < H; ++h) {
+    for (int u = 0; u < dk; ++u) {
+      const size_t i = (size_t)h * dk + u;
+      double E = 0.0, En = 0.0, L = 0.0;
+      for (int d = 0; d < D; ++d) {
+        const double* s = sums + (size_t)d * 3 * hk;
+        E = E + s[i] / counts[d];
+        En = En + s[hk + i] / counts[d];
+        L = L + s[2 * hk + i] / counts[d];
+      }
+      E = E / (double)D;
+      En = En / (double)D;
+      L = L / (double)D;
+      double a_eff = exp(L);
+      double one_minus = 1.0 - a_eff * a_eff;
+      double P = 1.0 / (one_minus > tau ? one_minus : tau);
+      double c;
+      if (selector == 0) c = E * P;
+      else if (selector == 1) c = E;
+      else if (selector == 2) c = P;
+      else if (selector == 3) c = En;
+      else c = rand[i];
+      if (score) score[i] = c;
+      if (stats) {
+        stats[i] = E;
+        stats[hk + i] = P;
+        stats[2 * hk + i] = En;
+        stats[3 * hk + i] = L;
+      }
+      rk[u].c = c;
+      rk[u].u = u;
+    }
+    qsort(rk, (size_t)dk, sizeof(orc_ranked), orc_rank_cmp);
+    memset(keep, 0, (size_t)dk);
+    for (int i = 0; i < k_hi; ++i) keep[rk[i].u] = 1;
+    int p = 0, s = 0;
+    for (int u = 0; u < dk; ++u)
+      if (keep[u]) {
+        perm[(size_t)h * dk + p++] = (uint8_t)u;
+        sel[(size_t)h * k_hi + s++] = u;
+      }
+    for (int u = 0; u < dk; ++u)
+      if (!keep[u]) perm[(size_t)h * dk + p++] = (uint8_t)u;
+  }
+  free(rk);
+  free(keep);
+  return 0;
+}

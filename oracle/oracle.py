@@ -86,6 +86,9 @@ def lib():
                                   i32, i32, vp, vp, vp, vp, vp, vp, f32, vp]
         L.orc_select.argtypes = [i32, i32, i32, i32, i32, vp, vp, i32, f64, vp, vp, vp, vp, vp]
         L.orc_select.restype = i32
+        L.orc_calib_accumulate.argtypes = [i32, vp, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp]
+        L.orc_calib_finalize.argtypes = [i32, i32, i32, vp, vp, i32, i32, f64, vp, vp, vp, vp, vp]
+        L.orc_calib_finalize.restype = i32
         _lib = L
     return _lib
 
@@ -351,3 +354,94 @@ def run_fp32(S0, *, kda: bool, q, k, v, g, beta, scale: float = 1.0, sample_ever
             samples.append(pool.buf.view(np.float32).reshape(B, HV, dk, dv).copy())
     S = pool.buf.view(np.float32).reshape(B, HV, dk, dv).copy()
     return S, np.stack(outs), (np.stack(samples) if samples else None)
+
+
+# ------------------------------------------------------------- calibration
+
+SEL_DAMP, SEL_ERROR, SEL_PERSISTENCE, SEL_STATE_ENERGY, SEL_RANDOM = 0, 1, 2, 3, 4
+
+
+class Calib:
+    """Accumulators of App. A.2 over sampled state writes, one set per
+    calibration domain: err, en, loga [D, H, dk] (Eq. (14), the state-energy
+    selector's squared row norms, Eq. (15)) and sample counts [D]. fmt names
+    Q_lo's low tier as for Pool (None: one fp32 (s, z) per row)."""
+
+    def __init__(self, *, kda: bool, H: int, dk: int, dv: int, num_domains: int = 1, fmt=None):
+        self.kda, self.H, self.dk, self.dv, self.fmt = kda, H, dk, dv, fmt
+        self.sums = np.zeros((num_domains, 3, H, dk))
+        self.counts = np.zeros(num_domains)
+
+    def accumulate(self, domain: int, states, g) -> None:
+        """states fp32 [B, H, dk, dv] in natural channel order; g bf16 bits of
+        the sampled token's log-decay, [B, H] (GDN) or [B, H, dk] (KDA)."""
+        states = np.ascontiguousarray(states, dtype=np.float32)
+        g = np.ascontiguousarray(g, dtype=np.uint16)
+        B = states.shape[0]
+        assert states.shape == (B, self.H, self.dk, self.dv)
+        assert g.shape == ((B, self.H, self.dk) if self.kda else (B, self.H))
+        s = self.sums[domain]
+        err, en, loga = (np.ascontiguousarray(s[i]) for i in range(3))
+        cnt = np.array([self.counts[domain]])
+        lib().orc_calib_accumulate(int(self.kda), _p(_fmt_arr(self.fmt)), B, self.H, self.dk,
+                                   self.dv, _p(states), _p(g), _p(err), _p(en), _p(loga),
+                                   _p(cnt))
+        s[0], s[1], s[2] = err, en, loga
+        self.counts[domain] = cnt[0]
+
+    def finalize(self, k_hi: int, selector: int = SEL_DAMP, tau: float = 1e-4,
+                 rand_scores=None) -> dict:
+        """Alg. 1 from the domain-balanced estimates (Eq. (13)-(15))."""
+        D, H, dk = self.sums.shape[0], self.H, self.dk
+        sums = np.ascontiguousarray(self.sums)
+        counts = np.ascontiguousarray(self.counts)
+        rs = None if rand_scores is None else np.ascontiguousarray(rand_scores, np.float64)
+        sel = np.zeros((H, k_hi), np.int32)
+        perm = np.zeros((H, dk), np.uint8)
+        score = np.zeros((H, dk))
+        stats = np.zeros((4, H, dk))
+        rc = lib().orc_calib_finalize(D, H, dk, _p(sums), _p(counts), selector, k_hi, float(tau),
+                                      _p(rs), _p(sel), _p(perm), _p(score), _p(stats))
+        if rc != 0:
+            raise ValueError("orc_calib_finalize rejected its arguments")
+        return dict(sel=sel, perm=perm, score=score, E=stats[0], P=stats[1], energy=stats[2],
+                    mean_log_a=stats[3])
+
+
+def calibrate_sequence(calib: Calib, domain: int, S0, *, stride: int, q, k, v, g, beta):
+    """The FP32 reference trajectory from S0 (natural order, [B, H, dk, dv])
+    over step-major inputs [T, B, ...], with the state write after every
+    `stride` tokens accumulated (App. A.3). Returns the final state."""
+    S, _, samples = run_fp32(S0, kda=calib.kda, q=q, k=k, v=v, g=g, beta=beta,
+                             sample_every=stride)
+    if samples is not None:
+        for n in range(samples.shape[0]):
+            calib.accumulate(domain, samples[n], g[(n + 1) * stride - 1])
+    return S
+
+
+def topk_overlap(sel_a, sel_b) -> float:
+    """|A intersect B| / k (App. B, calibration-split agreement)."""
+    a, b = np.asarray(sel_a).ravel(), np.asarray(sel_b).ravel()
+    return len(set(a.tolist()) & set(b.tolist())) / float(len(a))
+
+
+def spearman(a, b) -> float:
+    """Spearman rank correlation: Pearson correlation of the average ranks."""
+    def ranks(x):
+        x = np.asarray(x, dtype=np.float64)
+        order = np.argsort(x, kind="stable")
+        r = np.empty(len(x))
+        i = 0
+        while i < len(x):
+            j = i
+            while j + 1 < len(x) and x[order[j + 1]] == x[order[i]]:
+                j += 1
+            r[order[i:j + 1]] = (i + j) / 2.0 + 1.0
+            i = j + 1
+        return r
+    ra, rb = ranks(a), ranks(b)
+    ra -= ra.mean()
+    rb -= rb.mean()
+    den = np.sqrt((ra * ra).sum() * (rb * rb).sum())
+    return float((ra * rb).sum() / den) if den > 0 else float("nan")

@@ -55,4 +55,13 @@ inline hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
 // Returns DAMP_ERR_HIP with a message if the last launch failed.
 damp_status check_launch(const char* what);
 
+// Enqueues the prefill kernel for input tokens [t0, t0 + T) of arrays that
+// hold t_pitch tokens per request; o ([B, T, HV, d_v]) may be NULL. The
+// caller has validated the pool, the layer, the sizes and the pointers.
+void prefill_window(bool kda, const damp_pool* pool, int32_t layer, const int32_t* slot_idx,
+                    int32_t B, int32_t t0, int32_t T, int32_t t_pitch, int32_t num_k_heads,
+                    const uint16_t* q, const uint16_t* k, const uint16_t* v, const uint16_t* g,
+                    const uint16_t* beta, const uint8_t* perm, float scale, void* o,
+                    bool o_bf16, hipStream_t stream);
+
 }  // namespace damp

@@ -26,15 +26,17 @@ struct PrefillParams {
   uint64_t slot_stride;
   uint64_t tile_stride;
   const int32_t* slot_idx;
-  const uint16_t* q;  // [B, T, HK, D]
+  const uint16_t* q;  // [B, t_pitch, HK, D]
   const uint16_t* k;
-  const uint16_t* v;  // [B, T, HV, D]
-  const uint16_t* g;  // [B, T, HV] or [B, T, HV, D]
-  const uint16_t* beta;  // [B, T, HV]
+  const uint16_t* v;  // [B, t_pitch, HV, D]
+  const uint16_t* g;  // [B, t_pitch, HV] or [B, t_pitch, HV, D]
+  const uint16_t* beta;  // [B, t_pitch, HV]
   const uint8_t* perm;
-  void* o;  // [B, T, HV, D]
+  void* o;  // [B, T, HV, D], or NULL: no outputs
   float scale;
-  int32_t T;
+  int32_t T;        // tokens run by this launch
+  int32_t t_pitch;  // tokens per request in the input arrays
+  int32_t t0;       // first input token of this launch
   int32_t num_slots;
   int32_t HK;
   int32_t HV;
@@ -73,6 +75,7 @@ __global__ __launch_bounds__(NT) void prefill_kernel(const PrefillParams p) {
            static_cast<size_t>(j) * o_esize;
   };
   auto write_o = [&](int tok, int j, float val) {
+    if (!p.o) return;
     if (p.o_bf16) *reinterpret_cast<uint16_t*>(o_at(tok, j)) = f32_to_bf16(val);
     else *reinterpret_cast<float*>(o_at(tok, j)) = val;
   };
@@ -100,7 +103,7 @@ __global__ __launch_bounds__(NT) void prefill_kernel(const PrefillParams p) {
   const int my_u = (t < D && p.perm) ? (static_cast<int>(p.perm[static_cast<size_t>(h) * D + t]) & (D - 1)) : t;
   auto load_tok = [&](TokRegs& r, int tok) {
     if (t < D) {
-      const size_t bt = static_cast<size_t>(b) * T + tok;
+      const size_t bt = static_cast<size_t>(b) * p.t_pitch + p.t0 + tok;
       const size_t kq = (bt * p.HK + hk) * D;
       const size_t bth = bt * p.HV + h;
       r.k = p.k[kq + my_u];
@@ -224,6 +227,41 @@ void launch_kind(const damp_pool* pool, int D, const PrefillParams& p, int B, hi
   else launch_d<kMixed, KDA>(D, p, B, s);
 }
 
+}  // namespace
+
+void prefill_window(bool kda, const damp_pool* pool, int32_t layer, const int32_t* slot_idx,
+                    int32_t B, int32_t t0, int32_t T, int32_t t_pitch, int32_t num_k_heads,
+                    const uint16_t* q, const uint16_t* k, const uint16_t* v, const uint16_t* g,
+                    const uint16_t* beta, const uint8_t* perm, float scale, void* o,
+                    bool o_bf16, hipStream_t stream) {
+  PrefillParams p;
+  p.layer_base = layer_base(pool, layer);
+  p.tile_stride = pool->tile_stride;
+  p.slot_stride = pool->tile_stride * static_cast<uint64_t>(pool->num_v_heads);
+  p.slot_idx = slot_idx;
+  p.q = q;
+  p.k = k;
+  p.v = v;
+  p.g = g;
+  p.beta = beta;
+  p.perm = perm;
+  p.o = o;
+  p.scale = scale;
+  p.T = T;
+  p.t_pitch = t_pitch;
+  p.t0 = t0;
+  p.num_slots = pool->num_slots;
+  p.HK = num_k_heads;
+  p.HV = pool->num_v_heads;
+  p.k_hi = pool->layout.kind == DAMP_STATE_FP32 ? 0 : pool->layout.k_hi;
+  p.o_bf16 = o_bf16 ? 1 : 0;
+  p.had = pool->layout.hadamard;
+  if (kda) launch_kind<true>(pool, pool->layout.d_k, p, B, stream);
+  else launch_kind<false>(pool, pool->layout.d_k, p, B, stream);
+}
+
+namespace {
+
 damp_status prefill(bool kda, const damp_pool* pool, int32_t layer, const int32_t* slot_idx,
                     int32_t B, int32_t T, int32_t num_k_heads, const uint16_t* q,
                     const uint16_t* k, const uint16_t* v, const uint16_t* g, const uint16_t* beta,
@@ -248,29 +286,8 @@ damp_status prefill(bool kda, const damp_pool* pool, int32_t layer, const int32_
   if (!layout_has_kernels(&pool->layout))
     return fail(DAMP_ERR_UNSUPPORTED, "%s: no kernel for this layout", name);
 
-  PrefillParams p;
-  p.layer_base = layer_base(pool, layer);
-  p.tile_stride = pool->tile_stride;
-  p.slot_stride = pool->tile_stride * static_cast<uint64_t>(pool->num_v_heads);
-  p.slot_idx = slot_idx;
-  p.q = q;
-  p.k = k;
-  p.v = v;
-  p.g = g;
-  p.beta = beta;
-  p.perm = perm;
-  p.o = o;
-  p.scale = scale;
-  p.T = T;
-  p.num_slots = pool->num_slots;
-  p.HK = num_k_heads;
-  p.HV = pool->num_v_heads;
-  p.k_hi = pool->layout.kind == DAMP_STATE_FP32 ? 0 : pool->layout.k_hi;
-  p.o_bf16 = o_dtype == DAMP_DT_BF16;
-  p.had = pool->layout.hadamard;
-  hipStream_t s = as_stream(stream);
-  if (kda) launch_kind<true>(pool, pool->layout.d_k, p, B, s);
-  else launch_kind<false>(pool, pool->layout.d_k, p, B, s);
+  prefill_window(kda, pool, layer, slot_idx, B, 0, T, T, num_k_heads, q, k, v, g, beta, perm,
+                 scale, o, o_dtype == DAMP_DT_BF16, as_stream(stream));
   return check_launch(name);
 }
 

@@ -19,6 +19,9 @@ LIB_PATH = os.path.join(HERE, "libdamp.so")
 DAMP_OK, DAMP_ERR_INVALID_ARG, DAMP_ERR_UNSUPPORTED, DAMP_ERR_HIP = 0, 1, 2, 3
 DAMP_DT_FP32, DAMP_DT_BF16, DAMP_DT_FP16 = 0, 1, 2
 DAMP_STATE_FP32, DAMP_STATE_MIXED = 0, 1
+DAMP_SEL_DAMP, DAMP_SEL_ERROR, DAMP_SEL_PERSISTENCE, DAMP_SEL_STATE_ENERGY, DAMP_SEL_RANDOM = \
+    0, 1, 2, 3, 4
+DAMP_CALIB_MAX_DOMAINS = 64
 
 
 class DampError(RuntimeError):
@@ -32,6 +35,12 @@ class damp_layout(ctypes.Structure):
                 ("d_k", "d_v", "k_hi", "kind", "hi_dtype", "group", "meta_dtype", "hadamard")]
 
 
+class damp_calib(ctypes.Structure):
+    _fields_ = [("lo", damp_layout), ("is_kda", ctypes.c_int32), ("num_heads", ctypes.c_int32),
+                ("num_domains", ctypes.c_int32), ("sums", ctypes.c_void_p),
+                ("bytes", ctypes.c_size_t)]
+
+
 class damp_pool(ctypes.Structure):
     _fields_ = [("layout", damp_layout), ("num_layers", ctypes.c_int32),
                 ("num_slots", ctypes.c_int32), ("num_v_heads", ctypes.c_int32),
@@ -43,7 +52,9 @@ EXPORTS = ("damp_layout_init", "damp_tile_bytes", "damp_tile_stride", "damp_bits
            "damp_pool_required_bytes", "damp_pool_init", "damp_pool_reset_slots",
            "damp_state_update_gdn", "damp_state_update_kda", "damp_state_prefill_gdn",
            "damp_state_prefill_kda", "damp_state_pack", "damp_state_unpack",
-           "damp_select_channels", "damp_last_error")
+           "damp_select_channels", "damp_calib_required_bytes", "damp_calib_init",
+           "damp_calib_accumulate", "damp_calibrate_sequence", "damp_calib_finalize",
+           "damp_topk_overlap", "damp_spearman", "damp_last_error")
 
 _lib = None
 
@@ -60,6 +71,7 @@ def lib() -> ctypes.CDLL:
     P, i32, sz, f32, f64, st = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t,
                                 ctypes.c_float, ctypes.c_double, ctypes.c_int)
     LP, PP = ctypes.POINTER(damp_layout), ctypes.POINTER(damp_pool)
+    CP = ctypes.POINTER(damp_calib)
     sig = {
         "damp_layout_init": (st, [LP, i32, i32, i32, i32]),
         "damp_tile_bytes": (sz, [LP]),
@@ -77,6 +89,14 @@ def lib() -> ctypes.CDLL:
         "damp_state_pack": (st, [PP, i32, P, i32, P, P, P]),
         "damp_state_unpack": (st, [PP, i32, P, i32, P, P, P]),
         "damp_select_channels": (st, [i32, i32, i32, i32, i32, P, P, i32, f64, P, P, P, P]),
+        "damp_calib_required_bytes": (sz, [i32, i32, i32]),
+        "damp_calib_init": (st, [CP, LP, i32, i32, i32, P, sz, P]),
+        "damp_calib_accumulate": (st, [CP, i32, PP, i32, P, i32, P, P, P]),
+        "damp_calibrate_sequence": (st, [CP, i32, PP, i32, P, i32, i32, i32, i32, P, P, P, P, P,
+                                         P]),
+        "damp_calib_finalize": (st, [CP, i32, i32, f64, P, P, P, P, P, P]),
+        "damp_topk_overlap": (f64, [P, P, i32]),
+        "damp_spearman": (f64, [P, P, i32]),
         "damp_last_error": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sig.items():
@@ -320,6 +340,99 @@ def damp_select_channels(states, log_decay, k_hi: int, *, kda: bool, tau: float 
                                       k_hi, float(tau), _ptr(sel), _ptr(perm), _ptr(score),
                                       _stream(stream)))
     return sel, perm, score
+
+
+# ------------------------------------------------------------- calibration
+
+class Calib:
+    """Calibration accumulators (a torch float64 buffer on the GPU) and their
+    damp_calib descriptor (keeps the buffer alive)."""
+
+    def __init__(self, lo: damp_layout, *, kda: bool, num_heads: int, num_domains: int = 1,
+                 device="cuda", stream=None):
+        need = lib().damp_calib_required_bytes(num_domains, num_heads, lo.d_k)
+        if need == 0:
+            raise ValueError("invalid calibration shape")
+        self.buffer = torch.empty(need // 8, dtype=torch.float64, device=device)
+        self.desc = damp_calib()
+        _check(lib().damp_calib_init(ctypes.byref(self.desc), ctypes.byref(lo), int(kda),
+                                     num_heads, num_domains, _ptr(self.buffer), need,
+                                     _stream(stream)))
+        self.lo, self.kda = lo, kda
+        self.num_heads, self.num_domains = num_heads, num_domains
+
+
+def damp_calib_accumulate(calib: Calib, domain: int, pool: Pool, layer: int, slot_idx, g,
+                          perm=None, stream=None) -> None:
+    """One sampled state write of the FP32 pool's slots (g: bf16 log-decay of
+    the sampled token, [B, H] or [B, H, d_k])."""
+    slot_idx = _dev(slot_idx, torch.int32, "slot_idx")
+    B, H, d = slot_idx.numel(), calib.num_heads, calib.lo.d_k
+    _dev(g, torch.bfloat16, "g", (B, H, d) if calib.kda else (B, H))
+    if perm is not None:
+        _dev(perm, torch.uint8, "perm", (H, d))
+    _check(lib().damp_calib_accumulate(ctypes.byref(calib.desc), domain, ctypes.byref(pool.desc),
+                                       layer, _ptr(slot_idx), B, _ptr(perm), _ptr(g),
+                                       _stream(stream)))
+
+
+def damp_calibrate_sequence(calib: Calib, domain: int, pool: Pool, layer: int, slot_idx, q, k, v,
+                            g, beta, stride: int = 8, stream=None) -> None:
+    """Runs T tokens ([B, T, ...] inputs) of the FP32 recurrence on the pool,
+    accumulating the state write after every `stride` tokens."""
+    slot_idx = _dev(slot_idx, torch.int32, "slot_idx")
+    B, H, d = slot_idx.numel(), calib.num_heads, calib.lo.d_k
+    if q.dim() != 4:
+        raise ValueError("q must be [B, T, HK, d]")
+    T, HK = q.shape[1], q.shape[2]
+    _dev(q, torch.bfloat16, "q", (B, T, HK, d))
+    _dev(k, torch.bfloat16, "k", (B, T, HK, d))
+    _dev(v, torch.bfloat16, "v", (B, T, H, d))
+    _dev(g, torch.bfloat16, "g", (B, T, H, d) if calib.kda else (B, T, H))
+    _dev(beta, torch.bfloat16, "beta", (B, T, H))
+    _check(lib().damp_calibrate_sequence(ctypes.byref(calib.desc), domain, ctypes.byref(pool.desc),
+                                         layer, _ptr(slot_idx), B, T, stride, HK, _ptr(q), _ptr(k),
+                                         _ptr(v), _ptr(g), _ptr(beta), _stream(stream)))
+
+
+def damp_calib_finalize(calib: Calib, k_hi: int, selector: int = DAMP_SEL_DAMP,
+                        tau: float = 1e-4, rand_scores=None, stream=None) -> dict:
+    """Selection from the accumulated statistics; host tensors sel int32
+    [H, k_hi], perm uint8 [H, d_k], score and E, P, energy, mean log a
+    (float64 [H, d_k])."""
+    H, d = calib.num_heads, calib.lo.d_k
+    sel = torch.zeros((H, k_hi), dtype=torch.int32)
+    perm = torch.zeros((H, d), dtype=torch.uint8)
+    score = torch.zeros((H, d), dtype=torch.float64)
+    stats = torch.zeros((4, H, d), dtype=torch.float64)
+    rs = None
+    if rand_scores is not None:
+        rs = torch.as_tensor(rand_scores, dtype=torch.float64).contiguous()
+        if tuple(rs.shape) != (H, d) or rs.device.type != "cpu":
+            raise ValueError("rand_scores must be a host float64 [H, d_k] tensor")
+    _check(lib().damp_calib_finalize(ctypes.byref(calib.desc), selector, k_hi, float(tau),
+                                     _ptr(rs), _ptr(sel), _ptr(perm), _ptr(score), _ptr(stats),
+                                     _stream(stream)))
+    return dict(sel=sel, perm=perm, score=score, E=stats[0], P=stats[1], energy=stats[2],
+                mean_log_a=stats[3])
+
+
+def damp_topk_overlap(sel_a, sel_b) -> float:
+    """|A intersect B| / k of two [k] int32 host selections."""
+    a = torch.as_tensor(sel_a, dtype=torch.int32).contiguous()
+    b = torch.as_tensor(sel_b, dtype=torch.int32).contiguous()
+    if a.numel() != b.numel() or a.device.type != "cpu" or b.device.type != "cpu":
+        raise ValueError("two host selections of equal size")
+    return lib().damp_topk_overlap(_ptr(a), _ptr(b), a.numel())
+
+
+def damp_spearman(a, b) -> float:
+    """Spearman rank correlation of two host score vectors."""
+    x = torch.as_tensor(a, dtype=torch.float64).contiguous()
+    y = torch.as_tensor(b, dtype=torch.float64).contiguous()
+    if x.numel() != y.numel() or x.device.type != "cpu" or y.device.type != "cpu":
+        raise ValueError("two host score vectors of equal size")
+    return lib().damp_spearman(_ptr(x), _ptr(y), x.numel())
 
 
 class PreparedUpdate:

@@ -8,7 +8,9 @@ import json
 import os
 import re
 
+import numpy as np
 import pytest
+import scipy.stats
 
 from oracle import oracle as orc
 from paper_2608_27513_amd import damp as D
@@ -34,7 +36,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = declared_functions()
-    assert len(names) == 15
+    assert len(names) == 22
     for n in names:
         assert hasattr(L, n), n
     assert sorted(D.EXPORTS) == names
@@ -209,3 +211,76 @@ def test_select_validation(L):
     assert f(0, 0, 2, 128, 128, p, p, 16, 1e-4, p, p, None, None) == D.DAMP_ERR_INVALID_ARG
     assert f(0, 4, 2, 300, 128, p, p, 16, 1e-4, p, p, None, None) == D.DAMP_ERR_INVALID_ARG
     assert f(0, 4, 2, 128, 128, None, p, 16, 1e-4, p, p, None, None) == D.DAMP_ERR_INVALID_ARG
+
+
+def test_split_agreement_functions_match_scipy(L):
+    """damp_spearman / damp_topk_overlap (host code of the library) against
+    scipy's Spearman correlation and a set intersection."""
+    rng = np.random.default_rng(5)
+    for n in (2, 9, 128):
+        a = rng.standard_normal(n)
+        b = 0.5 * a + rng.standard_normal(n)
+        assert abs(D.damp_spearman(a, b) - scipy.stats.spearmanr(a, b).statistic) <= 1e-12
+    a = np.array([3.0, 1.0, 1.0, 2.0, 2.0, 2.0, 8.0])
+    b = np.array([1.0, 1.0, 4.0, 4.0, 0.5, 9.0, 9.0])
+    assert abs(D.damp_spearman(a, b) - scipy.stats.spearmanr(a, b).statistic) <= 1e-12
+    assert np.isnan(D.damp_spearman(np.ones(5), a[:5]))
+    for k in (1, 4, 16):
+        x = rng.permutation(128)[:k].astype(np.int32)
+        y = rng.permutation(128)[:k].astype(np.int32)
+        assert D.damp_topk_overlap(x, y) == len(set(x) & set(y)) / k
+    assert np.isnan(L.damp_topk_overlap(None, None, 4))
+
+
+def test_calib_validation_fails_before_launch(L):
+    lo = D.damp_layout_init(128, 128, 16)
+    cal = D.damp_calib()
+    p = ctypes.c_void_p(0x7f0000100000)  # never dereferenced
+    need = L.damp_calib_required_bytes(2, 32, 128)
+    assert need == 8 * 2 * (3 * 32 * 128 + 1)
+    assert L.damp_calib_required_bytes(0, 32, 128) == 0
+    st, msg = _status(L.damp_calib_init, ctypes.byref(cal), ctypes.byref(lo), 0, 32, 2, p, need - 8,
+                      None)
+    assert st == D.DAMP_ERR_INVALID_ARG and "need" in msg
+    st, _ = _status(L.damp_calib_init, ctypes.byref(cal), ctypes.byref(lo), 0, 32, 65, p, need, None)
+    assert st == D.DAMP_ERR_INVALID_ARG
+    fp = D.damp_layout_init(128, 128, 0, D.DAMP_STATE_FP32)
+    st, _ = _status(L.damp_calib_init, ctypes.byref(cal), ctypes.byref(fp), 0, 32, 2, p, need, None)
+    assert st == D.DAMP_ERR_INVALID_ARG
+    odd = D.damp_layout_init(128, 128, 16)
+    odd.group = 32  # grouped with fp32 metadata: no kernel
+    st, _ = _status(L.damp_calib_init, ctypes.byref(cal), ctypes.byref(odd), 0, 32, 2, p, need, None)
+    assert st == D.DAMP_ERR_UNSUPPORTED
+    # a descriptor filled by hand, as damp_calib_init would (no launch below)
+    cal.lo, cal.is_kda, cal.num_heads, cal.num_domains = lo, 0, 32, 2
+    cal.sums, cal.bytes = p, need
+    pool = _fake_pool(L, D.damp_layout_init(128, 128, 0, D.DAMP_STATE_FP32), hv=32)
+    mixed = _fake_pool(L, lo, hv=32)
+    acc = L.damp_calib_accumulate
+    assert acc(ctypes.byref(cal), 2, ctypes.byref(pool), 0, p, 4, None, p, None) == \
+        D.DAMP_ERR_INVALID_ARG  # domain out of range
+    st, msg = _status(acc, ctypes.byref(cal), 0, ctypes.byref(mixed), 0, p, 4, None, p, None)
+    assert st == D.DAMP_ERR_INVALID_ARG and "FP32" in msg
+    assert acc(ctypes.byref(cal), 0, ctypes.byref(pool), 0, None, 4, None, p, None) == \
+        D.DAMP_ERR_INVALID_ARG
+    assert acc(ctypes.byref(cal), 0, ctypes.byref(pool), 0, p, 0, None, p, None) == D.DAMP_OK
+    seq = L.damp_calibrate_sequence
+    args = [ctypes.byref(cal), 0, ctypes.byref(pool), 0, p, 4, 64, 8, 16, p, p, p, p, p, None]
+    for i, val in ((6, -1), (7, 0), (8, 5)):  # T, stride, num_k_heads
+        a = list(args)
+        a[i] = val
+        assert seq(*a) == D.DAMP_ERR_INVALID_ARG, i
+    a = list(args)
+    a[6] = 0
+    assert seq(*a) == D.DAMP_OK
+    sel = (ctypes.c_int32 * (32 * 16))()
+    perm = (ctypes.c_uint8 * (32 * 128))()
+    fin = L.damp_calib_finalize
+    assert fin(ctypes.byref(cal), 7, 16, 1e-4, None, sel, perm, None, None, None) == \
+        D.DAMP_ERR_INVALID_ARG
+    assert fin(ctypes.byref(cal), 0, 129, 1e-4, None, sel, perm, None, None, None) == \
+        D.DAMP_ERR_INVALID_ARG
+    assert fin(ctypes.byref(cal), 0, 16, 0.0, None, sel, perm, None, None, None) == \
+        D.DAMP_ERR_INVALID_ARG
+    assert fin(ctypes.byref(cal), D.DAMP_SEL_RANDOM, 16, 1e-4, None, sel, perm, None, None,
+               None) == D.DAMP_ERR_INVALID_ARG
