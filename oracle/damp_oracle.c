@@ -142,29 +142,38 @@ void orc_hadamard32(const float* x, float* y) {
 
 /* ------------------------------------------------- Eq. (3): one-row INT8 */
 
-/* Scale and zero point of a row (Eq. (3) with b = 8). */
-void orc_quant_params(const float* x, int n, float* s_out, float* z_out) {
+/* Scale and zero point of n values with 2^b - 1 = `levels` steps (Eq. (3)). */
+static void orc_quant_params_levels(const float* x, int n, float levels, float* s_out,
+                                    float* z_out) {
   float lo = x[0], hi = x[0];
   for (int j = 1; j < n; ++j) {
     if (x[j] < lo) lo = x[j];
     if (x[j] > hi) hi = x[j];
   }
-  float s = (hi - lo) / 255.0f;
+  float s = (hi - lo) / levels;
   if (!(s >= FLT_MIN)) {           /* constant row */
-    s = fabsf(lo) / 255.0f;
+    s = fabsf(lo) / levels;
     if (!(s >= FLT_MIN)) s = 1.0f; /* zero row */
   }
   *s_out = s;
   *z_out = rintf(-lo / s);
 }
 
-/* One code: round(x / s) + z, saturated to the unsigned 8-bit range. */
-static uint8_t orc_code(float x, float s, float z) {
+/* Scale and zero point of a row (Eq. (3) with b = 8). */
+void orc_quant_params(const float* x, int n, float* s_out, float* z_out) {
+  orc_quant_params_levels(x, n, 255.0f, s_out, z_out);
+}
+
+/* One code: round(x / s) + z, saturated to [0, levels]. */
+static uint8_t orc_code_levels(float x, float s, float z, float levels) {
   float c = rintf(x / s) + z;
   if (c < 0.0f) c = 0.0f;
-  if (c > 255.0f) c = 255.0f;
+  if (c > levels) c = levels;
   return (uint8_t)c;
 }
+
+/* One code: round(x / s) + z, saturated to the unsigned 8-bit range. */
+static uint8_t orc_code(float x, float s, float z) { return orc_code_levels(x, s, z, 255.0f); }
 
 /* Reconstruction Q(x) = s * (c - z). */
 static float orc_decode(uint8_t c, float s, float z) { return s * ((float)c - z); }
@@ -181,9 +190,10 @@ void orc_dequant_row(const uint8_t* codes, int n, float s, float z, float* out) 
 /* One group with FP16 metadata (App. A.1, integer formats): s from Eq. (3) in
  * fp32, stored in FP16; z from the stored s, stored in FP16; codes from the
  * stored pair. s and z are returned widened to fp32. */
-void orc_quant_group_fp16(const float* x, int n, uint8_t* codes, float* s_out, float* z_out) {
+static void orc_quant_group_fp16_levels(const float* x, int n, float levels, uint8_t* codes,
+                                        float* s_out, float* z_out) {
   float s, z;
-  orc_quant_params(x, n, &s, &z);
+  orc_quant_params_levels(x, n, levels, &s, &z);
   float lo = x[0];
   for (int j = 1; j < n; ++j)
     if (x[j] < lo) lo = x[j];
@@ -194,43 +204,175 @@ void orc_quant_group_fp16(const float* x, int n, uint8_t* codes, float* s_out, f
   if (zf > 65504.0f) zf = 65504.0f;
   if (zf < -65504.0f) zf = -65504.0f;
   float z16 = orc_from_fp16(orc_to_fp16(zf));
-  for (int j = 0; j < n; ++j) codes[j] = orc_code(x[j], s16, z16);
+  for (int j = 0; j < n; ++j) codes[j] = orc_code_levels(x[j], s16, z16, levels);
   *s_out = s16;
   *z_out = z16;
+}
+
+void orc_quant_group_fp16(const float* x, int n, uint8_t* codes, float* s_out, float* z_out) {
+  orc_quant_group_fp16_levels(x, n, 255.0f, codes, s_out, z_out);
+}
+
+/* INT4 of App. A.1: as above with 15 steps, codes in [0, 15]. */
+void orc_quant_group_fp16_u4(const float* x, int n, uint8_t* codes, float* s_out, float* z_out) {
+  orc_quant_group_fp16_levels(x, n, 15.0f, codes, s_out, z_out);
+}
+
+/* ------------------------------------------- small floating-point codes */
+
+/* OCP E4M3 (FN variant: bias 7, no infinities, largest finite 448), round to
+ * nearest even, saturating at +-448. Exact arithmetic in double. */
+uint8_t orc_to_e4m3(float f) {
+  uint8_t sign = signbit(f) ? 0x80 : 0x00;
+  double a = fabs((double)f);
+  if (a != a) return 0x7F;                         /* NaN */
+  if (a < 0.015625) {                              /* below 2^-6: steps of 2^-9 */
+    double m = rint(a * 512.0);                    /* 8 is the first normal */
+    return (uint8_t)(sign | (uint8_t)m);
+  }
+  int e2;
+  frexp(a, &e2);
+  int e = e2 - 1;                                  /* a in [2^e, 2^(e+1)) */
+  double m = rint(ldexp(a, 3 - e));                /* in [8, 16] */
+  if (m == 16.0) {
+    m = 8.0;
+    e += 1;
+  }
+  if (e > 8 || (e == 8 && m > 14.0)) return (uint8_t)(sign | 0x7E);  /* saturate at 448 */
+  return (uint8_t)(sign | (uint8_t)((e + 7) << 3) | (uint8_t)(m - 8.0));
+}
+
+float orc_from_e4m3(uint8_t c) {
+  int e = (c >> 3) & 15, m = c & 7;
+  double v = e == 0 ? ldexp((double)m, -9) : ldexp((double)(8 + m), e - 10);
+  if ((c & 0x7F) == 0x7F) v = NAN;
+  return (float)((c & 0x80) ? -v : v);
+}
+
+/* E2M1 (bias 1; magnitudes 0, 0.5, 1, 1.5, 2, 3, 4, 6), round to nearest
+ * even, saturating at +-6; bit 3 is the sign. */
+uint8_t orc_to_e2m1(float f) {
+  uint8_t sign = signbit(f) ? 0x8 : 0x0;
+  double a = fabs((double)f);
+  if (a >= 6.0) return (uint8_t)(sign | 0x7);
+  if (a < 1.0) return (uint8_t)(sign | (uint8_t)rint(a * 2.0));  /* 2 is the first normal */
+  int e2;
+  frexp(a, &e2);
+  int e = e2 - 1;                                  /* a in [2^e, 2^(e+1)), e in 0..2 */
+  double m = rint(ldexp(a, 1 - e));                /* in [2, 4] */
+  if (m == 4.0) {
+    m = 2.0;
+    e += 1;
+  }
+  if (e > 2) return (uint8_t)(sign | 0x7);
+  return (uint8_t)(sign | (uint8_t)((e + 1) << 1) | (uint8_t)(m - 2.0));
+}
+
+float orc_from_e2m1(uint8_t c) {
+  int e = (c >> 1) & 3, m = c & 1;
+  double v = e == 0 ? 0.5 * m : ldexp(1.0 + 0.5 * m, e - 1);
+  return (float)((c & 0x8) ? -v : v);
+}
+
+void orc_e4m3_round(const float* x, uint8_t* out, int64_t n) {
+  for (int64_t i = 0; i < n; ++i) out[i] = orc_to_e4m3(x[i]);
+}
+void orc_e4m3_widen(const uint8_t* c, float* out, int64_t n) {
+  for (int64_t i = 0; i < n; ++i) out[i] = orc_from_e4m3(c[i]);
+}
+void orc_e2m1_round(const float* x, uint8_t* out, int64_t n) {
+  for (int64_t i = 0; i < n; ++i) out[i] = orc_to_e2m1(x[i]);
+}
+void orc_e2m1_widen(const uint8_t* c, float* out, int64_t n) {
+  for (int64_t i = 0; i < n; ++i) out[i] = orc_from_e2m1(c[i]);
+}
+
+/* FP8 of App. A.1 (Eq. (16)): one fp32 scale per group, no zero point:
+ * s = max(max|x|, 1e-10) / 448, q = E4M3(clip(x / s, -448, 448)). */
+void orc_quant_group_e4m3(const float* x, int n, uint8_t* codes, float* s_out) {
+  float amax = 0.0f;
+  for (int j = 0; j < n; ++j)
+    if (fabsf(x[j]) > amax) amax = fabsf(x[j]);
+  float s = (amax > 1e-10f ? amax : 1e-10f) / 448.0f;
+  for (int j = 0; j < n; ++j) {
+    float y = x[j] / s;
+    if (y > 448.0f) y = 448.0f;
+    if (y < -448.0f) y = -448.0f;
+    codes[j] = orc_to_e4m3(y);
+  }
+  *s_out = s;
+}
+
+/* NVFP4 of App. A.1: the global scale of a tile's low tier from its largest
+ * magnitude, s_g = amax / (6 * 448) (1 if amax is 0). */
+float orc_nvfp4_global(float amax) {
+  return amax > 0.0f ? amax / 2688.0f : 1.0f;
+}
+
+/* One NVFP4 block: E4M3 block scale s_b = E4M3(max|x| / (6 s_g)); codes
+ * E2M1(x / (s_b s_g)) (all 0 if s_b is 0). Returns the block-scale code. */
+uint8_t orc_quant_block_e2m1(const float* x, int n, float s_g, uint8_t* codes) {
+  float amax = 0.0f;
+  for (int j = 0; j < n; ++j)
+    if (fabsf(x[j]) > amax) amax = fabsf(x[j]);
+  float t = amax / (6.0f * s_g);
+  if (t > 448.0f) t = 448.0f;
+  uint8_t sb = orc_to_e4m3(t);
+  float scale = orc_from_e4m3(sb) * s_g;
+  for (int j = 0; j < n; ++j) codes[j] = scale > 0.0f ? orc_to_e2m1(x[j] / scale) : 0;
+  return sb;
 }
 
 /* ------------------------------------------------------- layout (Eq. 17) */
 
 /* Storage format: fmt[0] high-tier type (1 BF16, 2 FP16), fmt[1] values per
- * (s, z) pair along d_v, fmt[2] metadata type (0 FP32, 2 FP16), fmt[3] 1 for
- * the block-32 Hadamard transform of the low tier. NULL: BF16, one pair per
- * row, FP32 metadata, no transform. */
+ * metadata group along d_v, fmt[2] metadata type (0 FP32, 2 FP16), fmt[3] 1
+ * for the block-32 Hadamard transform of the low tier, fmt[4] code type (3
+ * UINT8, 4 UINT4, 5 E4M3, 6 E2M1; the App. A.1 format table). NULL: BF16,
+ * one UINT8 (s, z) pair per row in FP32, no transform. */
+enum { ORC_CODE_U8 = 3, ORC_CODE_U4 = 4, ORC_CODE_E4M3 = 5, ORC_CODE_E2M1 = 6 };
 typedef struct {
-  int hi_fp16, group, meta_fp16, hadamard;
+  int hi_fp16, group, meta_fp16, hadamard, code;
 } orc_fmt_t;
 
 static orc_fmt_t orc_fmt(const int32_t* f, int dv) {
-  orc_fmt_t r = {0, dv, 0, 0};
+  orc_fmt_t r = {0, dv, 0, 0, ORC_CODE_U8};
   if (f) {
     r.hi_fp16 = f[0] == 2;
     r.group = f[1];
     r.meta_fp16 = f[2] == 2;
     r.hadamard = f[3] != 0;
+    r.code = f[4];
   }
   return r;
 }
 
-static int64_t orc_meta_row_bytes(orc_fmt_t f, int dv) {
-  return (int64_t)(dv / f.group) * 2 * (f.meta_fp16 ? 2 : 4);
+static int orc_code_is_nibble(orc_fmt_t f) {
+  return f.code == ORC_CODE_U4 || f.code == ORC_CODE_E2M1;
 }
 
-/* Bytes of one tile: high tier, codes, then the (s, z) metadata of each low
- * row, group by group. */
+/* Bytes per low row: codes (two per byte for 4-bit codes, the even column in
+ * the low nibble) and metadata: (s, z) per group for the integer codes, an
+ * fp32 s per group for E4M3, an E4M3 block scale per group for E2M1. */
+static int64_t orc_code_row_bytes(orc_fmt_t f, int dv) {
+  return orc_code_is_nibble(f) ? dv / 2 : dv;
+}
+static int64_t orc_meta_row_bytes(orc_fmt_t f, int dv) {
+  const int64_t groups = dv / f.group;
+  if (f.code == ORC_CODE_E4M3) return groups * 4;
+  if (f.code == ORC_CODE_E2M1) return groups;
+  return groups * 2 * (f.meta_fp16 ? 2 : 4);
+}
+/* E2M1 tiles end with the fp32 global scale of their low tier. */
+static int64_t orc_tile_tail_bytes(orc_fmt_t f) { return f.code == ORC_CODE_E2M1 ? 4 : 0; }
+
+/* Bytes of one tile: high tier, codes, the metadata of each low row group by
+ * group, then (E2M1) the global scale. */
 int64_t orc_tile_bytes(int kind, const int32_t* fmt, int dk, int dv, int k_hi) {
   if (kind == ORC_KIND_FP32) return (int64_t)dk * dv * 4;
   orc_fmt_t f = orc_fmt(fmt, dv);
-  return (int64_t)k_hi * dv * 2 + (int64_t)(dk - k_hi) * dv +
-         (int64_t)(dk - k_hi) * orc_meta_row_bytes(f, dv);
+  return (int64_t)k_hi * dv * 2 + (int64_t)(dk - k_hi) * orc_code_row_bytes(f, dv) +
+         (int64_t)(dk - k_hi) * orc_meta_row_bytes(f, dv) + orc_tile_tail_bytes(f);
 }
 
 /* Storage bits per value of a mixed layout, general form of Eq. (7): the low
@@ -242,6 +384,25 @@ double orc_bits_per_value(int dk, int k_hi, int hi_bits, int code_bits, int grou
   return b_lo + ((double)k_hi / (double)dk) * (b_hi - b_lo);
 }
 
+/* Codes of one low row as one byte per value. */
+static void orc_codes_unpack(orc_fmt_t f, const uint8_t* row, int dv, uint8_t* c) {
+  if (!orc_code_is_nibble(f)) {
+    memcpy(c, row, (size_t)dv);
+    return;
+  }
+  for (int j = 0; j < dv; j += 2) {
+    c[j] = row[j / 2] & 0xF;
+    c[j + 1] = row[j / 2] >> 4;
+  }
+}
+static void orc_codes_pack(orc_fmt_t f, const uint8_t* c, int dv, uint8_t* row) {
+  if (!orc_code_is_nibble(f)) {
+    memcpy(row, c, (size_t)dv);
+    return;
+  }
+  for (int j = 0; j < dv; j += 2) row[j / 2] = (uint8_t)((c[j] & 0xF) | (c[j + 1] << 4));
+}
+
 /* Decode tile rows (in tile order) into S[dk][dv]. */
 static void orc_tile_decode(int kind, orc_fmt_t f, int dk, int dv, int k_hi,
                             const uint8_t* tile, float* S) {
@@ -251,8 +412,11 @@ static void orc_tile_decode(int kind, orc_fmt_t f, int dk, int dv, int k_hi,
   }
   const uint8_t* hi = tile;
   const uint8_t* codes = tile + (size_t)k_hi * dv * 2;
-  const uint8_t* meta = codes + (size_t)(dk - k_hi) * dv;
+  const uint8_t* meta = codes + (size_t)(dk - k_hi) * orc_code_row_bytes(f, dv);
   const int64_t mrow = orc_meta_row_bytes(f, dv);
+  float s_g = 1.0f;
+  if (f.code == ORC_CODE_E2M1) memcpy(&s_g, meta + (size_t)(dk - k_hi) * mrow, 4);
+  uint8_t crow[4096];
   for (int r = 0; r < dk; ++r) {
     float* x = S + (size_t)r * dv;
     if (r < k_hi) {
@@ -264,9 +428,23 @@ static void orc_tile_decode(int kind, orc_fmt_t f, int dk, int dv, int k_hi,
       continue;
     }
     int l = r - k_hi;
+    orc_codes_unpack(f, codes + (size_t)l * orc_code_row_bytes(f, dv), dv, crow);
     for (int g = 0; g < dv / f.group; ++g) {
       float sz[2];
       const uint8_t* m = meta + (size_t)l * mrow;
+      float* xg = x + (size_t)g * f.group;
+      const uint8_t* cg = crow + (size_t)g * f.group;
+      if (f.code == ORC_CODE_E4M3) {            /* x = s q */
+        float sc;
+        memcpy(&sc, m + (size_t)g * 4, 4);
+        for (int j = 0; j < f.group; ++j) xg[j] = sc * orc_from_e4m3(cg[j]);
+        continue;
+      }
+      if (f.code == ORC_CODE_E2M1) {            /* x = q (s_b s_g) */
+        const float scale = orc_from_e4m3(m[g]) * s_g;
+        for (int j = 0; j < f.group; ++j) xg[j] = orc_from_e2m1(cg[j]) * scale;
+        continue;
+      }
       if (f.meta_fp16) {
         uint16_t h[2];
         memcpy(h, m + (size_t)g * 4, 4);
@@ -275,8 +453,7 @@ static void orc_tile_decode(int kind, orc_fmt_t f, int dk, int dv, int k_hi,
       } else {
         memcpy(sz, m + (size_t)g * 8, 8);
       }
-      float* xg = x + (size_t)g * f.group;
-      orc_dequant_row(codes + (size_t)l * dv + (size_t)g * f.group, f.group, sz[0], sz[1], xg);
+      orc_dequant_row(cg, f.group, sz[0], sz[1], xg);
       if (f.hadamard) {
         float y[32];
         orc_hadamard32(xg, y);
@@ -295,8 +472,17 @@ static void orc_tile_encode(int kind, orc_fmt_t f, int dk, int dv, int k_hi, con
   }
   uint8_t* hi = tile;
   uint8_t* codes = tile + (size_t)k_hi * dv * 2;
-  uint8_t* meta = codes + (size_t)(dk - k_hi) * dv;
+  uint8_t* meta = codes + (size_t)(dk - k_hi) * orc_code_row_bytes(f, dv);
   const int64_t mrow = orc_meta_row_bytes(f, dv);
+  float s_g = 1.0f;
+  if (f.code == ORC_CODE_E2M1) {  /* the global scale of the low tier */
+    float amax = 0.0f;
+    for (int64_t i = (int64_t)k_hi * dv; i < (int64_t)dk * dv; ++i)
+      if (fabsf(S[i]) > amax) amax = fabsf(S[i]);
+    s_g = orc_nvfp4_global(amax);
+    memcpy(meta + (size_t)(dk - k_hi) * mrow, &s_g, 4);
+  }
+  uint8_t crow[4096];
   for (int r = 0; r < dk; ++r) {
     const float* x = S + (size_t)r * dv;
     if (r < k_hi) {
@@ -314,10 +500,19 @@ static void orc_tile_encode(int kind, orc_fmt_t f, int dk, int dv, int k_hi, con
         orc_hadamard32(xg, y);
         xg = y;
       }
-      uint8_t* c = codes + (size_t)l * dv + (size_t)g * f.group;
+      uint8_t* c = crow + (size_t)g * f.group;
       uint8_t* m = meta + (size_t)l * mrow;
       float sz[2];
-      if (f.meta_fp16) {
+      if (f.code == ORC_CODE_E4M3) {
+        orc_quant_group_e4m3(xg, f.group, c, &sz[0]);
+        memcpy(m + (size_t)g * 4, &sz[0], 4);
+      } else if (f.code == ORC_CODE_E2M1) {
+        m[g] = orc_quant_block_e2m1(xg, f.group, s_g, c);
+      } else if (f.code == ORC_CODE_U4) {
+        orc_quant_group_fp16_u4(xg, f.group, c, &sz[0], &sz[1]);
+        uint16_t h[2] = {orc_to_fp16(sz[0]), orc_to_fp16(sz[1])};
+        memcpy(m + (size_t)g * 4, h, 4);
+      } else if (f.meta_fp16) {
         orc_quant_group_fp16(xg, f.group, c, &sz[0], &sz[1]);
         uint16_t h[2] = {orc_to_fp16(sz[0]), orc_to_fp16(sz[1])};
         memcpy(m + (size_t)g * 4, h, 4);
@@ -326,6 +521,7 @@ static void orc_tile_encode(int kind, orc_fmt_t f, int dk, int dv, int k_hi, con
         memcpy(m + (size_t)g * 8, sz, 8);
       }
     }
+    orc_codes_pack(f, crow, dv, codes + (size_t)l * orc_code_row_bytes(f, dv));
   }
 }
 
@@ -626,6 +822,7 @@ int orc_select(int is_kda, int N, int H, int dk, int dv, const float* states,
  * reconstruction is taken back to the state's domain before the difference;
  * squared differences are summed in double over ascending columns. */
 static double orc_row_error_fmt(const float* x, int n, orc_fmt_t f) {
+  if (f.code != ORC_CODE_U8) return NAN;  /* calibration takes the UINT8 tiers */
   if (!f.meta_fp16) return orc_row_error(x, n);
   double acc = 0.0;
   for (int g0 = 0; g0 < n; g0 += f.group) {

@@ -31,11 +31,19 @@ LIB = os.path.join(HERE, "liboracle.so")
 KIND_FP32 = 0
 KIND_MIXED = 1
 
-# Storage formats (high-tier type, values per (s, z) pair, metadata type,
-# Hadamard): types 1 = BF16, 2 = FP16, 0 = FP32. None is the default format:
-# BF16 high tier, one fp32 (s, z) pair per row, no transform.
-FMT_PAPER = (2, 32, 2, 1)        # App. A.1: INT8 + H32, FP16 (s, z) per 32; FP16 tier
-FMT_PAPER_PLAIN = (2, 32, 2, 0)  # the same without the transform
+# Storage formats (high-tier type, values per metadata group, metadata type,
+# Hadamard[, code type]): types 1 = BF16, 2 = FP16, 0 = FP32, 5 = E4M3; code
+# types 3 = UINT8 (the default when omitted), 4 = UINT4, 5 = E4M3, 6 = E2M1.
+# None is the default format: BF16 high tier, one fp32 (s, z) pair per row,
+# no transform. The others are rows of App. A.1's format table, each with an
+# FP16 high tier.
+FMT_PAPER = (2, 32, 2, 1)        # INT8 + H32, FP16 (s, z) per 32 (the paper's layout)
+FMT_PAPER_PLAIN = (2, 32, 2, 0)  # INT8, FP16 (s, z) per 32
+FMT_INT4_H32 = (2, 32, 2, 1, 4)  # INT4 + H32, FP16 (s, z) per 32
+FMT_INT4 = (2, 32, 2, 0, 4)      # INT4, FP16 (s, z) per 32
+FMT_FP8 = (2, 32, 0, 0, 5)       # E4M3 codes, one fp32 scale per 32 (Eq. (16))
+FMT_NVFP4 = (2, 16, 5, 0, 6)     # E2M1 codes, E4M3 scale per 16, fp32 scale per tile
+CODE_U8, CODE_U4, CODE_E4M3, CODE_E2M1 = 3, 4, 5, 6
 
 _lib = None
 
@@ -70,6 +78,14 @@ def lib():
         L.orc_fp16_widen.argtypes = [vp, vp, i64]
         L.orc_hadamard32.argtypes = [vp, vp]
         L.orc_quant_group_fp16.argtypes = [vp, i32, vp, vp, vp]
+        L.orc_quant_group_fp16_u4.argtypes = [vp, i32, vp, vp, vp]
+        L.orc_quant_group_e4m3.argtypes = [vp, i32, vp, vp]
+        L.orc_quant_block_e2m1.argtypes = [vp, i32, f32, vp]
+        L.orc_quant_block_e2m1.restype = ctypes.c_uint8
+        L.orc_nvfp4_global.argtypes = [f32]
+        L.orc_nvfp4_global.restype = f32
+        for nm in ("orc_e4m3_round", "orc_e4m3_widen", "orc_e2m1_round", "orc_e2m1_widen"):
+            getattr(L, nm).argtypes = [vp, vp, i64]
         L.orc_quant_params.argtypes = [vp, i32, vp, vp]
         L.orc_quant_row.argtypes = [vp, i32, vp, vp, vp]
         L.orc_dequant_row.argtypes = [vp, i32, f32, f32, vp]
@@ -150,13 +166,80 @@ def quant_group_fp16(x):
     return codes, np.float32(s.value), np.float32(z.value)
 
 
+def fmt5(fmt):
+    """The five-field form of a format (code type UINT8 when omitted)."""
+    return None if fmt is None else (tuple(fmt) + (CODE_U8,))[:5]
+
+
 def _fmt_arr(fmt):
     if fmt is None:
         return None
-    hi, group, meta, had = fmt
-    assert hi in (1, 2) and meta in (0, 2) and group > 0
-    assert not had or group == 32
-    return np.ascontiguousarray(fmt, dtype=np.int32)
+    hi, group, meta, had, code = fmt5(fmt)
+    assert hi in (1, 2) and group > 0
+    assert (code, meta, group) in ((CODE_U8, 0, group), (CODE_U8, 2, group), (CODE_U4, 2, 32),
+                                   (CODE_E4M3, 0, 32), (CODE_E2M1, 5, 16))
+    assert not had or (group == 32 and code in (CODE_U8, CODE_U4))
+    return np.ascontiguousarray(fmt5(fmt), dtype=np.int32)
+
+
+def e4m3_round(x) -> np.ndarray:
+    """fp32 -> OCP E4M3 (FN) codes, round to nearest even, saturating."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    out = np.empty(x.shape, np.uint8)
+    lib().orc_e4m3_round(_p(x), _p(out), x.size)
+    return out
+
+
+def e4m3_widen(c) -> np.ndarray:
+    c = np.ascontiguousarray(c, dtype=np.uint8)
+    out = np.empty(c.shape, np.float32)
+    lib().orc_e4m3_widen(_p(c), _p(out), c.size)
+    return out
+
+
+def e2m1_round(x) -> np.ndarray:
+    """fp32 -> E2M1 codes (sign in bit 3), round to nearest even, saturating."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    out = np.empty(x.shape, np.uint8)
+    lib().orc_e2m1_round(_p(x), _p(out), x.size)
+    return out
+
+
+def e2m1_widen(c) -> np.ndarray:
+    c = np.ascontiguousarray(c, dtype=np.uint8)
+    out = np.empty(c.shape, np.float32)
+    lib().orc_e2m1_widen(_p(c), _p(out), c.size)
+    return out
+
+
+def quant_group_fp16_u4(x):
+    """INT4 (App. A.1) on one group with FP16 (s, z): (codes, s, z)."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    codes = np.empty(x.shape, np.uint8)
+    s, z = ctypes.c_float(), ctypes.c_float()
+    lib().orc_quant_group_fp16_u4(_p(x), x.size, _p(codes), ctypes.byref(s), ctypes.byref(z))
+    return codes, np.float32(s.value), np.float32(z.value)
+
+
+def quant_group_e4m3(x):
+    """FP8 of Eq. (16) on one group: (E4M3 codes, fp32 s)."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    codes = np.empty(x.shape, np.uint8)
+    s = ctypes.c_float()
+    lib().orc_quant_group_e4m3(_p(x), x.size, _p(codes), ctypes.byref(s))
+    return codes, np.float32(s.value)
+
+
+def nvfp4_global(amax: float) -> np.float32:
+    return np.float32(lib().orc_nvfp4_global(ctypes.c_float(amax)))
+
+
+def quant_block_e2m1(x, s_g):
+    """One NVFP4 block: (E2M1 codes, E4M3 block-scale code)."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    codes = np.empty(x.shape, np.uint8)
+    sb = lib().orc_quant_block_e2m1(_p(x), x.size, ctypes.c_float(s_g), _p(codes))
+    return codes, np.uint8(sb)
 
 
 def quant_row(x):
@@ -368,6 +451,8 @@ class Calib:
     Q_lo's low tier as for Pool (None: one fp32 (s, z) per row)."""
 
     def __init__(self, *, kda: bool, H: int, dk: int, dv: int, num_domains: int = 1, fmt=None):
+        if fmt is not None and fmt5(fmt)[4] != CODE_U8:
+            raise ValueError("calibration takes the UINT8 low tiers")
         self.kda, self.H, self.dk, self.dv, self.fmt = kda, H, dk, dv, fmt
         self.sums = np.zeros((num_domains, 3, H, dk))
         self.counts = np.zeros(num_domains)
