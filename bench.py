@@ -187,12 +187,13 @@ class Workload:
         warm state (permuted by the selection). Set r is slots r*B .. r*B+B-1
         in order, or with `scattered` B slots drawn at random from the whole
         pool, in random order. `tiers` = (hi_dtype, group, meta_dtype,
-        hadamard) selects another storage format than the default."""
+        hadamard[, code_dtype]) selects another storage format than the default."""
         torch, D = self.torch, self.D
         B, HV, d = self.B, self.HV, self.d
         layout = D.damp_layout_init(d, d, k_hi, kind)
         if tiers is not None:
-            layout.hi_dtype, layout.group, layout.meta_dtype, layout.hadamard = tiers
+            (layout.hi_dtype, layout.group, layout.meta_dtype, layout.hadamard,
+             layout.code_dtype) = (tuple(tiers) + (D.DAMP_DT_U8,))[:5]
         pool = D.Pool(layout, 1, B * rotations, HV)
         if scattered:
             order = torch.from_numpy(self.inputs.slot_order(7, B * rotations, B * rotations)).cuda()
@@ -525,12 +526,17 @@ def main():
         log(f"  uniform int8: {i8['us_per_step']:.1f} us/step, kernel {i8['kernel_us']:.1f} us")
         extra["baselines_gdn"] = {"fp32_state": fp, "uniform_int8": i8,
                                   "speedup_vs_fp32_state": fp["kernel_us"] / head["kernel_us"]}
-        # the paper's own tiers: FP16 rows, INT8 groups of 32 with FP16 (s, z)
+        # the paper's own tiers (FP16 rows, INT8 groups of 32 with FP16 (s, z))
+        # and the other rows of its format table
         paper = {}
-        for name, had in (("int8_h32", 1), ("int8_g32", 0)):
+        fp16, u8 = D.DAMP_DT_FP16, D.DAMP_DT_U8
+        for name, tiers in (("int8_h32", (fp16, 32, fp16, 1, u8)), ("int8_g32", (fp16, 32, fp16, 0, u8)),
+                            ("int4_h32", (fp16, 32, fp16, 1, D.DAMP_DT_U4)),
+                            ("int4_g32", (fp16, 32, fp16, 0, D.DAMP_DT_U4)),
+                            ("fp8_e4m3", (fp16, 32, D.DAMP_DT_FP32, 0, D.DAMP_DT_E4M3)),
+                            ("nvfp4", (fp16, 16, D.DAMP_DT_E4M3, 0, D.DAMP_DT_E2M1))):
             r = measure(torch, D, gdn, D.DAMP_STATE_MIXED, k_hi, args.rotations, args.warmup,
-                        args.steps, torch.bfloat16,
-                        tiers=(D.DAMP_DT_FP16, 32, D.DAMP_DT_FP16, had))
+                        args.steps, torch.bfloat16, tiers=tiers)
             log(f"  paper tiers ({name}): kernel {r['kernel_us']:.1f} us, "
                 f"{r['kernel_gbs']:.0f} GB/s, {r['bits_per_value']} bits/value")
             paper[name] = r

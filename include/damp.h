@@ -42,6 +42,18 @@
  *            the codes of each group of 32 are those of its normalized
  *            Hadamard transform
  *     [meta] (d_k - k_hi) x (d_v / 32) x {s, z} FP16 (4 bytes per group)
+ *   DAMP_STATE_MIXED, the other rows of App. A.1's format table (FP16 high
+ *   tier, hi_dtype = DAMP_DT_FP16; d_v >= 32):
+ *     INT4 (code_dtype = DAMP_DT_U4, group = 32, meta_dtype = DAMP_DT_FP16,
+ *       hadamard = 0 or 1): [code] (d_k - k_hi) x d_v / 2 bytes, two codes
+ *       per byte, the even column in the low nibble; [meta] as INT8.
+ *     FP8 (code_dtype = DAMP_DT_E4M3, group = 32, meta_dtype = DAMP_DT_FP32,
+ *       hadamard = 0): [code] (d_k - k_hi) x d_v E4M3 bytes; [meta]
+ *       (d_k - k_hi) x (d_v / 32) fp32 scales.
+ *     NVFP4 (code_dtype = DAMP_DT_E2M1, group = 16, meta_dtype =
+ *       DAMP_DT_E4M3, hadamard = 0): [code] (d_k - k_hi) x d_v / 2 bytes as
+ *       INT4; [meta] (d_k - k_hi) x (d_v / 16) E4M3 block scales; then one
+ *       fp32 global scale for the tile's low tier.
  *   DAMP_STATE_FP32:
  *     d_k x d_v fp32, row-major
  *
@@ -57,7 +69,16 @@
  * Sylvester matrix H, its own inverse), then round s to FP16 (kept within
  * [2^-24, 65504]), compute z = round(-min / s) from the stored s, round it
  * to FP16 (within +-65504), and code with the stored pair; reconstruction is
- * s * (c - z) followed by the inverse transform.
+ * s * (c - z) followed by the inverse transform. INT4 is the same with 15
+ * steps and codes in [0, 15].
+ * FP8 (Eq. (16)): per group s = max(max |x|, 1e-10) / 448 (fp32), codes
+ * E4M3(clip(x / s, -448, 448)) in the OCP E4M3 encoding (bias 7, largest
+ * finite 448) rounded to nearest even; x_hat = s * q.
+ * NVFP4: the tile's low tier has the global scale s_g = amax / 2688 (amax
+ * its largest magnitude; 1 if amax is 0); each block of 16 the E4M3 scale
+ * s_b = E4M3(min(block amax / (6 s_g), 448)); codes E2M1(x / (s_b s_g)) with
+ * magnitudes {0, 0.5, 1, 1.5, 2, 3, 4, 6} (sign in bit 3), rounded to nearest
+ * even and saturated at 6 (zero codes where s_b is 0); x_hat = q (s_b s_g).
  * The tile stride in a pool is the tile size rounded up to 128 bytes.
  */
 #ifndef DAMP_H
@@ -77,7 +98,15 @@ typedef enum {
   DAMP_ERR_HIP = 3          /* a HIP runtime call failed */
 } damp_status;
 
-typedef enum { DAMP_DT_FP32 = 0, DAMP_DT_BF16 = 1, DAMP_DT_FP16 = 2 } damp_dtype;
+typedef enum {
+  DAMP_DT_FP32 = 0,
+  DAMP_DT_BF16 = 1,
+  DAMP_DT_FP16 = 2,
+  DAMP_DT_U8 = 3,    /* low-tier codes: unsigned 8-bit (the default) */
+  DAMP_DT_U4 = 4,    /* unsigned 4-bit, two per byte */
+  DAMP_DT_E4M3 = 5,  /* OCP FP8 E4M3 (codes, or NVFP4 block scales) */
+  DAMP_DT_E2M1 = 6   /* FP4 E2M1, two per byte */
+} damp_dtype;
 
 typedef enum {
   DAMP_STATE_FP32 = 0,  /* uncompressed state (the deployment baseline) */
@@ -95,14 +124,15 @@ typedef struct {
   int32_t group;      /* values per (s, z) pair along d_v; d_v = one per row */
   int32_t meta_dtype; /* damp_dtype of s and z (FP32 per row, or FP16 per group of 32) */
   int32_t hadamard;   /* 1 = block-32 Hadamard before quantization (paper's tiers) */
+  int32_t code_dtype; /* damp_dtype of the low-tier codes: U8 (default), U4, E4M3, E2M1 */
 } damp_layout;
 
 /* Fills `out` with the default layout: BF16 high tier, one fp32 (s, z) pair
- * per low-tier row, no Hadamard. Kernels exist for d_k == d_v in
- * {16, 32, 64, 128}, and for the paper's tiers (FP16 high tier and FP16
- * (s, z) per group of 32, with or without the transform) for d_k == d_v in
- * {32, 64, 128}; other layouts are valid for the size queries but calls that
- * move state return DAMP_ERR_UNSUPPORTED. Returns DAMP_ERR_INVALID_ARG if
+ * per low-tier row, UINT8 codes, no Hadamard. Kernels exist for d_k == d_v
+ * in {16, 32, 64, 128}, and for the paper's tiers and the other formats
+ * above (set the fields after this call) for d_k == d_v in {32, 64, 128};
+ * other layouts are valid for the size queries but calls that move state
+ * return DAMP_ERR_UNSUPPORTED. Returns DAMP_ERR_INVALID_ARG if
  * out is NULL, d_k or d_v is not positive, or k_hi is outside [0, d_k]. */
 damp_status damp_layout_init(damp_layout* out, int32_t d_k, int32_t d_v,
                              int32_t k_hi, int32_t kind);
@@ -131,7 +161,6 @@ typedef struct {
   int32_t num_layers;
   int32_t num_slots;
   int32_t num_v_heads;
-  int32_t reserved;
   void* base;          /* device memory, 256-byte aligned */
   size_t tile_stride;  /* bytes */
   size_t bytes;        /* bytes the pool spans */

@@ -14,6 +14,27 @@ constexpr int kMixed = 1;  // DAMP_STATE_MIXED with the default tiers
 // rows; low rows in groups of 32 values with FP16 (s, z), optionally after
 // the normalized block-32 Hadamard transform.
 constexpr int kPaper = 2;
+// The other rows of App. A.1's format table, each with an FP16 high tier:
+// INT4 (groups of 32, FP16 (s, z), optional block-32 transform), FP8 E4M3
+// (one fp32 scale per group of 32, Eq. (16)) and NVFP4 (E2M1 in blocks of
+// 16 with an E4M3 block scale and one fp32 global scale per tile).
+constexpr int kInt4 = 3;
+constexpr int kFp8 = 4;
+constexpr int kNvfp4 = 5;
+
+template <int KIND>
+constexpr bool is_nibble() {
+  return KIND == kInt4 || KIND == kNvfp4;
+}
+// Bytes of one low-tier row: codes, then metadata.
+template <int KIND, int D>
+constexpr int code_row_bytes() {
+  return is_nibble<KIND>() ? D / 2 : D;
+}
+template <int KIND, int D>
+constexpr int meta_row_bytes() {
+  return KIND == kMixed ? 8 : (KIND == kNvfp4 ? D / 16 : (D / 32) * 4);
+}
 
 // ------------------------------------------------------------ conversions
 
@@ -217,13 +238,14 @@ __device__ __forceinline__ void fwht32_pair(float (&x)[16], bool upper) {
 // fp32 (constant groups as for rows), rounded to FP16 and kept positive and
 // finite; z = round(-min / s) from the stored s, within FP16's finite range,
 // rounded to FP16. Divisions are IEEE (a few per group).
+template <int LEVELS = 255>
 __device__ __forceinline__ void group_qparams_f16(float mn, float mx, float& s16, float& z16,
                                                   float& inv) {
   mn = fminf(mn, dpp_mov<0xb1>(mn));
   mx = fmaxf(mx, dpp_mov<0xb1>(mx));
-  float s = (mx - mn) / 255.0f;
+  float s = (mx - mn) / static_cast<float>(LEVELS);
   if (!(s >= FLT_MIN)) {
-    s = fabsf(mn) / 255.0f;
+    s = fabsf(mn) / static_cast<float>(LEVELS);
     if (!(s >= FLT_MIN)) s = 1.0f;
   }
   s16 = round_f16(s);
@@ -236,6 +258,194 @@ __device__ __forceinline__ void group_qparams_f16(float mn, float mx, float& s16
   inv = fmaf(fmaf(-rc, s16, 1.0f), rc, rc);
 }
 
+// ------------------------------------------ small floating-point codes
+
+// The gfx950 conversions between fp32 and OCP E4M3 (bias 7, largest finite
+// 448) and E2M1 (magnitudes 0, 0.5, 1, 1.5, 2, 3, 4, 6; sign in bit 3): they
+// round to nearest even and saturate at the largest finite value, as the
+// formats' definitions (a scale of 1 leaves the E2M1 values unscaled).
+// Two fp32 values into bytes 2 HI, 2 HI + 1 of `old`.
+template <bool HI>
+__device__ __forceinline__ uint32_t cvt_e4m3x2(float a, float b, uint32_t old) {
+  return static_cast<uint32_t>(__builtin_amdgcn_cvt_pk_fp8_f32(a, b, static_cast<int>(old), HI));
+}
+template <int BYTE>
+__device__ __forceinline__ float e4m3_byte(uint32_t w) {
+  return __builtin_amdgcn_cvt_f32_fp8(static_cast<int>(w), BYTE);
+}
+// Two fp32 values into the nibbles of byte BYTE of `old` (a in the low one).
+template <int BYTE>
+__device__ __forceinline__ uint32_t cvt_e2m1x2(float a, float b, uint32_t old) {
+  return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(old, a, b, 1.0f, BYTE);
+}
+template <int BYTE>
+__device__ __forceinline__ void e2m1_byte(uint32_t w, float& lo, float& hi) {
+  const auto v = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w, 1.0f, BYTE);
+  lo = v[0];
+  hi = v[1];
+}
+
+// 1 / s from the hardware reciprocal refined by one residual step.
+__device__ __forceinline__ float refined_rcp(float s) {
+  const float rc = __builtin_amdgcn_rcpf(s);
+  return fmaf(fmaf(-rc, s, 1.0f), rc, rc);
+}
+
+// NVFP4 global scale of a tile's low tier from its largest magnitude.
+__device__ __forceinline__ float nvfp4_global(float amax) {
+  return amax > 0.0f ? amax / 2688.0f : 1.0f;  // 2688 = 6 * 448
+}
+
+// Where an E2M1 tile keeps its global scale: after the metadata of its low
+// rows (byte-wise, as the offset may be only 2-aligned).
+template <int D>
+__device__ __forceinline__ float load_global_scale(const uint8_t* meta_bytes, int k_hi) {
+  const uint8_t* p = meta_bytes + static_cast<size_t>(D - k_hi) * (D / 16);
+  return __uint_as_float(static_cast<uint32_t>(p[0]) | (static_cast<uint32_t>(p[1]) << 8) |
+                         (static_cast<uint32_t>(p[2]) << 16) | (static_cast<uint32_t>(p[3]) << 24));
+}
+template <int D>
+__device__ __forceinline__ void store_global_scale(uint8_t* meta_bytes, int k_hi, float s_g) {
+  uint8_t* p = meta_bytes + static_cast<size_t>(D - k_hi) * (D / 16);
+  const uint32_t w = __float_as_uint(s_g);
+  p[0] = static_cast<uint8_t>(w);
+  p[1] = static_cast<uint8_t>(w >> 8);
+  p[2] = static_cast<uint8_t>(w >> 16);
+  p[3] = static_cast<uint8_t>(w >> 24);
+}
+
+// Largest value of v over the workgroup (every thread receives it). Called
+// by all threads of the workgroup.
+template <int NT>
+__device__ __forceinline__ float block_max(float v) {
+  __shared__ float part[NT / 64];
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, 64));
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = v;
+  __syncthreads();
+  float r = part[0];
+#pragma unroll
+  for (int i = 1; i < NT / 64; ++i) r = fmaxf(r, part[i]);
+  __syncthreads();
+  return r;
+}
+
+// One lane's slice (16 values = half a group of 32, or one NVFP4 block) of a
+// low row encoded in the table formats. `codes` and `meta_bytes` point at the
+// row's codes and metadata.
+template <int KIND, int D>
+__device__ __forceinline__ void encode_slice_table(const float* x, int cg, int col0, bool had,
+                                                   float s_g, uint8_t* codes, uint8_t* meta) {
+  if constexpr (KIND == kInt4) {
+    float y[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) y[j] = x[j];
+    if (had) {
+      fwht32_pair(y, (cg & 1) != 0);
+#pragma unroll
+      for (int j = 0; j < 16; ++j) y[j] *= kInvSqrt32;
+    }
+    float mn = y[0], mx = y[0];
+#pragma unroll
+    for (int j = 1; j < 16; ++j) {
+      mn = fminf(mn, y[j]);
+      mx = fmaxf(mx, y[j]);
+    }
+    float s16, z16, inv;
+    group_qparams_f16<15>(mn, mx, s16, z16, inv);
+    uint32_t w[2] = {0u, 0u};
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const float c = __builtin_amdgcn_fmed3f(rintf(fmaf(y[j], inv, z16)), 0.0f, 15.0f);
+      w[j >> 3] |= static_cast<uint32_t>(c) << (4 * (j & 7));
+    }
+    store_words<8>(codes + col0 / 2, w);
+    if ((cg & 1) == 0) reinterpret_cast<uint32_t*>(meta)[col0 >> 5] = pack_f16x2(s16, z16);
+  } else if constexpr (KIND == kFp8) {
+    float amax = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) amax = fmaxf(amax, fabsf(x[j]));
+    amax = fmaxf(amax, dpp_mov<0xb1>(amax));  // the lane pair holds the group
+    const float s = __fdiv_rn(amax > 1e-10f ? amax : 1e-10f, 448.0f);
+    const float inv = refined_rcp(s);
+    uint32_t w[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint32_t lo = cvt_e4m3x2<false>(x[4 * k] * inv, x[4 * k + 1] * inv, 0u);
+      w[k] = cvt_e4m3x2<true>(x[4 * k + 2] * inv, x[4 * k + 3] * inv, lo);
+    }
+    store_words<16>(codes + col0, w);
+    if ((cg & 1) == 0) reinterpret_cast<float*>(meta)[col0 >> 5] = s;
+  } else {
+    static_assert(KIND == kNvfp4, "table formats only");
+    float amax = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) amax = fmaxf(amax, fabsf(x[j]));
+    const float t = fminf(__fdiv_rn(amax, 6.0f * s_g), 448.0f);
+    const uint32_t sb = cvt_e4m3x2<false>(t, 0.0f, 0u) & 0xffu;
+    const float scale = e4m3_byte<0>(sb) * s_g;
+    uint32_t w[2] = {0u, 0u};
+    if (scale > 0.0f) {
+      const float inv = refined_rcp(scale);
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        uint32_t v = cvt_e2m1x2<0>(x[8 * k] * inv, x[8 * k + 1] * inv, 0u);
+        v = cvt_e2m1x2<1>(x[8 * k + 2] * inv, x[8 * k + 3] * inv, v);
+        v = cvt_e2m1x2<2>(x[8 * k + 4] * inv, x[8 * k + 5] * inv, v);
+        w[k] = cvt_e2m1x2<3>(x[8 * k + 6] * inv, x[8 * k + 7] * inv, v);
+      }
+    }
+    store_words<8>(codes + col0 / 2, w);
+    meta[cg] = static_cast<uint8_t>(sb);
+  }
+}
+
+// The inverse: one lane's 16 decoded values of a low row (before the inverse
+// transform of INT4 with had, which the caller applies with fwht32_pair).
+// For INT4 the values are s (c - z) scaled by `a` (the caller's decay and the
+// transform's normalization), as one FMA each.
+template <int KIND, int D>
+__device__ __forceinline__ void decode_slice_table(const uint8_t* codes, const uint8_t* meta,
+                                                   int cg, int col0, float s_g, float a,
+                                                   float* x) {
+  if constexpr (KIND == kInt4) {
+    uint32_t w[2];
+    load_words<8>(codes + col0 / 2, w);
+    const uint32_t m = reinterpret_cast<const uint32_t*>(meta)[col0 >> 5];
+    const float A = a * f16_lo(m);
+    const float B0 = -A * f16_hi(m);
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+      x[j] = fmaf(A, static_cast<float>((w[j >> 3] >> (4 * (j & 7))) & 0xfu), B0);
+  } else if constexpr (KIND == kFp8) {
+    uint32_t w[4];
+    load_words<16>(codes + col0, w);
+    const float s = reinterpret_cast<const float*>(meta)[col0 >> 5];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      x[4 * k + 0] = a * (s * e4m3_byte<0>(w[k]));
+      x[4 * k + 1] = a * (s * e4m3_byte<1>(w[k]));
+      x[4 * k + 2] = a * (s * e4m3_byte<2>(w[k]));
+      x[4 * k + 3] = a * (s * e4m3_byte<3>(w[k]));
+    }
+  } else {
+    static_assert(KIND == kNvfp4, "table formats only");
+    uint32_t w[2];
+    load_words<8>(codes + col0 / 2, w);
+    const float scale = e4m3_byte<0>(meta[cg]) * s_g;
+    float q[16];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      e2m1_byte<0>(w[k], q[8 * k + 0], q[8 * k + 1]);
+      e2m1_byte<1>(w[k], q[8 * k + 2], q[8 * k + 3]);
+      e2m1_byte<2>(w[k], q[8 * k + 4], q[8 * k + 5]);
+      e2m1_byte<3>(w[k], q[8 * k + 6], q[8 * k + 7]);
+    }
+#pragma unroll
+    for (int j = 0; j < 16; ++j) x[j] = a * (q[j] * scale);
+  }
+}
+
 // ------------------------------------------------------------- row encode
 
 // Stores one row slice of CPT values (columns col0..col0+CPT of tile row r)
@@ -245,8 +455,21 @@ __device__ __forceinline__ void group_qparams_f16(float mn, float mx, float& s16
 template <int KIND, int D, int CPT, int TPR>
 __device__ __forceinline__ void encode_row(const float* x, int r, int k_hi, int cg, int col0,
                                            uint8_t* tile, uint8_t* codes, uint8_t* meta_bytes,
-                                           bool had = false) {
-  if constexpr (KIND == kPaper) {
+                                           bool had = false, float s_g = 1.0f) {
+  if constexpr (KIND >= kInt4) {
+    static_assert(CPT == 16, "a lane holds 16 values of a row");
+    if (r < k_hi) {
+      uint32_t w[CPT / 2];
+#pragma unroll
+      for (int j = 0; j < CPT / 2; ++j) w[j] = pack_f16x2(x[2 * j], x[2 * j + 1]);
+      store_words<CPT * 2>(tile + (static_cast<size_t>(r) * D + col0) * 2, w);
+      return;
+    }
+    const size_t l = static_cast<size_t>(r - k_hi);
+    encode_slice_table<KIND, D>(x, cg, col0, had, s_g, codes + l * code_row_bytes<KIND, D>(),
+                                meta_bytes + l * meta_row_bytes<KIND, D>());
+    return;
+  } else if constexpr (KIND == kPaper) {
     static_assert(CPT == 16, "a lane pair holds one group of 32");
     if (r < k_hi) {
       uint32_t w[CPT / 2];
@@ -340,11 +563,22 @@ __device__ __forceinline__ void decode_row(const uint8_t* tile, const uint8_t* c
     load_words<CPT * 2>(tile + (static_cast<size_t>(r) * D + col0) * 2, w);
 #pragma unroll
     for (int j = 0; j < CPT / 2; ++j) {
-      x[2 * j] = KIND == kPaper ? f16_lo(w[j]) : bf16_lo(w[j]);
-      x[2 * j + 1] = KIND == kPaper ? f16_hi(w[j]) : bf16_hi(w[j]);
+      x[2 * j] = KIND >= kPaper ? f16_lo(w[j]) : bf16_lo(w[j]);
+      x[2 * j + 1] = KIND >= kPaper ? f16_hi(w[j]) : bf16_hi(w[j]);
     }
     return;
   }
+  if constexpr (KIND >= kInt4) {
+    const size_t lr = static_cast<size_t>(r - k_hi);
+    const float s_g = KIND == kNvfp4 ? load_global_scale<D>(meta_bytes, k_hi) : 1.0f;
+    decode_slice_table<KIND, D>(codes + lr * code_row_bytes<KIND, D>(),
+                                meta_bytes + lr * meta_row_bytes<KIND, D>(), cg, col0, s_g,
+                                (KIND == kInt4 && had) ? kInvSqrt32 : 1.0f, x);
+    if constexpr (KIND == kInt4) {
+      if (had) fwht32_pair(reinterpret_cast<float(&)[16]>(*x), (cg & 1) != 0);
+    }
+    return;
+  } else {
   const int l = r - k_hi;
   uint32_t w[CPT / 4];
   load_words<CPT>(codes + static_cast<size_t>(l) * D + col0, w);
@@ -372,6 +606,7 @@ __device__ __forceinline__ void decode_row(const uint8_t* tile, const uint8_t* c
   }
   if constexpr (KIND == kPaper && CPT == 16) {
     if (had) fwht32_pair(reinterpret_cast<float(&)[16]>(*x), (cg & 1) != 0);
+  }
   }
 }
 

@@ -15,7 +15,8 @@ struct TileGeom {
   int32_t dk, dv, k_hi, kind;
   size_t hi_bytes;    // k_hi * dv * 2 (mixed) or dk * dv * 4 (fp32)
   size_t code_bytes;  // (dk - k_hi) * dv
-  size_t meta_bytes;  // (dk - k_hi) * 8
+  size_t meta_bytes;  // (dk - k_hi) * metadata bytes per row
+  size_t tail_bytes;  // 4 (the E2M1 global scale) or 0
   size_t bytes;       // sum of the regions
   size_t stride;      // bytes rounded up to 128
 };
@@ -24,8 +25,23 @@ struct TileGeom {
 // not one the layout math accepts.
 bool tile_geom(const damp_layout* layout, TileGeom* g);
 
+// Kernel codec of a layout (the KIND template argument of the kernels):
+// the FP32 state, the default tiers, the paper's INT8 tiers, or the other
+// rows of App. A.1's format table; kCodecNone if no kernel encodes it.
+enum Codec {
+  kCodecFp32 = 0,
+  kCodecDefault = 1,
+  kCodecPaper = 2,
+  kCodecInt4 = 3,
+  kCodecFp8 = 4,
+  kCodecNvfp4 = 5,
+  kCodecNone = -1
+};
+int layout_codec(const damp_layout* layout);
+
 // True for the paper's tiers (App. A.1, Eq. (17)): FP16 high tier, groups
-// of 32 with FP16 (s, z), with or without the block-32 Hadamard transform.
+// of 32 with FP16 (s, z), UINT8 codes, with or without the block-32
+// Hadamard transform.
 bool layout_is_paper(const damp_layout* layout);
 
 // True for the default tiers: BF16 high tier, one fp32 (s, z) pair per row,
@@ -34,7 +50,7 @@ bool layout_is_default(const damp_layout* layout);
 
 // True if the layout has kernels: d_k == d_v in {16, 32, 64, 128} with the
 // FP32 state or the default tiers, or d_k == d_v in {32, 64, 128} with the
-// paper's tiers.
+// paper's tiers or another format of App. A.1's table.
 bool layout_has_kernels(const damp_layout* layout);
 
 // Validates a pool descriptor (non-null, consistent strides and counts).

@@ -18,6 +18,7 @@ int dtype_bits(int32_t dt) {
     case DAMP_DT_FP32: return 32;
     case DAMP_DT_BF16: return 16;
     case DAMP_DT_FP16: return 16;
+    case DAMP_DT_E4M3: return 8;
     default: return -1;
   }
 }
@@ -56,6 +57,7 @@ bool tile_geom(const damp_layout* L, TileGeom* g) {
   g->dv = L->d_v;
   g->kind = L->kind;
   const size_t dk = static_cast<size_t>(L->d_k), dv = static_cast<size_t>(L->d_v);
+  g->tail_bytes = 0;
   if (L->kind == DAMP_STATE_FP32) {
     g->k_hi = 0;
     g->hi_bytes = dk * dv * 4;
@@ -66,7 +68,7 @@ bool tile_geom(const damp_layout* L, TileGeom* g) {
       return false;
     }
     const int hb = dtype_bits(L->hi_dtype), mb = dtype_bits(L->meta_dtype);
-    if (hb < 0 || mb < 0) {
+    if (hb < 0 || hb == 8 || mb < 0) {
       fail(DAMP_ERR_INVALID_ARG, "unknown high-tier or metadata dtype");
       return false;
     }
@@ -74,34 +76,72 @@ bool tile_geom(const damp_layout* L, TileGeom* g) {
       fail(DAMP_ERR_INVALID_ARG, "group = %d does not divide d_v = %d", L->group, L->d_v);
       return false;
     }
+    // metadata per group: (s, z) for the integer codes, one fp32 scale for
+    // E4M3, one E4M3 block scale for E2M1 (plus the tile's fp32 global scale)
+    const int cd = L->code_dtype;
+    const bool ok = (cd == DAMP_DT_U8 && (mb == 32 || mb == 16)) ||
+                    (cd == DAMP_DT_U4 && L->meta_dtype == DAMP_DT_FP16) ||
+                    (cd == DAMP_DT_E4M3 && L->meta_dtype == DAMP_DT_FP32) ||
+                    (cd == DAMP_DT_E2M1 && L->meta_dtype == DAMP_DT_E4M3);
+    if (!ok) {
+      fail(DAMP_ERR_INVALID_ARG, "code dtype %d with metadata dtype %d is not a format", cd,
+           L->meta_dtype);
+      return false;
+    }
+    const bool nibble = cd == DAMP_DT_U4 || cd == DAMP_DT_E2M1;
+    if (nibble && L->d_v % 2 != 0) {
+      fail(DAMP_ERR_INVALID_ARG, "4-bit codes need an even d_v");
+      return false;
+    }
     const size_t lo_rows = dk - static_cast<size_t>(L->k_hi);
+    const size_t groups = dv / static_cast<size_t>(L->group);
     g->k_hi = L->k_hi;
     g->hi_bytes = static_cast<size_t>(L->k_hi) * dv * static_cast<size_t>(hb / 8);
-    g->code_bytes = lo_rows * dv;
-    g->meta_bytes = lo_rows * (dv / static_cast<size_t>(L->group)) * 2 *
-                    static_cast<size_t>(mb / 8);
+    g->code_bytes = lo_rows * (nibble ? dv / 2 : dv);
+    const size_t words = (cd == DAMP_DT_U8 || cd == DAMP_DT_U4) ? 2 : 1;
+    g->meta_bytes = lo_rows * groups * words * static_cast<size_t>(mb / 8);
+    g->tail_bytes = cd == DAMP_DT_E2M1 ? 4 : 0;
   }
-  g->bytes = g->hi_bytes + g->code_bytes + g->meta_bytes;
+  g->bytes = g->hi_bytes + g->code_bytes + g->meta_bytes + g->tail_bytes;
   g->stride = (g->bytes + 127) / 128 * 128;
   return true;
 }
 
 bool layout_is_paper(const damp_layout* L) {
-  return L->kind == DAMP_STATE_MIXED && L->hi_dtype == DAMP_DT_FP16 &&
-         L->meta_dtype == DAMP_DT_FP16 && L->group == 32 && (L->hadamard == 0 || L->hadamard == 1);
+  return layout_codec(L) == kCodecPaper;
 }
 
 bool layout_is_default(const damp_layout* L) {
   return L->kind == DAMP_STATE_MIXED && L->hi_dtype == DAMP_DT_BF16 &&
-         L->meta_dtype == DAMP_DT_FP32 && L->group == L->d_v && L->hadamard == 0;
+         L->meta_dtype == DAMP_DT_FP32 && L->group == L->d_v && L->hadamard == 0 &&
+         L->code_dtype == DAMP_DT_U8;
+}
+
+int layout_codec(const damp_layout* L) {
+  if (L->kind == DAMP_STATE_FP32) return kCodecFp32;
+  if (L->kind != DAMP_STATE_MIXED) return kCodecNone;
+  if (layout_is_default(L)) return kCodecDefault;
+  if (L->hi_dtype != DAMP_DT_FP16) return kCodecNone;
+  const bool had01 = L->hadamard == 0 || L->hadamard == 1;
+  if (L->code_dtype == DAMP_DT_U8 && L->meta_dtype == DAMP_DT_FP16 && L->group == 32 && had01)
+    return kCodecPaper;
+  if (L->code_dtype == DAMP_DT_U4 && L->meta_dtype == DAMP_DT_FP16 && L->group == 32 && had01)
+    return kCodecInt4;
+  if (L->code_dtype == DAMP_DT_E4M3 && L->meta_dtype == DAMP_DT_FP32 && L->group == 32 &&
+      L->hadamard == 0)
+    return kCodecFp8;
+  if (L->code_dtype == DAMP_DT_E2M1 && L->meta_dtype == DAMP_DT_E4M3 && L->group == 16 &&
+      L->hadamard == 0)
+    return kCodecNvfp4;
+  return kCodecNone;
 }
 
 bool layout_has_kernels(const damp_layout* L) {
   if (L->d_k != L->d_v) return false;
   if (L->d_k != 16 && L->d_k != 32 && L->d_k != 64 && L->d_k != 128) return false;
-  if (L->kind == DAMP_STATE_FP32) return true;
-  if (layout_is_paper(L)) return L->d_k >= 32;
-  return layout_is_default(L);
+  const int c = layout_codec(L);
+  if (c == kCodecFp32 || c == kCodecDefault) return true;
+  return c != kCodecNone && L->d_k >= 32;
 }
 
 damp_status check_pool(const damp_pool* pool) {
@@ -144,6 +184,7 @@ damp_status damp_layout_init(damp_layout* out, int32_t d_k, int32_t d_v, int32_t
   L.group = d_v;
   L.meta_dtype = DAMP_DT_FP32;
   L.hadamard = 0;
+  L.code_dtype = DAMP_DT_U8;
   TileGeom g;
   if (!tile_geom(&L, &g)) return DAMP_ERR_INVALID_ARG;
   *out = L;
@@ -165,9 +206,13 @@ double damp_bits_per_value(const damp_layout* layout) {
   if (!tile_geom(layout, &g)) return -1.0;
   if (layout->kind == DAMP_STATE_FP32) return 32.0;
   // Eq. (7): b = b_lo + (k_hi / d_k) (b_hi - b_lo), with b_lo = code bits plus
-  // two metadata words per group.
-  const double meta_bits = layout->meta_dtype == DAMP_DT_FP32 ? 32.0 : 16.0;
-  const double b_lo = 8.0 + 2.0 * meta_bits / static_cast<double>(layout->group);
+  // the metadata words of a group (the per-tile global scale of E2M1 is left
+  // out, as App. A.1 does).
+  const int cd = layout->code_dtype;
+  const double meta_bits = static_cast<double>(dtype_bits(layout->meta_dtype));
+  const double words = (cd == DAMP_DT_U8 || cd == DAMP_DT_U4) ? 2.0 : 1.0;
+  const double code_bits = (cd == DAMP_DT_U4 || cd == DAMP_DT_E2M1) ? 4.0 : 8.0;
+  const double b_lo = code_bits + words * meta_bits / static_cast<double>(layout->group);
   const double b_hi = layout->hi_dtype == DAMP_DT_FP32 ? 32.0 : 16.0;
   return b_lo + (static_cast<double>(layout->k_hi) / layout->d_k) * (b_hi - b_lo);
 }

@@ -41,8 +41,20 @@ __global__ __launch_bounds__(Shape<D>::NT) void pack_kernel(const TileParams p) 
                   static_cast<size_t>(h) * p.tile_stride;
   const int k_hi = KIND == kFp32 ? D : p.k_hi;
   uint8_t* codes = tile + static_cast<size_t>(k_hi) * D * 2;
-  uint8_t* meta = codes + static_cast<size_t>(D - k_hi) * D;
+  uint8_t* meta = codes + static_cast<size_t>(D - k_hi) * code_row_bytes<KIND, D>();
   const float* src = p.S + (static_cast<size_t>(b) * p.HV + h) * D * D;
+  float s_g = 1.0f;
+  if constexpr (KIND == kNvfp4) {  // the global scale of the tile's low tier
+    float amax = 0.0f;
+    for (int i = 0; i < Sh::RPT; ++i) {
+      const int r = rg + Sh::RG * i;
+      if (r < k_hi) continue;
+      const int u = p.perm ? (static_cast<int>(p.perm[static_cast<size_t>(h) * D + r]) & (D - 1)) : r;
+      for (int j = 0; j < Sh::CPT; ++j) amax = fmaxf(amax, fabsf(src[static_cast<size_t>(u) * D + col0 + j]));
+    }
+    s_g = nvfp4_global(block_max<Sh::NT>(amax));
+    if (t == 0) store_global_scale<D>(meta, k_hi, s_g);
+  }
 #pragma unroll
   for (int i = 0; i < Sh::RPT; ++i) {
     const int r = rg + Sh::RG * i;
@@ -52,7 +64,8 @@ __global__ __launch_bounds__(Shape<D>::NT) void pack_kernel(const TileParams p) 
     load_words<Sh::CPT * 4>(reinterpret_cast<const uint8_t*>(src + static_cast<size_t>(u) * D + col0), w);
 #pragma unroll
     for (int j = 0; j < Sh::CPT; ++j) x[j] = __uint_as_float(w[j]);
-    encode_row<KIND, D, Sh::CPT, Sh::TPR>(x, r, k_hi, cg, col0, tile, codes, meta, p.had != 0);
+    encode_row<KIND, D, Sh::CPT, Sh::TPR>(x, r, k_hi, cg, col0, tile, codes, meta, p.had != 0,
+                                          s_g);
   }
 }
 
@@ -68,14 +81,44 @@ __global__ __launch_bounds__(Shape<D>::NT) void unpack_kernel(const TileParams p
                         static_cast<size_t>(h) * p.tile_stride;
   const int k_hi = KIND == kFp32 ? D : p.k_hi;
   const uint8_t* codes = tile + static_cast<size_t>(k_hi) * D * 2;
-  const float2* meta = reinterpret_cast<const float2*>(codes + static_cast<size_t>(D - k_hi) * D);
-  const uint32_t* meta16 = reinterpret_cast<const uint32_t*>(codes + static_cast<size_t>(D - k_hi) * D);
+  const uint8_t* meta_bytes = codes + static_cast<size_t>(D - k_hi) * code_row_bytes<KIND, D>();
+  const float2* meta = reinterpret_cast<const float2*>(meta_bytes);
+  const uint32_t* meta16 = reinterpret_cast<const uint32_t*>(meta_bytes);
 #pragma unroll
   for (int i = 0; i < Sh::RPT; ++i) {
     const int r = rg + Sh::RG * i;
     const int u = p.perm ? (static_cast<int>(p.perm[static_cast<size_t>(h) * D + r]) & (D - 1)) : r;
     uint32_t out[Sh::CPT];
-    if constexpr (KIND == kPaper) {
+    if constexpr (KIND >= kInt4) {
+      // FP16 rows; low rows as Eq. (16) or NVFP4 reconstruct (one product),
+      // INT4 as s * (c - z) then the inverse transform
+      float y[Sh::CPT];
+      if (!live) {
+#pragma unroll
+        for (int j = 0; j < Sh::CPT; ++j) y[j] = 0.0f;
+      } else if (r < k_hi) {
+        decode_row<KIND, D, Sh::CPT>(tile, codes, meta_bytes, r, k_hi, cg, col0, false, y);
+      } else if constexpr (KIND == kInt4) {
+        const size_t l = static_cast<size_t>(r - k_hi);
+        uint32_t w[2];
+        load_words<8>(codes + l * code_row_bytes<KIND, D>() + col0 / 2, w);
+        const uint32_t m = reinterpret_cast<const uint32_t*>(
+            meta_bytes + l * meta_row_bytes<KIND, D>())[col0 >> 5];
+        const float s16 = f16_lo(m), z16 = f16_hi(m);
+#pragma unroll
+        for (int j = 0; j < Sh::CPT; ++j)
+          y[j] = __fmul_rn(s16, __fsub_rn(static_cast<float>((w[j >> 3] >> (4 * (j & 7))) & 0xfu), z16));
+        if (p.had) {
+          fwht32_pair(y, (cg & 1) != 0);
+#pragma unroll
+          for (int j = 0; j < Sh::CPT; ++j) y[j] *= kInvSqrt32;
+        }
+      } else {
+        decode_row<KIND, D, Sh::CPT>(tile, codes, meta_bytes, r, k_hi, cg, col0, false, y);
+      }
+#pragma unroll
+      for (int j = 0; j < Sh::CPT; ++j) out[j] = __float_as_uint(y[j]);
+    } else if constexpr (KIND == kPaper) {
       // FP16 rows; low rows: s * (c - z) per group of 32, then the inverse
       // transform (the lane pair holds the group)
       float y[Sh::CPT];
@@ -149,7 +192,10 @@ __global__ __launch_bounds__(Shape<D>::NT) void reset_kernel(const TileParams p)
                   static_cast<size_t>(slot) * p.slot_stride + static_cast<size_t>(h) * p.tile_stride;
   const int k_hi = KIND == kFp32 ? D : p.k_hi;
   uint8_t* codes = tile + static_cast<size_t>(k_hi) * D * 2;
-  uint8_t* meta = codes + static_cast<size_t>(D - k_hi) * D;
+  uint8_t* meta = codes + static_cast<size_t>(D - k_hi) * code_row_bytes<KIND, D>();
+  if constexpr (KIND == kNvfp4) {
+    if (t == 0) store_global_scale<D>(meta, k_hi, nvfp4_global(0.0f));
+  }
   float x[Sh::CPT];
 #pragma unroll
   for (int j = 0; j < Sh::CPT; ++j) x[j] = 0.0f;
@@ -175,7 +221,7 @@ template <int KIND>
 void launch_d(Op op, int D, const TileParams& p, dim3 grid, hipStream_t s) {
   switch (D) {
     case 16:
-      if constexpr (KIND != kPaper) launch<KIND, 16>(op, p, grid, s);  // groups need d_v >= 32
+      if constexpr (KIND < kPaper) launch<KIND, 16>(op, p, grid, s);  // groups need d_v >= 32
       break;
     case 32: launch<KIND, 32>(op, p, grid, s); break;
     case 64: launch<KIND, 64>(op, p, grid, s); break;
@@ -212,12 +258,16 @@ damp_status run(Op op, const char* name, const damp_pool* pool, int32_t layer,
   p.k_hi = pool->layout.kind == DAMP_STATE_FP32 ? 0 : pool->layout.k_hi;
   p.had = pool->layout.hadamard;
   const dim3 grid(pool->num_v_heads, B, all_layers ? pool->num_layers : 1);
-  if (pool->layout.kind == DAMP_STATE_FP32)
-    launch_d<kFp32>(op, pool->layout.d_k, p, grid, as_stream(stream));
-  else if (layout_is_paper(&pool->layout))
-    launch_d<kPaper>(op, pool->layout.d_k, p, grid, as_stream(stream));
-  else
-    launch_d<kMixed>(op, pool->layout.d_k, p, grid, as_stream(stream));
+  const int D = pool->layout.d_k;
+  hipStream_t s = as_stream(stream);
+  switch (layout_codec(&pool->layout)) {
+    case kCodecFp32: launch_d<kFp32>(op, D, p, grid, s); break;
+    case kCodecPaper: launch_d<kPaper>(op, D, p, grid, s); break;
+    case kCodecInt4: launch_d<kInt4>(op, D, p, grid, s); break;
+    case kCodecFp8: launch_d<kFp8>(op, D, p, grid, s); break;
+    case kCodecNvfp4: launch_d<kNvfp4>(op, D, p, grid, s); break;
+    default: launch_d<kMixed>(op, D, p, grid, s); break;
+  }
   return check_launch(name);
 }
 

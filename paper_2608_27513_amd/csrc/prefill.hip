@@ -90,7 +90,7 @@ __global__ __launch_bounds__(NT) void prefill_kernel(const PrefillParams p) {
                   static_cast<size_t>(h) * p.tile_stride;
   const int k_hi = KIND == kFp32 ? D : p.k_hi;
   uint8_t* codes = tile + static_cast<size_t>(k_hi) * D * 2;
-  uint8_t* meta_bytes = codes + static_cast<size_t>(D - k_hi) * D;
+  uint8_t* meta_bytes = codes + static_cast<size_t>(D - k_hi) * code_row_bytes<KIND, D>();
   const bool had = p.had != 0;
 
   // ---- decode the stored state once
@@ -195,9 +195,21 @@ __global__ __launch_bounds__(NT) void prefill_kernel(const PrefillParams p) {
   }
 
   // ---- store the chunk-final state per its tier
+  float s_g = 1.0f;
+  if constexpr (KIND == kNvfp4) {  // the global scale of the final low tier
+    float amax = 0.0f;
+#pragma unroll
+    for (int i = 0; i < RPT; ++i)
+      if (rg + RG * i >= k_hi)
+#pragma unroll
+        for (int j = 0; j < CPT; ++j) amax = fmaxf(amax, fabsf(x[i][j]));
+    s_g = nvfp4_global(block_max<NT>(amax));
+    if (t == 0) store_global_scale<D>(meta_bytes, k_hi, s_g);
+  }
 #pragma unroll
   for (int i = 0; i < RPT; ++i)
-    encode_row<KIND, D, CPT, TPR>(x[i], rg + RG * i, k_hi, cg, col0, tile, codes, meta_bytes, had);
+    encode_row<KIND, D, CPT, TPR>(x[i], rg + RG * i, k_hi, cg, col0, tile, codes, meta_bytes, had,
+                                  s_g);
 }
 
 template <int KIND, bool KDA, int D>
@@ -212,7 +224,7 @@ template <int KIND, bool KDA>
 void launch_d(int D, const PrefillParams& p, int B, hipStream_t stream) {
   switch (D) {
     case 16:
-      if constexpr (KIND != kPaper) launch<KIND, KDA, 16>(p, B, stream);  // groups need d_v >= 32
+      if constexpr (KIND < kPaper) launch<KIND, KDA, 16>(p, B, stream);  // groups need d_v >= 32
       break;
     case 32: launch<KIND, KDA, 32>(p, B, stream); break;
     case 64: launch<KIND, KDA, 64>(p, B, stream); break;
@@ -222,9 +234,14 @@ void launch_d(int D, const PrefillParams& p, int B, hipStream_t stream) {
 
 template <bool KDA>
 void launch_kind(const damp_pool* pool, int D, const PrefillParams& p, int B, hipStream_t s) {
-  if (pool->layout.kind == DAMP_STATE_FP32) launch_d<kFp32, KDA>(D, p, B, s);
-  else if (layout_is_paper(&pool->layout)) launch_d<kPaper, KDA>(D, p, B, s);
-  else launch_d<kMixed, KDA>(D, p, B, s);
+  switch (layout_codec(&pool->layout)) {
+    case kCodecFp32: launch_d<kFp32, KDA>(D, p, B, s); break;
+    case kCodecPaper: launch_d<kPaper, KDA>(D, p, B, s); break;
+    case kCodecInt4: launch_d<kInt4, KDA>(D, p, B, s); break;
+    case kCodecFp8: launch_d<kFp8, KDA>(D, p, B, s); break;
+    case kCodecNvfp4: launch_d<kNvfp4, KDA>(D, p, B, s); break;
+    default: launch_d<kMixed, KDA>(D, p, B, s); break;
+  }
 }
 
 }  // namespace

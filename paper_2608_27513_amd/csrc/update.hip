@@ -62,7 +62,7 @@ __global__ __launch_bounds__(NT) void update_kernel(const UpdateParams p) {
                   static_cast<size_t>(h) * p.tile_stride;
   const int k_hi = KIND == kFp32 ? D : p.k_hi;
   uint8_t* codes = tile + static_cast<size_t>(k_hi) * D * 2;
-  uint8_t* meta_bytes = codes + static_cast<size_t>(D - k_hi) * D;
+  uint8_t* meta_bytes = codes + static_cast<size_t>(D - k_hi) * code_row_bytes<KIND, D>();
   const float2* meta = reinterpret_cast<const float2*>(meta_bytes);
   // paper tiers: one word (FP16 s, FP16 z) per row and group of 32
   const uint32_t* meta16 = reinterpret_cast<const uint32_t*>(meta_bytes);
@@ -73,7 +73,9 @@ __global__ __launch_bounds__(NT) void update_kernel(const UpdateParams p) {
 #pragma unroll
   for (int i = 0; i < RPT; ++i) {
     const int r = rg + RG * i;
-    if (r < k_hi) {
+    if constexpr (KIND >= kInt4) {
+      // the table formats decode through decode_row below
+    } else if (r < k_hi) {
       load_words<CPT * EB>(tile + (static_cast<size_t>(r) * D + col0) * EB, raw[i]);
       sz[i] = make_float2(0.0f, 0.0f);
     } else {
@@ -113,7 +115,11 @@ __global__ __launch_bounds__(NT) void update_kernel(const UpdateParams p) {
 #pragma unroll
   for (int i = 0; i < RPT; ++i) {
     const int r = rg + RG * i;
-    if (r < k_hi) {
+    if constexpr (KIND >= kInt4) {
+      decode_row<KIND, D, CPT>(tile, codes, meta_bytes, r, k_hi, cg, col0, p.had != 0, x[i]);
+#pragma unroll
+      for (int j = 0; j < CPT; ++j) x[i][j] *= aa[i];
+    } else if (r < k_hi) {
       if (KIND == kFp32) {
 #pragma unroll
         for (int j = 0; j < CPT; ++j) x[i][j] = aa[i] * __uint_as_float(raw[i][j]);
@@ -200,12 +206,25 @@ __global__ __launch_bounds__(NT) void update_kernel(const UpdateParams p) {
   }
 #pragma unroll
   for (int i = 0; i < RPT; ++i) {
-    const int r = rg + RG * i;
     const float bk = beta * kk[i];
 #pragma unroll
     for (int j = 0; j < CPT; ++j) x[i][j] = fmaf(bk, dl[j], x[i][j]);
-    encode_row<KIND, D, CPT, TPR>(x[i], r, k_hi, cg, col0, tile, codes, meta_bytes, p.had != 0);
   }
+  float s_g = 1.0f;
+  if constexpr (KIND == kNvfp4) {  // the global scale of the updated low tier
+    float amax = 0.0f;
+#pragma unroll
+    for (int i = 0; i < RPT; ++i)
+      if (rg + RG * i >= k_hi)
+#pragma unroll
+        for (int j = 0; j < CPT; ++j) amax = fmaxf(amax, fabsf(x[i][j]));
+    s_g = nvfp4_global(block_max<NT>(amax));
+    if (t == 0) store_global_scale<D>(meta_bytes, k_hi, s_g);
+  }
+#pragma unroll
+  for (int i = 0; i < RPT; ++i)
+    encode_row<KIND, D, CPT, TPR>(x[i], rg + RG * i, k_hi, cg, col0, tile, codes, meta_bytes,
+                                  p.had != 0, s_g);
 }
 
 template <int KIND, bool KDA, int D>
@@ -220,11 +239,23 @@ template <int KIND, bool KDA>
 void launch_d(int D, const UpdateParams& p, int B, hipStream_t stream) {
   switch (D) {
     case 16:
-      if constexpr (KIND != kPaper) launch<KIND, KDA, 16>(p, B, stream);  // groups need d_v >= 32
+      if constexpr (KIND < kPaper) launch<KIND, KDA, 16>(p, B, stream);  // groups need d_v >= 32
       break;
     case 32: launch<KIND, KDA, 32>(p, B, stream); break;
     case 64: launch<KIND, KDA, 64>(p, B, stream); break;
     default: launch<KIND, KDA, 128>(p, B, stream); break;
+  }
+}
+
+template <bool KDA>
+void launch_codec(int codec, int D, const UpdateParams& p, int B, hipStream_t s) {
+  switch (codec) {
+    case kCodecFp32: launch_d<kFp32, KDA>(D, p, B, s); break;
+    case kCodecPaper: launch_d<kPaper, KDA>(D, p, B, s); break;
+    case kCodecInt4: launch_d<kInt4, KDA>(D, p, B, s); break;
+    case kCodecFp8: launch_d<kFp8, KDA>(D, p, B, s); break;
+    case kCodecNvfp4: launch_d<kNvfp4, KDA>(D, p, B, s); break;
+    default: launch_d<kMixed, KDA>(D, p, B, s); break;
   }
 }
 
@@ -279,16 +310,8 @@ damp_status update(bool kda, const damp_pool* pool, int32_t layer, const int32_t
       return fail(DAMP_ERR_HIP, "%s: occupancy query failed", name);
     return check_launch(name);
   }
-  if (pool->layout.kind == DAMP_STATE_FP32) {
-    if (kda) launch_d<kFp32, true>(D, p, B, s);
-    else launch_d<kFp32, false>(D, p, B, s);
-  } else if (layout_is_paper(&pool->layout)) {
-    if (kda) launch_d<kPaper, true>(D, p, B, s);
-    else launch_d<kPaper, false>(D, p, B, s);
-  } else {
-    if (kda) launch_d<kMixed, true>(D, p, B, s);
-    else launch_d<kMixed, false>(D, p, B, s);
-  }
+  if (kda) launch_codec<true>(layout_codec(&pool->layout), D, p, B, s);
+  else launch_codec<false>(layout_codec(&pool->layout), D, p, B, s);
   return check_launch(name);
 }
 

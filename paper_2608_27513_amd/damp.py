@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(HERE, "libdamp.so")
 
 DAMP_OK, DAMP_ERR_INVALID_ARG, DAMP_ERR_UNSUPPORTED, DAMP_ERR_HIP = 0, 1, 2, 3
 DAMP_DT_FP32, DAMP_DT_BF16, DAMP_DT_FP16 = 0, 1, 2
+DAMP_DT_U8, DAMP_DT_U4, DAMP_DT_E4M3, DAMP_DT_E2M1 = 3, 4, 5, 6
 DAMP_STATE_FP32, DAMP_STATE_MIXED = 0, 1
 DAMP_SEL_DAMP, DAMP_SEL_ERROR, DAMP_SEL_PERSISTENCE, DAMP_SEL_STATE_ENERGY, DAMP_SEL_RANDOM = \
     0, 1, 2, 3, 4
@@ -32,7 +33,8 @@ class DampError(RuntimeError):
 
 class damp_layout(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in
-                ("d_k", "d_v", "k_hi", "kind", "hi_dtype", "group", "meta_dtype", "hadamard")]
+                ("d_k", "d_v", "k_hi", "kind", "hi_dtype", "group", "meta_dtype", "hadamard",
+                 "code_dtype")]
 
 
 class damp_calib(ctypes.Structure):
@@ -44,7 +46,7 @@ class damp_calib(ctypes.Structure):
 class damp_pool(ctypes.Structure):
     _fields_ = [("layout", damp_layout), ("num_layers", ctypes.c_int32),
                 ("num_slots", ctypes.c_int32), ("num_v_heads", ctypes.c_int32),
-                ("reserved", ctypes.c_int32), ("base", ctypes.c_void_p),
+                ("base", ctypes.c_void_p),
                 ("tile_stride", ctypes.c_size_t), ("bytes", ctypes.c_size_t)]
 
 

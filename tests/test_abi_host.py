@@ -62,6 +62,33 @@ def test_tile_geometry_matches_oracle(L, d):
                                                               orc.FMT_PAPER)
 
 
+@pytest.mark.parametrize("fmt,bits", [(orc.FMT_INT4, 5.0), (orc.FMT_INT4_H32, 5.0),
+                                      (orc.FMT_FP8, 9.0), (orc.FMT_NVFP4, 4.5)])
+def test_table_format_geometry(L, fmt, bits):
+    """The other rows of App. A.1's format table: tile bytes equal the
+    oracle's and the low tier costs the table's bits per value."""
+    for d in (32, 64, 128):
+        for k_hi in sorted({0, 8, d // 4, d}):
+            lay = D.damp_layout_init(d, d, k_hi, D.DAMP_STATE_MIXED)
+            lay.hi_dtype, lay.group, lay.meta_dtype, lay.hadamard, lay.code_dtype = fmt
+            assert D.damp_tile_bytes(lay) == orc.tile_bytes(D.DAMP_STATE_MIXED, d, d, k_hi, fmt)
+            assert D.damp_tile_stride(lay) == orc.tile_stride(D.DAMP_STATE_MIXED, d, d, k_hi, fmt)
+            if k_hi == 0:
+                assert D.damp_bits_per_value(lay) == bits
+    lay = D.damp_layout_init(16, 16, 4, D.DAMP_STATE_MIXED)
+    lay.hi_dtype, lay.group, lay.meta_dtype, lay.hadamard, lay.code_dtype = fmt
+    if fmt[1] > 16:  # a group wider than d_v: not a layout
+        assert L.damp_tile_bytes(ctypes.byref(lay)) == 0
+    else:            # a layout, but the kernels need d_v >= 32
+        pool = _fake_pool(L, lay)
+        p = ctypes.c_void_p(0x7f0000100000)
+        assert L.damp_state_pack(ctypes.byref(pool), 0, p, 4, p, None, None) == \
+            D.DAMP_ERR_UNSUPPORTED
+    bad = D.damp_layout_init(64, 64, 8, D.DAMP_STATE_MIXED)
+    bad.code_dtype = D.DAMP_DT_E2M1  # E2M1 codes with fp32 (s, z) pairs: not a format
+    assert L.damp_tile_bytes(ctypes.byref(bad)) == 0
+
+
 def test_bits_per_value_of_the_paper_layout(L):
     gold = json.load(open(GOLDEN))["damp_bits_per_value"]
     lay = D.damp_layout_init(128, 128, 16, D.DAMP_STATE_MIXED)
