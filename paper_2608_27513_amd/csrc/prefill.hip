@@ -592,11 +592,17 @@ template <int KIND, bool KDA, int D>
 void launch(const PrefillParams& p, int B, hipStream_t stream) {
   // the column kernel addresses one request's inputs with 32-bit offsets
   const int64_t span = static_cast<int64_t>(p.t_pitch) * (p.HK > p.HV ? p.HK : p.HV) * D * 2;
-  if (D == 128 && !KDA) {
+  if constexpr (D == 128 && !KDA) {
+    (void)span;
     hipLaunchKernelGGL((prefill_gdn_sgpr128<KIND>), dim3(p.HV, B), dim3(128), 0, stream, p);
-  } else if (D == 128 && span <= INT32_MAX) {
-    hipLaunchKernelGGL((prefill_col128<KIND, KDA>), dim3(p.HV, B), dim3(256), 0, stream, p);
-  } else {
+    return;
+  } else if constexpr (D == 128) {
+    if (span <= INT32_MAX) {
+      hipLaunchKernelGGL((prefill_col128<KIND, KDA>), dim3(p.HV, B), dim3(256), 0, stream, p);
+      return;
+    }
+  }
+  {
     constexpr int NT = D >= 32 ? 2 * D : 64;
     constexpr int CPT = D >= 32 ? 16 : 4;
     hipLaunchKernelGGL((prefill_kernel<KIND, KDA, D, NT, CPT>), dim3(p.HV, B), dim3(NT), 0,
