@@ -305,8 +305,9 @@ damp_status update(bool kda, const damp_pool* pool, int32_t layer, const int32_t
   hipStream_t s = as_stream(stream);
   // the persistent kernel numbers the B * HV tiles with 32-bit integers
   const bool tiles_fit = static_cast<int64_t>(B) * p.HV <= INT32_MAX;
-  if (layout_is_default(&pool->layout) && D == 128 && p.k_hi <= 32 && tiles_fit) {
-    if (!launch_stream128(kda, p, B, s))
+  const bool paper = layout_is_paper(&pool->layout);
+  if ((layout_is_default(&pool->layout) || paper) && D == 128 && p.k_hi <= 32 && tiles_fit) {
+    if (!launch_stream128(kda, paper, p, B, s))
       return fail(DAMP_ERR_HIP, "%s: occupancy query failed", name);
     return check_launch(name);
   }

@@ -30,6 +30,6 @@ struct UpdateParams {
 
 // The streaming kernel for d = 128 mixed tiles with k_hi <= 32 (update_stream.hip).
 // Returns false if it did not launch (a HIP query failed).
-bool launch_stream128(bool kda, const UpdateParams& p, int B, hipStream_t stream);
+bool launch_stream128(bool kda, bool paper, const UpdateParams& p, int B, hipStream_t stream);
 
 }  // namespace damp

@@ -21,6 +21,8 @@
 // can be in the high (bf16) tier, the others are low (uint8) rows.
 // Operands are staged once per tile by threads t < 128 (one tile row each):
 // k~, q~, the row decay a~ and v, in LDS; q~ . k~ is reduced there too.
+#include <type_traits>
+
 #include "device.hpp"
 #include "internal.hpp"
 #include "update.hpp"
@@ -83,12 +85,14 @@ __device__ __forceinline__ float fold8(float a, float b, bool upper) {
 }
 
 // Packed bytes of one tile as loaded by one thread: its four row slices
-// (16 bytes each), the second half of a bf16 row slot 0, and the (s, z) pair
-// of one row of its wave.
-struct RawSet {
+// (16 bytes each), the second half of a 16-bit row slot 0, and the metadata
+// of one row of its wave: the (s, z) pair of the default tiers (8 bytes) or
+// the four FP16 (s, z) words of the paper's groups (16 bytes).
+template <int FMT>
+struct RawSetT {
   u32x4 ra[4];
   u32x4 rb0 = u32x4{0u, 0u, 0u, 0u};
-  u32x2 rm;
+  typename std::conditional<FMT == kPaper, u32x4, u32x2>::type rm;
 };
 
 // Operands of one tile as loaded by threads t < 128 (raw bf16 bits).
@@ -96,10 +100,21 @@ struct OpsRegs {
   uint32_t k, q, g, v, beta;
 };
 
-template <bool KDA>
+// FMT = kMixed: the default tiers (BF16 high rows, one fp32 (s, z) per low
+// row). FMT = kPaper: the paper's tiers (FP16 high rows, FP16 (s, z) per group
+// of 32). With the block-32 transform (p.had) the recurrence runs in the
+// transformed domain: H is symmetric and orthonormal, so a low row is used as
+// stored (s (c - z) of the transformed values) and only the FP16 rows are
+// transformed, on load and before the store; v is transformed on staging and
+// o transformed back before it is written. Eq. (1) commutes with the
+// transform: S H = Lambda S_prev H + beta k (H delta)^T, delta_H = H v - (S_bar
+// H)^T k, o = H (S H)^T q.
+template <bool KDA, int FMT>
 __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, const int ntiles,
                                                         const int tile_bytes) {
   constexpr int D = 128, RG = 32, RPT = 4, CPT = 16, TPR = 8;
+  constexpr bool kP = FMT == kPaper;
+  using RawSet = RawSetT<FMT>;
   constexpr int kDrop = 0x40000000;  // buffer offset past any tile: the store is dropped
   // Per-wave partial column sums of k~ . S_bar (index c) and q~ . S_bar
   // (index D + c), in the slot order described at the reduction below;
@@ -111,9 +126,13 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
   __shared__ float4 opr[3][D];
   __shared__ float vsh[3][D];
   __shared__ float opsc[3][4];
-  // Per wave: the (s, z) pairs of its 32 rows (8 wave + j + 32 i at index
-  // j + 8 i) of the next tile as loaded [0], and as re-encoded [1].
-  __shared__ float2 msh[4][2][32];
+  // Per wave: the metadata of its 32 rows (8 wave + j + 32 i at index j +
+  // 8 i) of the next tile as loaded [0], and as re-encoded [1]: (s, z) pairs,
+  // or the four FP16 (s, z) words of the paper's groups.
+  __shared__ float2 msh[4][2][kP ? 1 : 32];
+  __shared__ u32x4 mshp[4][2][kP ? 32 : 1];
+  __shared__ float osh[kP ? D : 1];  // o in the transformed domain (wave 3)
+  const bool had = kP && p.had != 0;
 
   const int t = threadIdx.x;
   const int lane = t & 63;
@@ -130,6 +149,7 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
   const bool hi0 = rg < k_hi;  // row slot 0 of this thread is in the bf16 tier
   const int lo0 = k_hi * D * 2;
   const int meta0 = lo0 + (D - k_hi) * D;
+  constexpr int kMetaRow = kP ? 16 : 8;  // metadata bytes per low row
   const int o_esize = p.o_bf16 ? 2 : 4;
   // slot ids are read-only here: scalar loads through the constant address space
   const __attribute__((address_space(4))) int32_t* slots =
@@ -152,7 +172,7 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
   // the high tier have no metadata: their loads read bytes of the tile that
   // are never used, their stores are dropped.
   const int mrow = 8 * wave + (lane & 7) + 32 * (lane >> 3);
-  const int off_m = lane < 32 ? meta0 + (mrow - k_hi) * 8 : kDrop;
+  const int off_m = lane < 32 ? meta0 + (mrow - k_hi) * kMetaRow : kDrop;
   const int st_m = (lane < 32 && mrow >= k_hi) ? off_m : kDrop;
   const int rgw = lane >> 3;  // row group within the wave
   const int my_u = (t < D && p.perm) ? (static_cast<int>(p.perm[h * D + t]) & (D - 1)) : t;
@@ -187,7 +207,16 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
       const float qf = bf16_to_f32(static_cast<uint16_t>(r.q));
       const float gf = bf16_to_f32(static_cast<uint16_t>(r.g));
       opr[buf][t] = make_float4(kf, qf, KDA ? __expf(gf) : 1.0f, 0.0f);
-      vsh[buf][t] = bf16_to_f32(static_cast<uint16_t>(r.v));
+      float vf = bf16_to_f32(static_cast<uint16_t>(r.v));
+      if (had) {  // v in the transformed domain: 32 consecutive lanes hold a group
+#pragma unroll
+        for (int m = 1; m < 32; m <<= 1) {
+          const float o_ = __shfl_xor(vf, m, 64);
+          vf = (t & m) ? o_ - vf : vf + o_;
+        }
+        vf *= kInvSqrt32;
+      }
+      vsh[buf][t] = vf;
       const float kq = wave_sum_dpp(kf * qf);
       if ((t & 63) == 0) opsc[buf][2 + (t >> 6)] = kq;
       if (t == 0) {
@@ -205,7 +234,8 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
     return __builtin_amdgcn_make_buffer_rsrc(base, 0, live ? tile_bytes : 0, kBufferConfig);
   };
   auto issue_raw = [&](RawSet& rs, __amdgpu_buffer_rsrc_t r) {
-    rs.rm = ld8(r, off_m);
+    if constexpr (kP) rs.rm = ld16(r, off_m);
+    else rs.rm = ld8(r, off_m);
     rs.ra[0] = ld16(r, off_a0);
     if (!wave_lo) rs.rb0 = ld16(r, off_b0);
 #pragma unroll
@@ -213,8 +243,10 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
   };
   // metadata of a prefetched tile into the wave's LDS slice
   auto stage_meta = [&](const RawSet& rs) {
-    if (lane < 32)
-      msh[wave][0][lane] = make_float2(__uint_as_float(rs.rm.x), __uint_as_float(rs.rm.y));
+    if (lane < 32) {
+      if constexpr (kP) mshp[wave][0][lane] = rs.rm;
+      else msh[wave][0][lane] = make_float2(__uint_as_float(rs.rm.x), __uint_as_float(rs.rm.y));
+    }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
@@ -261,16 +293,36 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
     }
     float2 sz[RPT];
 #pragma unroll
-    for (int i = 0; i < RPT; ++i) sz[i] = msh[wave][0][rgw + 8 * i];
+    for (int i = 0; i < RPT; ++i) {
+      if constexpr (kP) {  // this lane's group: FP16 (s, z) in one word
+        const uint32_t m = reinterpret_cast<const uint32_t*>(&mshp[wave][0][0])[(rgw + 8 * i) * 4 +
+                                                                               (cg >> 1)];
+        sz[i] = make_float2(f16_lo(m), f16_hi(m));
+      } else {
+        sz[i] = msh[wave][0][rgw + 8 * i];
+      }
+    }
     float x[RPT][CPT];
     const u32x4* ra = cur.ra;
     if (hi0) {
+      if constexpr (kP) {  // FP16 rows, into the transformed domain with had
+        const float a0 = aa[0] * (had ? kInvSqrt32 : 1.0f);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        x[0][2 * j] = aa[0] * bf16_lo(ra[0][j]);
-        x[0][2 * j + 1] = aa[0] * bf16_hi(ra[0][j]);
-        x[0][8 + 2 * j] = aa[0] * bf16_lo(cur.rb0[j]);
-        x[0][8 + 2 * j + 1] = aa[0] * bf16_hi(cur.rb0[j]);
+        for (int j = 0; j < 4; ++j) {
+          x[0][2 * j] = a0 * f16_lo(ra[0][j]);
+          x[0][2 * j + 1] = a0 * f16_hi(ra[0][j]);
+          x[0][8 + 2 * j] = a0 * f16_lo(cur.rb0[j]);
+          x[0][8 + 2 * j + 1] = a0 * f16_hi(cur.rb0[j]);
+        }
+        if (had) fwht32_pair(x[0], (cg & 1) != 0);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          x[0][2 * j] = aa[0] * bf16_lo(ra[0][j]);
+          x[0][2 * j + 1] = aa[0] * bf16_hi(ra[0][j]);
+          x[0][8 + 2 * j] = aa[0] * bf16_lo(cur.rb0[j]);
+          x[0][8 + 2 * j + 1] = aa[0] * bf16_hi(cur.rb0[j]);
+        }
       }
     } else {
       const float A = aa[0] * sz[0].x;
@@ -382,6 +434,32 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
       const __amdgpu_buffer_rsrc_t ro =
           __builtin_amdgcn_make_buffer_rsrc(obase, 0, D * o_esize, kBufferConfig);
       if (wave != 3) {
+      } else if (had) {
+        // back from the transformed domain: columns lane and lane + 64,
+        // each group of 32 in 32 consecutive lanes
+        if (b5) {
+          *reinterpret_cast<float2*>(&osh[c_pair]) = make_float2(ov[0], ov[1]);
+          *reinterpret_cast<float2*>(&osh[c_pair + 8]) = make_float2(ov[2], ov[3]);
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+        float o0 = osh[lane], o1 = osh[lane + 64];
+#pragma unroll
+        for (int m = 1; m < 32; m <<= 1) {
+          const float a_ = __shfl_xor(o0, m, 64), c_ = __shfl_xor(o1, m, 64);
+          o0 = (lane & m) ? a_ - o0 : o0 + a_;
+          o1 = (lane & m) ? c_ - o1 : o1 + c_;
+        }
+        o0 *= kInvSqrt32;
+        o1 *= kInvSqrt32;
+        if (p.o_bf16) {
+          __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16(o0), ro, lane * 2, 0, 0);
+          __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16(o1), ro, (lane + 64) * 2, 0, 0);
+        } else {
+          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(o0), ro, lane * 4, 0, 0);
+          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(o1), ro, (lane + 64) * 4, 0, 0);
+        }
       } else if (p.o_bf16) {
         __builtin_amdgcn_raw_buffer_store_b32(pack_bf16x2(ov[0], ov[1]), ro, st_o, 0, 0);
         __builtin_amdgcn_raw_buffer_store_b32(pack_bf16x2(ov[2], ov[3]), ro, st_o, 16, 0);
@@ -424,10 +502,23 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
 #pragma unroll
     for (int i = 0; i < RPT; ++i) {
       if (i == 0 && hi0) {
+        if constexpr (kP) {  // FP16 rows, back from the transformed domain with had
+          if (had) {
+            fwht32_pair(x[0], (cg & 1) != 0);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          wa[0][j] = pack_bf16x2(x[0][2 * j], x[0][2 * j + 1]);
-          wb0[j] = pack_bf16x2(x[0][8 + 2 * j], x[0][8 + 2 * j + 1]);
+            for (int j = 0; j < CPT; ++j) x[0][j] *= kInvSqrt32;
+          }
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            wa[0][j] = pack_f16x2(x[0][2 * j], x[0][2 * j + 1]);
+            wb0[j] = pack_f16x2(x[0][8 + 2 * j], x[0][8 + 2 * j + 1]);
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            wa[0][j] = pack_bf16x2(x[0][2 * j], x[0][2 * j + 1]);
+            wb0[j] = pack_bf16x2(x[0][8 + 2 * j], x[0][8 + 2 * j + 1]);
+          }
         }
         wm[0] = make_float2(0.0f, 0.0f);
         continue;
@@ -438,9 +529,13 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
         mn = fminf(mn, x[i][j]);
         mx = fmaxf(mx, x[i][j]);
       }
-      group_minmax<TPR>(mn, mx);
       float s, z, inv;
-      row_qparams(mn, mx, s, z, inv);
+      if constexpr (kP) {  // the lane pair's group of 32, FP16 (s, z)
+        group_qparams_f16(mn, mx, s, z, inv);
+      } else {
+        group_minmax<TPR>(mn, mx);
+        row_qparams(mn, mx, s, z, inv);
+      }
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         // v_cvt_pk_u8_f32 rounds to nearest even and saturates to [0, 255]
@@ -453,21 +548,32 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
       if (i == 0) wb0 = u32x4{0u, 0u, 0u, 0u};
     }
     // metadata of the wave's rows, gathered through its LDS slice
-    if (cg == 0) {
+    if constexpr (kP) {
+      if ((cg & 1) == 0) {
+#pragma unroll
+        for (int i = 0; i < RPT; ++i)
+          reinterpret_cast<uint32_t*>(&mshp[wave][1][0])[(rgw + 8 * i) * 4 + (cg >> 1)] =
+              pack_f16x2(wm[i].x, wm[i].y);
+      }
+    } else if (cg == 0) {
 #pragma unroll
       for (int i = 0; i < RPT; ++i) msh[wave][1][rgw + 8 * i] = wm[i];
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
-    const float2 mo = msh[wave][1][lane & 31];
     // every lane issues the same stores; lanes with nothing to write use an
     // offset past the buffer, which the hardware drops
     st16(wa[0], rs_cur, off_a0);
     if (!wave_lo) st16(wb0, rs_cur, st_b0);
 #pragma unroll
     for (int i = 1; i < RPT; ++i) st16(wa[i], rs_cur, off_a1, (i - 1) * kStepA);
-    st8(u32x2{__float_as_uint(mo.x), __float_as_uint(mo.y)}, rs_cur, st_m);
+    if constexpr (kP) {
+      st16(mshp[wave][1][lane & 31], rs_cur, st_m);
+    } else {
+      const float2 mo = msh[wave][1][lane & 31];
+      st8(u32x2{__float_as_uint(mo.x), __float_as_uint(mo.y)}, rs_cur, st_m);
+    }
     if (has_next) stage_meta(oth);
 
     done = !has_next;
@@ -506,10 +612,10 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
 
 struct Occupancy {
   int cus = 0;
-  int per_cu[2] = {0, 0};
+  int per_cu[4] = {0, 0, 0, 0};
 };
 
-bool occupancy(bool kda, int& cus, int& per_cu) {
+bool occupancy(bool kda, bool paper, int& cus, int& per_cu) {
   static Occupancy cache[16];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 16) return false;
@@ -518,26 +624,25 @@ bool occupancy(bool kda, int& cus, int& per_cu) {
     int n = 0;
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
       return false;
-    int a = 0, b = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&a, update_stream128<false>, 256, 0) !=
-            hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, update_stream128<true>, 256, 0) !=
-            hipSuccess)
+    int a[4] = {0, 0, 0, 0};
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&a[0], update_stream128<false, kMixed>, 256, 0) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&a[1], update_stream128<true, kMixed>, 256, 0) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&a[2], update_stream128<false, kPaper>, 256, 0) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&a[3], update_stream128<true, kPaper>, 256, 0) != hipSuccess)
       return false;
-    c.per_cu[0] = a > 0 ? a : 1;
-    c.per_cu[1] = b > 0 ? b : 1;
+    for (int i = 0; i < 4; ++i) c.per_cu[i] = a[i] > 0 ? a[i] : 1;
     c.cus = n;
   }
   cus = c.cus;
-  per_cu = c.per_cu[kda ? 1 : 0];
+  per_cu = c.per_cu[(kda ? 1 : 0) + (paper ? 2 : 0)];
   return true;
 }
 
 }  // namespace
 
-bool launch_stream128(bool kda, const UpdateParams& p, int B, hipStream_t stream) {
+bool launch_stream128(bool kda, bool paper, const UpdateParams& p, int B, hipStream_t stream) {
   int cus = 0, per_cu = 0;
-  if (!occupancy(kda, cus, per_cu)) return false;
+  if (!occupancy(kda, paper, cus, per_cu)) return false;
   const int ntiles = B * p.HV;
   // resident workgroups, rounded down to a multiple of HV (at least HV)
   const long capacity = static_cast<long>(cus) * per_cu;
@@ -545,13 +650,17 @@ bool launch_stream128(bool kda, const UpdateParams& p, int B, hipStream_t stream
   if (per_head < 1) per_head = 1;
   if (per_head > B) per_head = B;
   const int grid = static_cast<int>(per_head * p.HV);
-  const int tile_bytes = p.k_hi * 128 * 2 + (128 - p.k_hi) * 128 + (128 - p.k_hi) * 8;
-  if (kda)
-    hipLaunchKernelGGL(update_stream128<true>, dim3(grid), dim3(256), 0, stream, p, ntiles,
-                       tile_bytes);
+  const int tile_bytes =
+      p.k_hi * 128 * 2 + (128 - p.k_hi) * 128 + (128 - p.k_hi) * (paper ? 16 : 8);
+  const dim3 g(grid), blk(256);
+  if (kda && paper)
+    hipLaunchKernelGGL((update_stream128<true, kPaper>), g, blk, 0, stream, p, ntiles, tile_bytes);
+  else if (kda)
+    hipLaunchKernelGGL((update_stream128<true, kMixed>), g, blk, 0, stream, p, ntiles, tile_bytes);
+  else if (paper)
+    hipLaunchKernelGGL((update_stream128<false, kPaper>), g, blk, 0, stream, p, ntiles, tile_bytes);
   else
-    hipLaunchKernelGGL(update_stream128<false>, dim3(grid), dim3(256), 0, stream, p, ntiles,
-                       tile_bytes);
+    hipLaunchKernelGGL((update_stream128<false, kMixed>), g, blk, 0, stream, p, ntiles, tile_bytes);
   return true;
 }
 

@@ -140,3 +140,33 @@ def test_trajectory_from_the_zero_state():
         _say(f"  step {t}: o rel-L2 {err:.2e}")
         assert err <= O_TOL_MIXED
     compare_tiles(gpool.buffer.cpu().numpy(), ref, "paper trajectory")
+
+
+@pytest.mark.parametrize("kda,had,k_hi", [(False, 1, 16), (True, 1, 16), (False, 0, 32),
+                                          (True, 0, 8)])
+def test_many_tiles_per_workgroup(kda, had, k_hi):
+    """d = 128 with more requests than resident workgroups, so each
+    workgroup streams several tiles; slots in random order, some padded or
+    out of range (o = 0, their tiles untouched)."""
+    d, HV, B = 128, 4, 300
+    HK = HV if kda else 2
+    _say(f"paper many tiles kda={kda} had={had} k_hi={k_hi}")
+    seed = 900 + 3 * kda + had + k_hi
+    n_slots = B + 40
+    slots = inputs.slot_order(seed, n_slots, B)
+    slots[::37] = -1
+    slots[5] = n_slots  # out of range
+    perm = inputs.random_perms(seed, HV, d)
+    S = inputs.synthetic_states(seed, B, HV, d)
+    inputs.scale_channels(S, inputs.outlier_channels(seed, HV, d, 8), 10.0)
+    ref = orc.Pool(orc.KIND_MIXED, d, d, k_hi, 1, n_slots, HV, fmt=_fmt(had))
+    live = (slots >= 0) & (slots < n_slots)
+    orc.pack(ref, 0, slots[live], S[live], perm)
+    gpool = gpu_pool_from(ref, D)
+    inp = inputs.step(inputs.decode_inputs(seed, 1, B, HK, HV, d, kda=kda), 0)
+    o_gpu, o_ref = _step(kda, ref, gpool, slots, inp, perm, scale=1.0)
+    assert np.all(o_gpu[~live] == 0) and np.all(o_ref[~live] == 0)
+    err = rel_l2(o_gpu, o_ref)
+    stats = compare_tiles(gpool.buffer.cpu().numpy(), ref, f"paper many tiles kda={kda}")
+    _say(f"  o rel-L2 {err:.2e}  {stats}")
+    assert err <= 1e-4
