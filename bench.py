@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--rotations", type=int, default=8)
+    ap.add_argument("--prewarm", type=float, default=PREWARM_S,
+                    help="seconds of launches before the warm-up steps of each measurement")
     ap.add_argument("--quick", action="store_true", help="headline only: no baselines, no CPU")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
@@ -219,11 +221,24 @@ class Workload:
                 for i in range(len(calls))]
 
 
-def time_steps(torch, calls, warmup: int, steps: int):
+PREWARM_S = 0.5
+
+
+def time_steps(torch, calls, warmup: int, steps: int, prewarm_s: float = None):
     """`steps` back-to-back launches between two synchronisations: wall time,
     and the HIP-event time over the same region on the launch stream (its
-    mean per launch is the kernel duration the roofline uses)."""
+    mean per launch is the kernel duration the roofline uses). Before the
+    `warmup` untimed launches the same calls run for `prewarm_s` seconds, so
+    that the GPU has left its idle clocks: a decode loop runs the kernel back
+    to back, and the first ~50 ms of launches after idle run up to 10% slower."""
     n = len(calls)
+    t_end = time.perf_counter() + (PREWARM_S if prewarm_s is None else prewarm_s)
+    i = 0
+    while time.perf_counter() < t_end:
+        for _ in range(32):
+            calls[i % n]()
+            i += 1
+        torch.cuda.synchronize()
     for i in range(warmup):
         calls[i % n]()
     torch.cuda.synchronize()
@@ -292,7 +307,7 @@ def sweep(torch, D, inputs, steps: int, log=print):
                     D.damp_state_pack(pool, 0, sl, S, perm)
                 calls = [D.PreparedUpdate(kda, pool, 0, sl, x["q"], x["k"], x["v"], x["g"],
                                           x["beta"], perm, 1.0, o) for sl in sets]
-                t = time_steps(torch, calls, 10, steps)
+                t = time_steps(torch, calls, 10, steps, prewarm_s=0.1)
                 nbytes = algorithmic_bytes(tb, B, HK, HV, d, kda, 2)
                 out.append(dict(model="KDA" if kda else "GDN", B=B,
                                 layout="fp32" if kind == D.DAMP_STATE_FP32 else
@@ -340,8 +355,13 @@ def multilayer(torch, D, inputs, steps: int, log=print):
             with torch.cuda.graph(g):
                 step(s_)
             graphs.append((g, s_))
-        for i in range(4):
+        t_end = time.perf_counter() + PREWARM_S  # leave the idle clocks (time_steps)
+        i = 0
+        while time.perf_counter() < t_end or i < 4:
             graphs[i % 2][0].replay()
+            i += 1
+            if i % 8 == 0:
+                torch.cuda.synchronize()
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         t0 = time.perf_counter()
@@ -485,6 +505,8 @@ def cpu_baseline(seconds: float, log=print):
 
 def main():
     args = parse()
+    global PREWARM_S
+    PREWARM_S = args.prewarm
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the state update has no "
               "cross-GPU step (tiles shard by value heads or request slots with no collective).", file=sys.stderr)

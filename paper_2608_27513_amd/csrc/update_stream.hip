@@ -127,11 +127,18 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
   __shared__ float vsh[3][D];
   __shared__ float opsc[3][4];
   // Per wave: the metadata of its 32 rows (8 wave + j + 32 i at index j +
-  // 8 i) of the next tile as loaded [0], and as re-encoded [1]: (s, z) pairs,
-  // or the four FP16 (s, z) words of the paper's groups.
-  __shared__ float2 msh[4][2][kP ? 1 : 32];
+  // 8 i) of the next tile as loaded: (s, z) pairs, or (paper tiers, [0]) the
+  // four FP16 (s, z) words of the groups, which also pass through [1] as
+  // re-encoded.
+  __shared__ float2 msh[4][kP ? 1 : 32];
   __shared__ u32x4 mshp[4][2][kP ? 32 : 1];
-  __shared__ float osh[kP ? D : 1];  // o in the transformed domain (wave 3)
+  // Default tiers: the re-encoded (s, z) of every row of a tile, by tile
+  // parity, stored after the next tile's workgroup barrier as whole lines.
+  __shared__ float2 mout[2][kP ? 1 : D];
+  // Per wave: its 8 high rows (slot 0) in tile order, 2 KB, for the
+  // exchange between the lane layout and whole 1 KB loads and stores.
+  __shared__ u32x4 hsh[4][2 * 64];
+  __shared__ float osh[D];  // o of the tile (wave 3), staged for one whole-row store
   const bool had = kP && p.had != 0;
 
   const int t = threadIdx.x;
@@ -155,18 +162,23 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
   const __attribute__((address_space(4))) int32_t* slots =
       (const __attribute__((address_space(4))) int32_t*)p.slot_idx;
 
+  // every lane of this wave has a low row slot 0 (no bf16 second half to
+  // load or store), or every lane a high one
+  const bool wave_lo = 8 * wave >= k_hi;
+  const bool wave_hi = 8 * wave + 8 <= k_hi;
   // Byte offsets of this thread's row slices inside a tile (same for every
-  // tile). Row slot 0 is a bf16 row (two 16-byte halves at off_a0 and
+  // tile). Row slot 0 is a 16-bit row (two 16-byte halves at off_a0 and
   // off_b0) or a row of codes; rows 1..3 (always low) sit at off_a1 +
-  // (i-1) * 32 rows of codes (scalar offsets).
-  const int off_a0 = hi0 ? (rg * D + col0) * 2 : lo0 + (rg - k_hi) * D + col0;
-  const int off_b0 = off_a0 + 16;
+  // (i-1) * 32 rows of codes (scalar offsets). A wave whose slot-0 rows are
+  // all high (rows 8 wave .. 8 wave + 7, 2 KB of the tile) loads them as two
+  // whole 1 KB blocks instead, lane l taking bytes 16 l of each; the rows
+  // reach the lane layout through the wave's LDS slice (stage_meta).
+  const int off_a0 = wave_hi ? 2048 * wave + 16 * lane
+                             : (hi0 ? (rg * D + col0) * 2 : lo0 + (rg - k_hi) * D + col0);
+  const int off_b0 = wave_hi ? off_a0 + 1024 : off_a0 + 16;
   const int off_a1 = lo0 + (rg + RG - k_hi) * D + col0;
   constexpr int kStepA = RG * D;
-  const int st_b0 = hi0 ? off_b0 : kDrop;                    // second bf16 half
-  // every lane of this wave has a low row slot 0 (no bf16 second half to
-  // load or store)
-  const bool wave_lo = 8 * wave >= k_hi;
+  const int st_b0 = hi0 ? off_b0 : kDrop;  // second half of a 16-bit row
   // The metadata of the wave's 32 rows moves with one 8-byte access per
   // lane: lane l < 32 handles row 8 wave + (l & 7) + 32 (l >> 3). Rows of
   // the high tier have no metadata: their loads read bytes of the tile that
@@ -185,7 +197,11 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
   const int s0q = (b5 ? D / 4 : 0) + cg * 4 + 2 * (b4 ? 1 : 0) + (b3 ? 1 : 0);  // float4 index
   const int dq = cg * 4 + 2 * (b4 ? 1 : 0) + (b3 ? 1 : 0);  // float4 index of delta in dwv
   // o: the q-kind lanes of wave 3 write columns c_pair + {0, 1} and c_pair + 8 + {0, 1}
-  const int st_o = (wave == 3 && b5) ? c_pair * o_esize : kDrop;
+  auto wave_sync = [] {  // orders the wave's own LDS accesses
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+  };
 
   if (static_cast<int>(blockIdx.x) >= ntiles) return;
 
@@ -233,23 +249,41 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
                     static_cast<size_t>(h) * p.tile_stride;
     return __builtin_amdgcn_make_buffer_rsrc(base, 0, live ? tile_bytes : 0, kBufferConfig);
   };
-  auto issue_raw = [&](RawSet& rs, __amdgpu_buffer_rsrc_t r) {
-    if constexpr (kP) rs.rm = ld16(r, off_m);
-    else rs.rm = ld8(r, off_m);
-    rs.ra[0] = ld16(r, off_a0);
-    if (!wave_lo) rs.rb0 = ld16(r, off_b0);
-#pragma unroll
-    for (int i = 1; i < RPT; ++i) rs.ra[i] = ld16(r, off_a1, (i - 1) * kStepA);
+  // The loads of a tile in four parts (metadata and row slot 0, then one
+  // slot of codes each), issued at four points of the previous tile's
+  // computation: a burst of them would stall the wave on the full
+  // address queue while it has arithmetic to do.
+  auto issue_raw_part = [&](RawSet& rs, __amdgpu_buffer_rsrc_t r, int part) {
+    if (part == 0) {
+      if constexpr (kP) rs.rm = ld16(r, off_m);
+      else rs.rm = ld8(r, off_m);
+      rs.ra[0] = ld16(r, off_a0);
+      if (!wave_lo) rs.rb0 = ld16(r, off_b0);
+    } else {
+      rs.ra[part] = ld16(r, off_a1, (part - 1) * kStepA);
+    }
   };
-  // metadata of a prefetched tile into the wave's LDS slice
-  auto stage_meta = [&](const RawSet& rs) {
+  auto issue_raw = [&](RawSet& rs, __amdgpu_buffer_rsrc_t r) {
+#pragma unroll
+    for (int part = 0; part < RPT; ++part) issue_raw_part(rs, r, part);
+  };
+  // metadata of a prefetched tile into the wave's LDS slice; the high rows
+  // of a wave_hi wave from whole blocks into the lane layout (row lane / 8,
+  // columns 16 (lane % 8) ..)
+  auto stage_meta = [&](RawSet& rs) {
     if (lane < 32) {
       if constexpr (kP) mshp[wave][0][lane] = rs.rm;
-      else msh[wave][0][lane] = make_float2(__uint_as_float(rs.rm.x), __uint_as_float(rs.rm.y));
+      else msh[wave][lane] = make_float2(__uint_as_float(rs.rm.x), __uint_as_float(rs.rm.y));
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+    if (wave_hi) {
+      hsh[wave][lane] = rs.ra[0];
+      hsh[wave][64 + lane] = rs.rb0;
+    }
+    wave_sync();
+    if (wave_hi) {
+      rs.ra[0] = hsh[wave][2 * lane];
+      rs.rb0 = hsh[wave][2 * lane + 1];
+    }
   };
   auto slot_of = [&](int b_) { return b_ < B ? slots[b_] : -1; };
 
@@ -266,6 +300,19 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
   __amdgpu_buffer_rsrc_t rs_n1 = make_rsrc(slot_n1);
   bool done = false;
   int buf = 0, pb = 0;
+  // The re-encoded (s, z) of a tile (default tiers) are stored after the
+  // next tile's workgroup barrier, when every wave's rows are in mout: wave
+  // w writes the 256 contiguous bytes of rows k_hi + 32 w ..
+  __amdgpu_buffer_rsrc_t rs_prev = make_rsrc(-1);
+  auto store_prev_meta = [&](int pbuf) {
+    if constexpr (!kP) {
+      const int r = k_hi + 32 * wave + lane;
+      const bool on = lane < 32 && r < D;
+      const float2 mo = mout[pbuf][on ? r : 0];
+      st8(u32x2{__float_as_uint(mo.x), __float_as_uint(mo.y)}, rs_prev,
+          on ? meta0 + (32 * wave + lane) * 8 : kDrop);
+    }
+  };
   int turn = b % 3;
 
   auto tile = [&](OpsRegs& pub, OpsRegs& nxt, RawSet& cur, RawSet& oth) {
@@ -299,7 +346,7 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
                                                                                (cg >> 1)];
         sz[i] = make_float2(f16_lo(m), f16_hi(m));
       } else {
-        sz[i] = msh[wave][0][rgw + 8 * i];
+        sz[i] = msh[wave][rgw + 8 * i];
       }
     }
     float x[RPT][CPT];
@@ -356,14 +403,17 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
                    "v"(x[i][10]), "v"(x[i][11]), "v"(x[i][12]), "v"(x[i][13]), "v"(x[i][14]),
                    "v"(x[i][15]));
 
-    // -- prefetch: packed bytes and operands two tiles ahead
+    // -- prefetch: packed bytes and operands two tiles ahead (the first part
+    // of the bytes here, the others between the read-out halves and after
+    // the barrier)
     const int b_n = b + b_step;
     const bool has_next = b_n < B;
+    const bool pf = b_n + b_step < B;
     __amdgpu_buffer_rsrc_t rs_n2 = rs_n1;
     int slot_n3 = -1;
-    if (b_n + b_step < B) {
+    if (pf) {
       rs_n2 = make_rsrc(slot_n2);
-      issue_raw(cur, rs_n2);
+      issue_raw_part(cur, rs_n2, 0);
       issue_ops(nxt, b_n + b_step);
       slot_n3 = slot_of(b_n + 2 * b_step);
     }
@@ -395,10 +445,15 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
       for (int j = 0; j < 4; ++j) r2[j] = fold16(r1[j], r1[j + 4]);  // column 8 hf + 4 b4 + j
 #pragma unroll
       for (int j = 0; j < 2; ++j) r3[2 * hf + j] = fold8(r2[j], r2[j + 2], b3);
+      __builtin_amdgcn_sched_barrier(0);
+      if (pf) issue_raw_part(cur, rs_n2, 1 + hf);
+      __builtin_amdgcn_sched_barrier(0);
     }
     part[pb][wave][s0q] = make_float4(r3[0], r3[1], r3[2], r3[3]);
     if (has_next) publish_ops(pub, buf_n);  // loaded a whole tile ago
     lds_barrier();
+    store_prev_meta(pb ^ 1);
+    if (pf) issue_raw_part(cur, rs_n2, 3);
 
     // -- column totals of this lane's 4 slots over the 4 waves; delta = v -
     // S_bar^T k~ on the k lanes; one swap gives every lane delta and the
@@ -433,41 +488,42 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
                        (static_cast<size_t>(b) * HV + h) * D * o_esize;
       const __amdgpu_buffer_rsrc_t ro =
           __builtin_amdgcn_make_buffer_rsrc(obase, 0, D * o_esize, kBufferConfig);
-      if (wave != 3) {
-      } else if (had) {
-        // back from the transformed domain: columns lane and lane + 64,
-        // each group of 32 in 32 consecutive lanes
+      if (wave == 3) {
         if (b5) {
           *reinterpret_cast<float2*>(&osh[c_pair]) = make_float2(ov[0], ov[1]);
           *reinterpret_cast<float2*>(&osh[c_pair + 8]) = make_float2(ov[2], ov[3]);
         }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
-        float o0 = osh[lane], o1 = osh[lane + 64];
+        wave_sync();
+        if (had) {
+          // back from the transformed domain: columns lane and lane + 64,
+          // each group of 32 in 32 consecutive lanes
+          float o0 = osh[lane], o1 = osh[lane + 64];
 #pragma unroll
-        for (int m = 1; m < 32; m <<= 1) {
-          const float a_ = __shfl_xor(o0, m, 64), c_ = __shfl_xor(o1, m, 64);
-          o0 = (lane & m) ? a_ - o0 : o0 + a_;
-          o1 = (lane & m) ? c_ - o1 : o1 + c_;
+          for (int m = 1; m < 32; m <<= 1) {
+            const float a_ = __shfl_xor(o0, m, 64), c_ = __shfl_xor(o1, m, 64);
+            o0 = (lane & m) ? a_ - o0 : o0 + a_;
+            o1 = (lane & m) ? c_ - o1 : o1 + c_;
+          }
+          wave_sync();
+          osh[lane] = o0 * kInvSqrt32;
+          osh[lane + 64] = o1 * kInvSqrt32;
+          wave_sync();
         }
-        o0 *= kInvSqrt32;
-        o1 *= kInvSqrt32;
+        // one store writes the whole row: 16 lanes x 16 bytes (bf16) or 32
+        // lanes x 16 bytes (fp32); the other lanes' offsets lie past the
+        // buffer and are dropped
+        const float4* o4 = reinterpret_cast<const float4*>(osh);
+        u32x4 ow;
         if (p.o_bf16) {
-          __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16(o0), ro, lane * 2, 0, 0);
-          __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16(o1), ro, (lane + 64) * 2, 0, 0);
+          const float4 a = o4[2 * (lane & 15)], c = o4[2 * (lane & 15) + 1];
+          ow = u32x4{pack_bf16x2(a.x, a.y), pack_bf16x2(a.z, a.w), pack_bf16x2(c.x, c.y),
+                     pack_bf16x2(c.z, c.w)};
         } else {
-          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(o0), ro, lane * 4, 0, 0);
-          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(o1), ro, (lane + 64) * 4, 0, 0);
+          const float4 a = o4[lane & 31];
+          ow = u32x4{__float_as_uint(a.x), __float_as_uint(a.y), __float_as_uint(a.z),
+                     __float_as_uint(a.w)};
         }
-      } else if (p.o_bf16) {
-        __builtin_amdgcn_raw_buffer_store_b32(pack_bf16x2(ov[0], ov[1]), ro, st_o, 0, 0);
-        __builtin_amdgcn_raw_buffer_store_b32(pack_bf16x2(ov[2], ov[3]), ro, st_o, 16, 0);
-      } else {
-        __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(ov[0]), __float_as_uint(ov[1])},
-                                              ro, st_o, 0, 0);
-        __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(ov[2]), __float_as_uint(ov[3])},
-                                              ro, st_o, 32, 0);
+        __builtin_amdgcn_raw_buffer_store_b128(ow, ro, lane * 16, 0, 0);
       }
     }
 
@@ -547,7 +603,10 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
       wm[i] = make_float2(s, z);
       if (i == 0) wb0 = u32x4{0u, 0u, 0u, 0u};
     }
-    // metadata of the wave's rows, gathered through its LDS slice
+    // metadata of the wave's rows: the paper tiers' 16 bytes per row go
+    // through the wave's LDS slice (a wave's 8 consecutive rows make a whole
+    // 128-byte line); the default tiers' (s, z) into the tile's table, stored
+    // after the next barrier (store_prev_meta)
     if constexpr (kP) {
       if ((cg & 1) == 0) {
 #pragma unroll
@@ -557,23 +616,26 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
       }
     } else if (cg == 0) {
 #pragma unroll
-      for (int i = 0; i < RPT; ++i) msh[wave][1][rgw + 8 * i] = wm[i];
+      for (int i = 0; i < RPT; ++i) mout[pb][rg + RG * i] = wm[i];
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+    // the high rows of a wave_hi wave as two whole 1 KB blocks
+    if (wave_hi) {
+      hsh[wave][2 * lane] = wa[0];
+      hsh[wave][2 * lane + 1] = wb0;
+    }
+    wave_sync();
     // every lane issues the same stores; lanes with nothing to write use an
     // offset past the buffer, which the hardware drops
-    st16(wa[0], rs_cur, off_a0);
-    if (!wave_lo) st16(wb0, rs_cur, st_b0);
+    if (wave_hi) {
+      st16(hsh[wave][lane], rs_cur, off_a0);
+      st16(hsh[wave][64 + lane], rs_cur, off_b0);
+    } else {
+      st16(wa[0], rs_cur, off_a0);
+      if (!wave_lo) st16(wb0, rs_cur, st_b0);
+    }
 #pragma unroll
     for (int i = 1; i < RPT; ++i) st16(wa[i], rs_cur, off_a1, (i - 1) * kStepA);
-    if constexpr (kP) {
-      st16(mshp[wave][1][lane & 31], rs_cur, st_m);
-    } else {
-      const float2 mo = msh[wave][1][lane & 31];
-      st8(u32x2{__float_as_uint(mo.x), __float_as_uint(mo.y)}, rs_cur, st_m);
-    }
+    if constexpr (kP) st16(mshp[wave][1][lane & 31], rs_cur, st_m);
     if (has_next) stage_meta(oth);
 
     done = !has_next;
@@ -583,6 +645,7 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
     slot_cur = slot_n1;
     slot_n1 = slot_n2;
     slot_n2 = slot_n3;
+    rs_prev = rs_cur;
     rs_cur = rs_n1;
     rs_n1 = rs_n2;
   };
@@ -607,6 +670,11 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
     if (done) break;
     tile(ops_a, ops_b, set_b, set_a);
     if (done) break;
+  }
+  // the last tile's (s, z), once every wave has put its rows in mout
+  if constexpr (!kP) {
+    lds_barrier();
+    store_prev_meta(pb ^ 1);
   }
 }
 
