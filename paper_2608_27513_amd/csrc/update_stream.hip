@@ -109,9 +109,13 @@ struct OpsRegs {
 // o transformed back before it is written. Eq. (1) commutes with the
 // transform: S H = Lambda S_prev H + beta k (H delta)^T, delta_H = H v - (S_bar
 // H)^T k, o = H (S H)^T q.
-template <bool KDA, int FMT>
-__global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, const int ntiles,
-                                                        const int tile_bytes) {
+// DEPTH = tiles of packed bytes prefetched into registers. DEPTH = 1 holds
+// one raw tile set (168 VGPRs, three workgroups per CU): the shorter
+// prologue and the larger resident front win on short streams. DEPTH = 2
+// holds two (two workgroups per CU) and hides more latency on long streams.
+template <bool KDA, int FMT, int DEPTH>
+__global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
+    const UpdateParams p, const int ntiles, const int tile_bytes) {
   constexpr int D = 128, RG = 32, RPT = 4, CPT = 16, TPR = 8;
   constexpr bool kP = FMT == kPaper;
   using RawSet = RawSetT<FMT>;
@@ -287,11 +291,13 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
   };
   auto slot_of = [&](int b_) { return b_ < B ? slots[b_] : -1; };
 
-  // ---- one tile (request b): its packed bytes are in `cur` and those of the
-  // next tile in flight in `oth`; the bytes two tiles ahead are loaded into
-  // `cur` once it is dequantized. Its operands are in buffer `buf`; those of
-  // the next tile are in flight in `pub` and are published into buffer
-  // `buf_n`; those two tiles ahead are loaded into `nxt`.
+  // ---- one tile (request b): its packed bytes are in `cur`; with DEPTH = 2
+  // those of the next tile are in flight in `oth` (with DEPTH = 1, `oth` is
+  // `cur`). Once `cur` is dequantized it receives the bytes DEPTH tiles
+  // ahead, in four parts over this tile's arithmetic. Its operands are in
+  // buffer `buf`; those of the next tile are in flight in `pub` and are
+  // published into buffer `buf_n`; those two tiles ahead are loaded into
+  // `nxt`.
   int b = blockIdx.x / HV;
   int slot_cur = slot_of(b);
   int slot_n1 = slot_of(b + b_step);
@@ -403,17 +409,19 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
                    "v"(x[i][10]), "v"(x[i][11]), "v"(x[i][12]), "v"(x[i][13]), "v"(x[i][14]),
                    "v"(x[i][15]));
 
-    // -- prefetch: packed bytes and operands two tiles ahead (the first part
-    // of the bytes here, the others between the read-out halves and after
-    // the barrier)
+    // -- prefetch: the packed bytes DEPTH tiles ahead (the first part here,
+    // the others between the read-out halves and after the barrier) and the
+    // operands two tiles ahead
     const int b_n = b + b_step;
     const bool has_next = b_n < B;
-    const bool pf = b_n + b_step < B;
+    const bool has_next2 = b_n + b_step < B;
     __amdgpu_buffer_rsrc_t rs_n2 = rs_n1;
     int slot_n3 = -1;
-    if (pf) {
-      rs_n2 = make_rsrc(slot_n2);
-      issue_raw_part(cur, rs_n2, 0);
+    if (has_next2) rs_n2 = make_rsrc(slot_n2);
+    const bool pf = DEPTH == 1 ? has_next : has_next2;
+    const __amdgpu_buffer_rsrc_t rs_pf = DEPTH == 1 ? rs_n1 : rs_n2;
+    if (pf) issue_raw_part(cur, rs_pf, 0);
+    if (has_next2) {
       issue_ops(nxt, b_n + b_step);
       slot_n3 = slot_of(b_n + 2 * b_step);
     }
@@ -446,14 +454,14 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
 #pragma unroll
       for (int j = 0; j < 2; ++j) r3[2 * hf + j] = fold8(r2[j], r2[j + 2], b3);
       __builtin_amdgcn_sched_barrier(0);
-      if (pf) issue_raw_part(cur, rs_n2, 1 + hf);
+      if (pf) issue_raw_part(cur, rs_pf, 1 + hf);
       __builtin_amdgcn_sched_barrier(0);
     }
     part[pb][wave][s0q] = make_float4(r3[0], r3[1], r3[2], r3[3]);
     if (has_next) publish_ops(pub, buf_n);  // loaded a whole tile ago
     lds_barrier();
     store_prev_meta(pb ^ 1);
-    if (pf) issue_raw_part(cur, rs_n2, 3);
+    if (pf) issue_raw_part(cur, rs_pf, 3);
 
     // -- column totals of this lane's 4 slots over the 4 waves; delta = v -
     // S_bar^T k~ on the k lanes; one swap gives every lane delta and the
@@ -650,25 +658,27 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
     rs_n1 = rs_n2;
   };
 
-  // ---- prologue: the bytes of tiles 0 and 1 and the operands of tile 0 in
-  // flight, tile 1's operands in flight
+  // ---- prologue: the bytes and operands of tile 0 in flight, and those of
+  // tile 1 (its bytes only with DEPTH = 2)
   OpsRegs ops_a = {0u, 0u, 0u, 0u, 0u}, ops_b = {0u, 0u, 0u, 0u, 0u};
   RawSet set_a, set_b;
   issue_ops(ops_a, b);
   issue_raw(set_a, rs_cur);
   if (b + b_step < B) {
-    issue_raw(set_b, rs_n1);
+    if constexpr (DEPTH == 2) issue_raw(set_b, rs_n1);
     issue_ops(ops_b, b + b_step);
   }
   publish_ops(ops_a, 0);
   stage_meta(set_a);
   lds_barrier();
 
-  // two tiles per trip so the operand register sets alternate without copies
+  // two tiles per trip so the operand (and with DEPTH = 2 the raw) register
+  // sets alternate without copies
+  RawSet& set_2 = DEPTH == 1 ? set_a : set_b;
   for (;;) {
-    tile(ops_b, ops_a, set_a, set_b);
+    tile(ops_b, ops_a, set_a, set_2);
     if (done) break;
-    tile(ops_a, ops_b, set_b, set_a);
+    tile(ops_a, ops_b, set_2, set_a);
     if (done) break;
   }
   // the last tile's (s, z), once every wave has put its rows in mout
@@ -678,12 +688,27 @@ __global__ __launch_bounds__(256) void update_stream128(const UpdateParams p, co
   }
 }
 
+// The instantiations that launch_stream128 chooses from, and their
+// resident workgroups per CU (queried once per device).
+enum StreamKernel { kGdnMixed1, kGdnMixed2, kKdaMixed1, kKdaMixed2, kGdnPaper2, kKdaPaper2, kNumStream };
+
+const void* stream_kernel(int which) {
+  switch (which) {
+    case kGdnMixed1: return reinterpret_cast<const void*>(update_stream128<false, kMixed, 1>);
+    case kGdnMixed2: return reinterpret_cast<const void*>(update_stream128<false, kMixed, 2>);
+    case kKdaMixed1: return reinterpret_cast<const void*>(update_stream128<true, kMixed, 1>);
+    case kKdaMixed2: return reinterpret_cast<const void*>(update_stream128<true, kMixed, 2>);
+    case kGdnPaper2: return reinterpret_cast<const void*>(update_stream128<false, kPaper, 2>);
+    default: return reinterpret_cast<const void*>(update_stream128<true, kPaper, 2>);
+  }
+}
+
 struct Occupancy {
   int cus = 0;
-  int per_cu[4] = {0, 0, 0, 0};
+  int per_cu[kNumStream] = {};
 };
 
-bool occupancy(bool kda, bool paper, int& cus, int& per_cu) {
+bool occupancy(int which, int& cus, int& per_cu) {
   static Occupancy cache[16];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 16) return false;
@@ -692,26 +717,32 @@ bool occupancy(bool kda, bool paper, int& cus, int& per_cu) {
     int n = 0;
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
       return false;
-    int a[4] = {0, 0, 0, 0};
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&a[0], update_stream128<false, kMixed>, 256, 0) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&a[1], update_stream128<true, kMixed>, 256, 0) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&a[2], update_stream128<false, kPaper>, 256, 0) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&a[3], update_stream128<true, kPaper>, 256, 0) != hipSuccess)
-      return false;
-    for (int i = 0; i < 4; ++i) c.per_cu[i] = a[i] > 0 ? a[i] : 1;
+    int a[kNumStream] = {};
+    for (int i = 0; i < kNumStream; ++i)
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&a[i], stream_kernel(i), 256, 0) != hipSuccess)
+        return false;
+    for (int i = 0; i < kNumStream; ++i) c.per_cu[i] = a[i] > 0 ? a[i] : 1;
     c.cus = n;
   }
   cus = c.cus;
-  per_cu = c.per_cu[(kda ? 1 : 0) + (paper ? 2 : 0)];
+  per_cu = c.per_cu[which];
   return true;
 }
 
 }  // namespace
 
 bool launch_stream128(bool kda, bool paper, const UpdateParams& p, int B, hipStream_t stream) {
-  int cus = 0, per_cu = 0;
-  if (!occupancy(kda, paper, cus, per_cu)) return false;
   const int ntiles = B * p.HV;
+  int which = paper ? (kda ? kKdaPaper2 : kGdnPaper2) : (kda ? kKdaMixed2 : kGdnMixed2);
+  int cus = 0, per_cu = 0;
+  if (!occupancy(which, cus, per_cu)) return false;
+  // The default tiers prefetch one tile with three workgroups per CU when
+  // each of the two-per-CU workgroups would stream at most 16 tiles (the
+  // batch of 256 requests x 32 heads), two tiles otherwise.
+  if (!paper && static_cast<long>(ntiles) <= 16L * cus * per_cu) {
+    which = kda ? kKdaMixed1 : kGdnMixed1;
+    if (!occupancy(which, cus, per_cu)) return false;
+  }
   // resident workgroups, rounded down to a multiple of HV (at least HV)
   const long capacity = static_cast<long>(cus) * per_cu;
   long per_head = capacity / p.HV;
@@ -721,14 +752,26 @@ bool launch_stream128(bool kda, bool paper, const UpdateParams& p, int B, hipStr
   const int tile_bytes =
       p.k_hi * 128 * 2 + (128 - p.k_hi) * 128 + (128 - p.k_hi) * (paper ? 16 : 8);
   const dim3 g(grid), blk(256);
-  if (kda && paper)
-    hipLaunchKernelGGL((update_stream128<true, kPaper>), g, blk, 0, stream, p, ntiles, tile_bytes);
-  else if (kda)
-    hipLaunchKernelGGL((update_stream128<true, kMixed>), g, blk, 0, stream, p, ntiles, tile_bytes);
-  else if (paper)
-    hipLaunchKernelGGL((update_stream128<false, kPaper>), g, blk, 0, stream, p, ntiles, tile_bytes);
-  else
-    hipLaunchKernelGGL((update_stream128<false, kMixed>), g, blk, 0, stream, p, ntiles, tile_bytes);
+  switch (which) {
+    case kGdnMixed1:
+      hipLaunchKernelGGL((update_stream128<false, kMixed, 1>), g, blk, 0, stream, p, ntiles, tile_bytes);
+      break;
+    case kGdnMixed2:
+      hipLaunchKernelGGL((update_stream128<false, kMixed, 2>), g, blk, 0, stream, p, ntiles, tile_bytes);
+      break;
+    case kKdaMixed1:
+      hipLaunchKernelGGL((update_stream128<true, kMixed, 1>), g, blk, 0, stream, p, ntiles, tile_bytes);
+      break;
+    case kKdaMixed2:
+      hipLaunchKernelGGL((update_stream128<true, kMixed, 2>), g, blk, 0, stream, p, ntiles, tile_bytes);
+      break;
+    case kGdnPaper2:
+      hipLaunchKernelGGL((update_stream128<false, kPaper, 2>), g, blk, 0, stream, p, ntiles, tile_bytes);
+      break;
+    default:
+      hipLaunchKernelGGL((update_stream128<true, kPaper, 2>), g, blk, 0, stream, p, ntiles, tile_bytes);
+      break;
+  }
   return true;
 }
 
