@@ -463,40 +463,42 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
     store_prev_meta(pb ^ 1);
     if (pf) issue_raw_part(cur, rs_pf, 3);
 
-    // -- column totals of this lane's 4 slots over the 4 waves; delta = v -
-    // S_bar^T k~ on the k lanes; one swap gives every lane delta and the
-    // q total of its 4 columns
-    float tq[4], dd[4];
+    // -- column totals of this lane's 4 slots over the 4 waves (the k lanes:
+    // S_bar^T k~, the q lanes: S_bar^T q~); delta = v - S_bar^T k~ on the k
+    // lanes
+    float tot[4], dd[4];
     {
       const float4 p0 = part[pb][0][s0q], p1 = part[pb][1][s0q];
       const float4 p2 = part[pb][2][s0q], p3 = part[pb][3][s0q];
-      const float tot[4] = {(p0.x + p1.x) + (p2.x + p3.x), (p0.y + p1.y) + (p2.y + p3.y),
-                            (p0.z + p1.z) + (p2.z + p3.z), (p0.w + p1.w) + (p2.w + p3.w)};
+      tot[0] = (p0.x + p1.x) + (p2.x + p3.x);
+      tot[1] = (p0.y + p1.y) + (p2.y + p3.y);
+      tot[2] = (p0.z + p1.z) + (p2.z + p3.z);
+      tot[3] = (p0.w + p1.w) + (p2.w + p3.w);
       const float2 v0 = *reinterpret_cast<const float2*>(&vsh[buf][c_pair]);
       const float2 v1 = *reinterpret_cast<const float2*>(&vsh[buf][c_pair + 8]);
       const float vv[4] = {v0.x, v0.y, v1.x, v1.y};
 #pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        const float val = b5 ? tot[m] : vv[m] - tot[m];
-        const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(val),
-                                                        __float_as_uint(val), false, false);
-        dd[m] = __uint_as_float(r[0]);
-        tq[m] = __uint_as_float(r[1]);
-      }
+      for (int m = 0; m < 4; ++m) dd[m] = vv[m] - tot[m];
     }
-    const float beta = opsc[buf][0], qk = opsc[buf][2] + opsc[buf][3];
+    const float beta = opsc[buf][0];
 
-    // -- output o = scale (S_bar^T q~ + beta (q~.k~) delta), written by the
-    // q lanes of wave 3
-    {
+    // -- output o = scale (S_bar^T q~ + beta (q~.k~) delta), by wave 3: one
+    // swap gives its q lanes the delta of their 4 columns
+    if (wave == 3) {
+      const float bqk = beta * (opsc[buf][2] + opsc[buf][3]);
       float ov[4];
 #pragma unroll
-      for (int m = 0; m < 4; ++m) ov[m] = live ? p.scale * fmaf(beta * qk, dd[m], tq[m]) : 0.0f;
+      for (int m = 0; m < 4; ++m) {
+        const float val = b5 ? tot[m] : dd[m];
+        const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(val),
+                                                        __float_as_uint(val), false, false);
+        ov[m] = live ? p.scale * fmaf(bqk, __uint_as_float(r[0]), __uint_as_float(r[1])) : 0.0f;
+      }
       uint8_t* obase = static_cast<uint8_t*>(p.o) +
                        (static_cast<size_t>(b) * HV + h) * D * o_esize;
       const __amdgpu_buffer_rsrc_t ro =
           __builtin_amdgcn_make_buffer_rsrc(obase, 0, D * o_esize, kBufferConfig);
-      if (wave == 3) {
+      {
         if (b5) {
           *reinterpret_cast<float2*>(&osh[c_pair]) = make_float2(ov[0], ov[1]);
           *reinterpret_cast<float2*>(&osh[c_pair + 8]) = make_float2(ov[2], ov[3]);
