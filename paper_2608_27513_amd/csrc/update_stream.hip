@@ -142,7 +142,7 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
   // Per wave: its 8 high rows (slot 0) in tile order, 2 KB, for the
   // exchange between the lane layout and whole 1 KB loads and stores.
   __shared__ u32x4 hsh[4][2 * 64];
-  __shared__ float osh[D];  // o of the tile (wave 3), staged for one whole-row store
+  __shared__ float osh[D];  // o of the tile (output wave), staged for one whole-row store
   const bool had = kP && p.had != 0;
 
   const int t = threadIdx.x;
@@ -191,7 +191,16 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
   const int off_m = lane < 32 ? meta0 + (mrow - k_hi) * kMetaRow : kDrop;
   const int st_m = (lane < 32 && mrow >= k_hi) ? off_m : kDrop;
   const int rgw = lane >> 3;  // row group within the wave
-  const int my_u = (t < D && p.perm) ? (static_cast<int>(p.perm[h * D + t]) & (D - 1)) : t;
+  // Two waves stage the operands, one tile row per thread, and one wave writes
+  // o. With the paper's tiers the waves holding the 16-bit rows (0 and 1 for
+  // k_hi = 16) also transform them, so waves 2 and 3 stage and wave 1 writes:
+  // measured, 2.7% (GDN) and 5.7% (KDA) faster than waves 0, 1 and 3.
+  constexpr int kOpsT = kP ? 128 : 0;  // first thread of the operand waves
+  constexpr int kOutWave = kP ? 1 : 3;
+  const int tr = t - kOpsT;            // tile row of an operand thread
+  const bool ops_thread = tr >= 0 && tr < D;
+  const int my_u =
+      (ops_thread && p.perm) ? (static_cast<int>(p.perm[h * D + tr]) & (D - 1)) : (tr & (D - 1));
 
   // Reduction slots: after the in-wave folds, lane (cg, b3, b4, b5) holds the
   // wave's partial sums of kind b5 (0: k~, 1: q~) for the columns
@@ -200,7 +209,7 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
   const int c_pair = col0 + 4 * (b4 ? 1 : 0) + 2 * (b3 ? 1 : 0);  // first column of hf = 0
   const int s0q = (b5 ? D / 4 : 0) + cg * 4 + 2 * (b4 ? 1 : 0) + (b3 ? 1 : 0);  // float4 index
   const int dq = cg * 4 + 2 * (b4 ? 1 : 0) + (b3 ? 1 : 0);  // float4 index of delta in dwv
-  // o: the q-kind lanes of wave 3 write columns c_pair + {0, 1} and c_pair + 8 + {0, 1}
+  // o: the q-kind lanes of the output wave hold columns c_pair + {0, 1} and c_pair + 8 + {0, 1}
   auto wave_sync = [] {  // orders the wave's own LDS accesses
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
     __builtin_amdgcn_wave_barrier();
@@ -209,37 +218,37 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
 
   if (static_cast<int>(blockIdx.x) >= ntiles) return;
 
-  // ---- operand staging: threads t < D (waves 0 and 1) gather one tile row
+  // ---- operand staging: the operand threads gather one tile row each
   auto issue_ops = [&](OpsRegs& r, int b_) {
-    if (t < D) {
+    if (ops_thread) {
       const size_t bh = static_cast<size_t>(b_) * HV + h;
       const size_t kq = (static_cast<size_t>(b_) * p.HK + hk) * D;
       r.k = p.k[kq + my_u];
       r.q = p.q[kq + my_u];
       r.g = KDA ? p.g[bh * D + my_u] : p.g[bh];
-      r.v = p.v[bh * D + t];
+      r.v = p.v[bh * D + tr];
       r.beta = p.beta[bh];
     }
   };
   auto publish_ops = [&](const OpsRegs& r, int buf) {
-    if (t < D) {
+    if (ops_thread) {
       const float kf = bf16_to_f32(static_cast<uint16_t>(r.k));
       const float qf = bf16_to_f32(static_cast<uint16_t>(r.q));
       const float gf = bf16_to_f32(static_cast<uint16_t>(r.g));
-      opr[buf][t] = make_float4(kf, qf, KDA ? __expf(gf) : 1.0f, 0.0f);
+      opr[buf][tr] = make_float4(kf, qf, KDA ? __expf(gf) : 1.0f, 0.0f);
       float vf = bf16_to_f32(static_cast<uint16_t>(r.v));
       if (had) {  // v in the transformed domain: 32 consecutive lanes hold a group
 #pragma unroll
         for (int m = 1; m < 32; m <<= 1) {
           const float o_ = __shfl_xor(vf, m, 64);
-          vf = (t & m) ? o_ - vf : vf + o_;
+          vf = (tr & m) ? o_ - vf : vf + o_;
         }
         vf *= kInvSqrt32;
       }
-      vsh[buf][t] = vf;
+      vsh[buf][tr] = vf;
       const float kq = wave_sum_dpp(kf * qf);
-      if ((t & 63) == 0) opsc[buf][2 + (t >> 6)] = kq;
-      if (t == 0) {
+      if ((tr & 63) == 0) opsc[buf][2 + (tr >> 6)] = kq;
+      if (tr == 0) {
         opsc[buf][0] = bf16_to_f32(static_cast<uint16_t>(r.beta));
         opsc[buf][1] = KDA ? 1.0f : __expf(gf);
       }
@@ -482,9 +491,9 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
     }
     const float beta = opsc[buf][0];
 
-    // -- output o = scale (S_bar^T q~ + beta (q~.k~) delta), by wave 3: one
-    // swap gives its q lanes the delta of their 4 columns
-    if (wave == 3) {
+    // -- output o = scale (S_bar^T q~ + beta (q~.k~) delta), by the output
+    // wave: one swap gives its q lanes the delta of their 4 columns
+    if (wave == kOutWave) {
       const float bqk = beta * (opsc[buf][2] + opsc[buf][3]);
       float ov[4];
 #pragma unroll
