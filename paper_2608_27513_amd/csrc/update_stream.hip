@@ -2,13 +2,14 @@
 // tiles with at most 32 high-precision rows (section 3.1 Eq. (1)-(2);
 // section 3.2 Eq. (3); section 5.2 and App. A.5).
 //
-// The state update moves ~2.4 bytes per state value and does ~8 VALU
-// operations per value, so on MI355X the memory time and the VALU time are of
-// the same size; the kernel must overlap them. Each workgroup (4 wave64) is
-// resident for the whole launch and walks the tiles (b, h) with a fixed value
-// head h = blockIdx.x mod HV, so the channel permutation and the row offsets
-// are computed once. While tile k is reduced, updated, re-encoded and
-// stored, the packed bytes of tile k+1 are already in flight into registers.
+// The state update moves ~2.4 bytes per state value and does ~11 VALU
+// instructions per value, so on MI355X the memory time and the VALU time are
+// of the same size; the kernel must overlap them. Each workgroup (4 wave64)
+// is resident for the whole launch and walks the tiles (b, h) with a fixed
+// value head h = blockIdx.x mod HV, so the channel permutation and the row
+// offsets are computed once. While tile k is reduced, updated, re-encoded
+// and stored, the packed bytes of the next one or two tiles are already in
+// flight into registers.
 //
 // Tiles are read and written through buffer resources whose size is the tile
 // size, or 0 for a padded request: then the loads return zeros and the
@@ -19,7 +20,7 @@
 // Per tile: thread t (row group rg = t / 8, column group cg = t % 8) holds
 // rows rg, rg+32, rg+64, rg+96, columns 16 cg .. 16 cg + 15. Row 0 of a thread
 // can be in the high (bf16) tier, the others are low (uint8) rows.
-// Operands are staged once per tile by threads t < 128 (one tile row each):
+// Operands are staged once per tile by two waves (one tile row per thread):
 // k~, q~, the row decay a~ and v, in LDS; q~ . k~ is reduced there too.
 #include <type_traits>
 
@@ -109,6 +110,7 @@ struct OpsRegs {
 // o transformed back before it is written. Eq. (1) commutes with the
 // transform: S H = Lambda S_prev H + beta k (H delta)^T, delta_H = H v - (S_bar
 // H)^T k, o = H (S H)^T q.
+//
 // DEPTH = tiles of packed bytes prefetched into registers. DEPTH = 1 holds
 // one raw tile set (168 VGPRs, three workgroups per CU): the shorter
 // prologue and the larger resident front win on short streams. DEPTH = 2
