@@ -622,6 +622,20 @@ def main():
                     "reduction_vs_fp32_pct": round(100 * (1 - head["bits_per_value"] / 32), 2)},
     }
     out.update(extra)
+    # the paper's own figures (section 1 and section 6, an unnamed NVIDIA GPU
+    # running its CUDA executor in SGLang), reported beside ours as context
+    out["paper_context"] = {
+        "state_update_speedup_vs_fp32_state": {"gdn": "1.46-1.65x", "kda": "1.81-2.01x",
+                                               "batch": "32-256", "format": "INT8+H32, 16 FP16 rows"},
+        "storage_cut_pct": 69.1,
+        "tpot_gain_pct_bs256": {"gdn": 10.9, "kda": 9.6},
+        "hardware": "unnamed NVIDIA GPU (CUDA executor in SGLang)",
+    }
+    if "baselines_gdn" in extra and "paper_tiers_gdn" in extra:
+        fp = extra["baselines_gdn"]["fp32_state"]["kernel_us"]
+        out["paper_context"]["this_build_gdn_speedup_vs_fp32_state"] = {
+            "default_tiers": round(fp / head["kernel_us"], 2),
+            "paper_tiers_int8_h32": round(fp / extra["paper_tiers_gdn"]["int8_h32"]["kernel_us"], 2)}
     print(json.dumps(out), flush=True)
 
 
