@@ -305,10 +305,15 @@ damp_status update(bool kda, const damp_pool* pool, int32_t layer, const int32_t
   hipStream_t s = as_stream(stream);
   // the persistent kernel numbers the B * HV tiles with 32-bit integers
   const bool tiles_fit = static_cast<int64_t>(B) * p.HV <= INT32_MAX;
-  const bool paper = layout_is_paper(&pool->layout);
-  if ((layout_is_default(&pool->layout) || paper) && D == 128 && p.k_hi <= 32 && tiles_fit) {
-    if (!launch_stream128(kda, paper, p, B, s))
-      return fail(DAMP_ERR_HIP, "%s: occupancy query failed", name);
+  const int codec = layout_codec(&pool->layout);
+  const int sfmt = codec == kCodecDefault ? kMixed
+                   : codec == kCodecPaper ? kPaper
+                   : codec == kCodecInt4  ? kInt4
+                   : codec == kCodecFp8   ? kFp8
+                                          : -1;
+  if (sfmt >= 0 && D == 128 && p.k_hi <= 32 && tiles_fit) {
+    if (!launch_stream128(kda, sfmt, p, B, s))
+      return fail(DAMP_ERR_HIP, "%s: occupancy query or launch failed", name);
     return check_launch(name);
   }
   if (kda) launch_codec<true>(layout_codec(&pool->layout), D, p, B, s);

@@ -28,8 +28,10 @@ struct UpdateParams {
   int32_t had;  // block-32 Hadamard on the low tier (paper tiers only)
 };
 
-// The streaming kernel for d = 128 mixed tiles with k_hi <= 32 (update_stream.hip).
-// Returns false if it did not launch (a HIP query failed).
-bool launch_stream128(bool kda, bool paper, const UpdateParams& p, int B, hipStream_t stream);
+// The streaming kernel for d = 128 mixed tiles with k_hi <= 32 (update_stream.hip)
+// in the default tiers (fmt = kMixed) or a group format of App. A.1's table
+// (kPaper, kInt4, kFp8). Returns false if it did not launch (the occupancy
+// query or the launch failed).
+bool launch_stream128(bool kda, int fmt, const UpdateParams& p, int B, hipStream_t stream);
 
 }  // namespace damp

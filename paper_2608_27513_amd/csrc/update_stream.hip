@@ -1,6 +1,7 @@
 // Persistent, software-pipelined decode-step update for d_k = d_v = 128 mixed
 // tiles with at most 32 high-precision rows (section 3.1 Eq. (1)-(2);
-// section 3.2 Eq. (3); section 5.2 and App. A.5).
+// section 3.2 Eq. (3); section 5.2 and App. A.5), in the default tiers or
+// the UINT8, UINT4 and FP8 rows of App. A.1's format table.
 //
 // The state update moves ~2.4 bytes per state value and does ~11 VALU
 // instructions per value, so on MI355X the memory time and the VALU time are
@@ -19,7 +20,8 @@
 //
 // Per tile: thread t (row group rg = t / 8, column group cg = t % 8) holds
 // rows rg, rg+32, rg+64, rg+96, columns 16 cg .. 16 cg + 15. Row 0 of a thread
-// can be in the high (bf16) tier, the others are low (uint8) rows.
+// can be in the high (16-bit) tier, the others are low rows (codes of one
+// byte, or half a byte for UINT4).
 // Operands are staged once per tile by two waves (one tile row per thread):
 // k~, q~, the row decay a~ and v, in LDS; q~ . k~ is reduced there too.
 #include <type_traits>
@@ -85,16 +87,61 @@ __device__ __forceinline__ float fold8(float a, float b, bool upper) {
                                                         true));
 }
 
-// Packed bytes of one tile as loaded by one thread: its four row slices
-// (16 bytes each), the second half of a 16-bit row slot 0, and the metadata
-// of one row of its wave: the (s, z) pair of the default tiers (8 bytes) or
-// the four FP16 (s, z) words of the paper's groups (16 bytes).
+// Packed bytes of one tile as loaded by one thread: row slot 0 (the first
+// 16 bytes of a 16-bit row slice, or its codes: 16 bytes, UINT4 8 in .xy),
+// the codes of slots 1..3 (16 bytes, UINT4 8), the second half of a 16-bit
+// row slot 0, and the metadata of one row of its wave: the (s, z) pair of the
+// default tiers (8 bytes) or the four words of its groups of 32 (16 bytes).
 template <int FMT>
 struct RawSetT {
-  u32x4 ra[4];
+  using Codes = typename std::conditional<FMT == kInt4, u32x2, u32x4>::type;
+  u32x4 ra0;
+  Codes rc[3];
   u32x4 rb0 = u32x4{0u, 0u, 0u, 0u};
-  typename std::conditional<FMT == kPaper, u32x4, u32x2>::type rm;
+  typename std::conditional<FMT == kMixed, u32x2, u32x4>::type rm;
 };
+
+// Sixteen low-tier values of one row slice from their codes: A c + B0 for
+// the integer codes (UINT8; UINT4 nibble j of word k is value 8 k + j), A c
+// for E4M3 (B0 unused). A and B0 fold the decay into the dequantization.
+template <int FMT, typename W>
+__device__ __forceinline__ void decode16(const W& w, float A, float B0, float (&x)[16]) {
+  if constexpr (FMT == kInt4) {
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      uint32_t ev = w[k] & 0x0f0f0f0fu, od = (w[k] >> 4) & 0x0f0f0f0fu;
+      // opaque to the optimizer, which would otherwise extract each nibble
+      // with its own bit-field instruction instead of v_cvt_f32_ubyte{m}
+      asm("" : "+v"(ev), "+v"(od));
+      x[8 * k + 0] = fmaf(A, ubyte<0>(ev), B0);
+      x[8 * k + 1] = fmaf(A, ubyte<0>(od), B0);
+      x[8 * k + 2] = fmaf(A, ubyte<1>(ev), B0);
+      x[8 * k + 3] = fmaf(A, ubyte<1>(od), B0);
+      x[8 * k + 4] = fmaf(A, ubyte<2>(ev), B0);
+      x[8 * k + 5] = fmaf(A, ubyte<2>(od), B0);
+      x[8 * k + 6] = fmaf(A, ubyte<3>(ev), B0);
+      x[8 * k + 7] = fmaf(A, ubyte<3>(od), B0);
+    }
+  } else if constexpr (FMT == kFp8) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const auto lo = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w[k]), false);
+      const auto hi = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w[k]), true);
+      x[4 * k + 0] = A * lo[0];
+      x[4 * k + 1] = A * lo[1];
+      x[4 * k + 2] = A * hi[0];
+      x[4 * k + 3] = A * hi[1];
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      x[4 * k + 0] = fmaf(A, ubyte<0>(w[k]), B0);
+      x[4 * k + 1] = fmaf(A, ubyte<1>(w[k]), B0);
+      x[4 * k + 2] = fmaf(A, ubyte<2>(w[k]), B0);
+      x[4 * k + 3] = fmaf(A, ubyte<3>(w[k]), B0);
+    }
+  }
+}
 
 // Operands of one tile as loaded by threads t < 128 (raw bf16 bits).
 struct OpsRegs {
@@ -102,8 +149,11 @@ struct OpsRegs {
 };
 
 // FMT = kMixed: the default tiers (BF16 high rows, one fp32 (s, z) per low
-// row). FMT = kPaper: the paper's tiers (FP16 high rows, FP16 (s, z) per group
-// of 32). With the block-32 transform (p.had) the recurrence runs in the
+// row). The group formats of App. A.1's table, each with FP16 high rows and
+// one 4-byte word per group of 32 low values: FMT = kPaper (UINT8 codes, FP16
+// (s, z)), kInt4 (UINT4 codes, FP16 (s, z)), kFp8 (E4M3 codes, one fp32 scale
+// of Eq. (16)). With the block-32 transform (p.had; UINT8 and UINT4 only) the
+// recurrence runs in the
 // transformed domain: H is symmetric and orthonormal, so a low row is used as
 // stored (s (c - z) of the transformed values) and only the FP16 rows are
 // transformed, on load and before the store; v is transformed on staging and
@@ -119,8 +169,12 @@ template <bool KDA, int FMT, int DEPTH>
 __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
     const UpdateParams p, const int ntiles, const int tile_bytes) {
   constexpr int D = 128, RG = 32, RPT = 4, CPT = 16, TPR = 8;
-  constexpr bool kP = FMT == kPaper;
+  constexpr bool kP = FMT != kMixed;  // a group format: FP16 rows, 16 metadata bytes per row
+  constexpr bool kNib = FMT == kInt4;
+  constexpr int kCodeRow = kNib ? D / 2 : D;  // code bytes per low row
+  constexpr int kSlice = kNib ? 8 : 16;       // code bytes per row slice
   using RawSet = RawSetT<FMT>;
+  using Codes = typename RawSet::Codes;
   constexpr int kDrop = 0x40000000;  // buffer offset past any tile: the store is dropped
   // Per-wave partial column sums of k~ . S_bar (index c) and q~ . S_bar
   // (index D + c), in the slot order described at the reduction below;
@@ -145,7 +199,7 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
   // exchange between the lane layout and whole 1 KB loads and stores.
   __shared__ u32x4 hsh[4][2 * 64];
   __shared__ float osh[D];  // o of the tile (output wave), staged for one whole-row store
-  const bool had = kP && p.had != 0;
+  const bool had = (FMT == kPaper || FMT == kInt4) && p.had != 0;
 
   const int t = threadIdx.x;
   const int lane = t & 63;
@@ -161,7 +215,7 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
   const int k_hi = p.k_hi;
   const bool hi0 = rg < k_hi;  // row slot 0 of this thread is in the bf16 tier
   const int lo0 = k_hi * D * 2;
-  const int meta0 = lo0 + (D - k_hi) * D;
+  const int meta0 = lo0 + (D - k_hi) * kCodeRow;
   constexpr int kMetaRow = kP ? 16 : 8;  // metadata bytes per low row
   const int o_esize = p.o_bf16 ? 2 : 4;
   // slot ids are read-only here: scalar loads through the constant address space
@@ -180,10 +234,10 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
   // whole 1 KB blocks instead, lane l taking bytes 16 l of each; the rows
   // reach the lane layout through the wave's LDS slice (stage_meta).
   const int off_a0 = wave_hi ? 2048 * wave + 16 * lane
-                             : (hi0 ? (rg * D + col0) * 2 : lo0 + (rg - k_hi) * D + col0);
+                             : (hi0 ? (rg * D + col0) * 2 : lo0 + (rg - k_hi) * kCodeRow + cg * kSlice);
   const int off_b0 = wave_hi ? off_a0 + 1024 : off_a0 + 16;
-  const int off_a1 = lo0 + (rg + RG - k_hi) * D + col0;
-  constexpr int kStepA = RG * D;
+  const int off_a1 = lo0 + (rg + RG - k_hi) * kCodeRow + cg * kSlice;
+  constexpr int kStepA = RG * kCodeRow;
   const int st_b0 = hi0 ? off_b0 : kDrop;  // second half of a 16-bit row
   // The metadata of the wave's 32 rows moves with one 8-byte access per
   // lane: lane l < 32 handles row 8 wave + (l & 7) + 32 (l >> 3). Rows of
@@ -272,10 +326,17 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
     if (part == 0) {
       if constexpr (kP) rs.rm = ld16(r, off_m);
       else rs.rm = ld8(r, off_m);
-      rs.ra[0] = ld16(r, off_a0);
+      if (kNib && wave_lo) {
+        const u32x2 c = ld8(r, off_a0);
+        rs.ra0 = __builtin_shufflevector(c, c, 0, 1, -1, -1);
+      } else {
+        rs.ra0 = ld16(r, off_a0);
+      }
       if (!wave_lo) rs.rb0 = ld16(r, off_b0);
+    } else if constexpr (kNib) {
+      rs.rc[part - 1] = ld8(r, off_a1, (part - 1) * kStepA);
     } else {
-      rs.ra[part] = ld16(r, off_a1, (part - 1) * kStepA);
+      rs.rc[part - 1] = ld16(r, off_a1, (part - 1) * kStepA);
     }
   };
   auto issue_raw = [&](RawSet& rs, __amdgpu_buffer_rsrc_t r) {
@@ -291,12 +352,12 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
       else msh[wave][lane] = make_float2(__uint_as_float(rs.rm.x), __uint_as_float(rs.rm.y));
     }
     if (wave_hi) {
-      hsh[wave][lane] = rs.ra[0];
+      hsh[wave][lane] = rs.ra0;
       hsh[wave][64 + lane] = rs.rb0;
     }
     wave_sync();
     if (wave_hi) {
-      rs.ra[0] = hsh[wave][2 * lane];
+      rs.ra0 = hsh[wave][2 * lane];
       rs.rb0 = hsh[wave][2 * lane + 1];
     }
   };
@@ -355,26 +416,36 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
       qq[i] = o4.y;
       aa[i] = KDA ? o4.z : alpha;
     }
-    float2 sz[RPT];
+    // per row slot: the dequantization of this lane's slice, A c + B0 (or A c
+    // for E4M3), with the decay folded in
+    float dA[RPT], dB[RPT];
 #pragma unroll
     for (int i = 0; i < RPT; ++i) {
-      if constexpr (kP) {  // this lane's group: FP16 (s, z) in one word
+      if constexpr (kP) {  // this lane's group: one word
         const uint32_t m = reinterpret_cast<const uint32_t*>(&mshp[wave][0][0])[(rgw + 8 * i) * 4 +
                                                                                (cg >> 1)];
-        sz[i] = make_float2(f16_lo(m), f16_hi(m));
+        if constexpr (FMT == kFp8) {
+          dA[i] = aa[i] * __uint_as_float(m);
+          dB[i] = 0.0f;
+        } else {
+          dA[i] = aa[i] * f16_lo(m);
+          dB[i] = -dA[i] * f16_hi(m);
+        }
       } else {
-        sz[i] = msh[wave][rgw + 8 * i];
+        const float2 sz = msh[wave][rgw + 8 * i];
+        dA[i] = aa[i] * sz.x;
+        dB[i] = -dA[i] * sz.y;
       }
     }
     float x[RPT][CPT];
-    const u32x4* ra = cur.ra;
+    const u32x4 ra0 = cur.ra0;
     if (hi0) {
       if constexpr (kP) {  // FP16 rows, into the transformed domain with had
         const float a0 = aa[0] * (had ? kInvSqrt32 : 1.0f);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          x[0][2 * j] = a0 * f16_lo(ra[0][j]);
-          x[0][2 * j + 1] = a0 * f16_hi(ra[0][j]);
+          x[0][2 * j] = a0 * f16_lo(ra0[j]);
+          x[0][2 * j + 1] = a0 * f16_hi(ra0[j]);
           x[0][8 + 2 * j] = a0 * f16_lo(cur.rb0[j]);
           x[0][8 + 2 * j + 1] = a0 * f16_hi(cur.rb0[j]);
         }
@@ -382,35 +453,19 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
       } else {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          x[0][2 * j] = aa[0] * bf16_lo(ra[0][j]);
-          x[0][2 * j + 1] = aa[0] * bf16_hi(ra[0][j]);
+          x[0][2 * j] = aa[0] * bf16_lo(ra0[j]);
+          x[0][2 * j + 1] = aa[0] * bf16_hi(ra0[j]);
           x[0][8 + 2 * j] = aa[0] * bf16_lo(cur.rb0[j]);
           x[0][8 + 2 * j + 1] = aa[0] * bf16_hi(cur.rb0[j]);
         }
       }
+    } else if constexpr (kNib) {
+      decode16<FMT>(u32x2{ra0.x, ra0.y}, dA[0], dB[0], x[0]);
     } else {
-      const float A = aa[0] * sz[0].x;
-      const float B0 = -A * sz[0].y;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        x[0][4 * j + 0] = fmaf(A, ubyte<0>(ra[0][j]), B0);
-        x[0][4 * j + 1] = fmaf(A, ubyte<1>(ra[0][j]), B0);
-        x[0][4 * j + 2] = fmaf(A, ubyte<2>(ra[0][j]), B0);
-        x[0][4 * j + 3] = fmaf(A, ubyte<3>(ra[0][j]), B0);
-      }
+      decode16<FMT>(ra0, dA[0], dB[0], x[0]);
     }
 #pragma unroll
-    for (int i = 1; i < RPT; ++i) {
-      const float A = aa[i] * sz[i].x;
-      const float B0 = -A * sz[i].y;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        x[i][4 * j + 0] = fmaf(A, ubyte<0>(ra[i][j]), B0);
-        x[i][4 * j + 1] = fmaf(A, ubyte<1>(ra[i][j]), B0);
-        x[i][4 * j + 2] = fmaf(A, ubyte<2>(ra[i][j]), B0);
-        x[i][4 * j + 3] = fmaf(A, ubyte<3>(ra[i][j]), B0);
-      }
-    }
+    for (int i = 1; i < RPT; ++i) decode16<FMT>(cur.rc[i - 1], dA[i], dB[i], x[i]);
     // the dequantized tile must exist before the next tile's loads are
     // issued, so that the waits for this tile's bytes precede the prefetch
 #pragma unroll
@@ -574,8 +629,10 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
 #pragma unroll
       for (int j = 0; j < CPT; ++j) x[i][j] = fmaf(bk, dl[j], x[i][j]);
     }
-    u32x4 wa[RPT], wb0;
-    float2 wm[RPT];
+    u32x4 wa0, wb0;
+    Codes wc[RPT];
+    float2 wm[RPT];    // default tiers: the row's (s, z)
+    uint32_t wg[RPT];  // group formats: the word of this lane's group
 #pragma unroll
     for (int i = 0; i < RPT; ++i) {
       if (i == 0 && hi0) {
@@ -587,44 +644,84 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
           }
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            wa[0][j] = pack_f16x2(x[0][2 * j], x[0][2 * j + 1]);
+            wa0[j] = pack_f16x2(x[0][2 * j], x[0][2 * j + 1]);
             wb0[j] = pack_f16x2(x[0][8 + 2 * j], x[0][8 + 2 * j + 1]);
           }
         } else {
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            wa[0][j] = pack_bf16x2(x[0][2 * j], x[0][2 * j + 1]);
+            wa0[j] = pack_bf16x2(x[0][2 * j], x[0][2 * j + 1]);
             wb0[j] = pack_bf16x2(x[0][8 + 2 * j], x[0][8 + 2 * j + 1]);
           }
         }
         wm[0] = make_float2(0.0f, 0.0f);
+        wg[0] = 0u;
         continue;
       }
-      float mn = x[i][0], mx = x[i][0];
+      if constexpr (FMT == kFp8) {
+        // Eq. (16): s = max |x| / 448 over the lane pair's group of 32
+        float amax = fabsf(x[i][0]);
 #pragma unroll
-      for (int j = 1; j < CPT; ++j) {
-        mn = fminf(mn, x[i][j]);
-        mx = fmaxf(mx, x[i][j]);
-      }
-      float s, z, inv;
-      if constexpr (kP) {  // the lane pair's group of 32, FP16 (s, z)
-        group_qparams_f16(mn, mx, s, z, inv);
+        for (int j = 1; j < CPT; ++j) amax = fmaxf(amax, fabsf(x[i][j]));
+        amax = fmaxf(amax, dpp_mov<0xb1>(amax));
+        const float s = __fdiv_rn(amax > 1e-10f ? amax : 1e-10f, 448.0f);
+        const float inv = refined_rcp(s);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const uint32_t lo = cvt_e4m3x2<false>(x[i][4 * k] * inv, x[i][4 * k + 1] * inv, 0u);
+          wc[i][k] = cvt_e4m3x2<true>(x[i][4 * k + 2] * inv, x[i][4 * k + 3] * inv, lo);
+        }
+        wg[i] = __float_as_uint(s);
       } else {
-        group_minmax<TPR>(mn, mx);
-        row_qparams(mn, mx, s, z, inv);
-      }
+        float mn = x[i][0], mx = x[i][0];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        // v_cvt_pk_u8_f32 rounds to nearest even and saturates to [0, 255]
-        uint32_t c = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(x[i][4 * j], inv, z), 0, 0u);
-        c = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(x[i][4 * j + 1], inv, z), 1, c);
-        c = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(x[i][4 * j + 2], inv, z), 2, c);
-        wa[i][j] = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(x[i][4 * j + 3], inv, z), 3, c);
+        for (int j = 1; j < CPT; ++j) {
+          mn = fminf(mn, x[i][j]);
+          mx = fmaxf(mx, x[i][j]);
+        }
+        float s, z, inv;
+        if constexpr (kP) {  // the lane pair's group of 32, FP16 (s, z)
+          group_qparams_f16<kNib ? 15 : 255>(mn, mx, s, z, inv);
+          wg[i] = pack_f16x2(s, z);
+        } else {
+          group_minmax<TPR>(mn, mx);
+          row_qparams(mn, mx, s, z, inv);
+          wm[i] = make_float2(s, z);
+        }
+        if constexpr (kNib) {
+          // codes clamped to [0, 15] before the conversion (it rounds to
+          // nearest even), then values 2 m and 2 m + 1 into the nibbles of byte m
+#pragma unroll
+          for (int k = 0; k < 2; ++k) {
+            uint32_t ev = 0u, od = 0u;
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+              const float ce = __builtin_amdgcn_fmed3f(fmaf(x[i][8 * k + 2 * m], inv, z), 0.0f, 15.0f);
+              const float co =
+                  __builtin_amdgcn_fmed3f(fmaf(x[i][8 * k + 2 * m + 1], inv, z), 0.0f, 15.0f);
+              ev = __builtin_amdgcn_cvt_pk_u8_f32(ce, m, ev);
+              od = __builtin_amdgcn_cvt_pk_u8_f32(co, m, od);
+            }
+            wc[i][k] = ev | (od << 4);
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            // v_cvt_pk_u8_f32 rounds to nearest even and saturates to [0, 255]
+            uint32_t c = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(x[i][4 * j], inv, z), 0, 0u);
+            c = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(x[i][4 * j + 1], inv, z), 1, c);
+            c = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(x[i][4 * j + 2], inv, z), 2, c);
+            wc[i][j] = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(x[i][4 * j + 3], inv, z), 3, c);
+          }
+        }
       }
-      wm[i] = make_float2(s, z);
-      if (i == 0) wb0 = u32x4{0u, 0u, 0u, 0u};
+      if (i == 0) {
+        if constexpr (kNib) wa0 = __builtin_shufflevector(wc[0], wc[0], 0, 1, -1, -1);
+        else wa0 = wc[0];
+        wb0 = u32x4{0u, 0u, 0u, 0u};
+      }
     }
-    // metadata of the wave's rows: the paper tiers' 16 bytes per row go
+    // metadata of the wave's rows: the group formats' 16 bytes per row go
     // through the wave's LDS slice (a wave's 8 consecutive rows make a whole
     // 128-byte line); the default tiers' (s, z) into the tile's table, stored
     // after the next barrier (store_prev_meta)
@@ -632,8 +729,7 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
       if ((cg & 1) == 0) {
 #pragma unroll
         for (int i = 0; i < RPT; ++i)
-          reinterpret_cast<uint32_t*>(&mshp[wave][1][0])[(rgw + 8 * i) * 4 + (cg >> 1)] =
-              pack_f16x2(wm[i].x, wm[i].y);
+          reinterpret_cast<uint32_t*>(&mshp[wave][1][0])[(rgw + 8 * i) * 4 + (cg >> 1)] = wg[i];
       }
     } else if (cg == 0) {
 #pragma unroll
@@ -641,7 +737,7 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
     }
     // the high rows of a wave_hi wave as two whole 1 KB blocks
     if (wave_hi) {
-      hsh[wave][2 * lane] = wa[0];
+      hsh[wave][2 * lane] = wa0;
       hsh[wave][2 * lane + 1] = wb0;
     }
     wave_sync();
@@ -650,12 +746,21 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
     if (wave_hi) {
       st16(hsh[wave][lane], rs_cur, off_a0);
       st16(hsh[wave][64 + lane], rs_cur, off_b0);
+    } else if constexpr (kNib) {  // 8 bytes of codes, or 32 of a 16-bit row
+      st8(u32x2{wa0.x, wa0.y}, rs_cur, off_a0);
+      if (!wave_lo) {
+        st8(u32x2{wa0.z, wa0.w}, rs_cur, hi0 ? off_a0 + 8 : kDrop);
+        st16(wb0, rs_cur, st_b0);
+      }
     } else {
-      st16(wa[0], rs_cur, off_a0);
+      st16(wa0, rs_cur, off_a0);
       if (!wave_lo) st16(wb0, rs_cur, st_b0);
     }
 #pragma unroll
-    for (int i = 1; i < RPT; ++i) st16(wa[i], rs_cur, off_a1, (i - 1) * kStepA);
+    for (int i = 1; i < RPT; ++i) {
+      if constexpr (kNib) st8(wc[i], rs_cur, off_a1, (i - 1) * kStepA);
+      else st16(wc[i], rs_cur, off_a1, (i - 1) * kStepA);
+    }
     if constexpr (kP) st16(mshp[wave][1][lane & 31], rs_cur, st_m);
     if (has_next) stage_meta(oth);
 
@@ -703,16 +808,31 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
 
 // The instantiations that launch_stream128 chooses from, and their
 // resident workgroups per CU (queried once per device).
-enum StreamKernel { kGdnMixed1, kGdnMixed2, kKdaMixed1, kKdaMixed2, kGdnPaper2, kKdaPaper2, kNumStream };
+enum StreamKernel {
+  kGdnMixed1, kGdnMixed2, kKdaMixed1, kKdaMixed2,
+  kGdnPaper2, kKdaPaper2, kGdnInt41, kGdnInt42, kKdaInt41, kKdaInt42,
+  kGdnFp82, kKdaFp82, kNumStream
+};
+
+template <bool KDA, int FMT, int DEPTH>
+const void* kernel_ptr() {
+  return reinterpret_cast<const void*>(update_stream128<KDA, FMT, DEPTH>);
+}
 
 const void* stream_kernel(int which) {
   switch (which) {
-    case kGdnMixed1: return reinterpret_cast<const void*>(update_stream128<false, kMixed, 1>);
-    case kGdnMixed2: return reinterpret_cast<const void*>(update_stream128<false, kMixed, 2>);
-    case kKdaMixed1: return reinterpret_cast<const void*>(update_stream128<true, kMixed, 1>);
-    case kKdaMixed2: return reinterpret_cast<const void*>(update_stream128<true, kMixed, 2>);
-    case kGdnPaper2: return reinterpret_cast<const void*>(update_stream128<false, kPaper, 2>);
-    default: return reinterpret_cast<const void*>(update_stream128<true, kPaper, 2>);
+    case kGdnMixed1: return kernel_ptr<false, kMixed, 1>();
+    case kGdnMixed2: return kernel_ptr<false, kMixed, 2>();
+    case kKdaMixed1: return kernel_ptr<true, kMixed, 1>();
+    case kKdaMixed2: return kernel_ptr<true, kMixed, 2>();
+    case kGdnPaper2: return kernel_ptr<false, kPaper, 2>();
+    case kKdaPaper2: return kernel_ptr<true, kPaper, 2>();
+    case kGdnInt41: return kernel_ptr<false, kInt4, 1>();
+    case kGdnInt42: return kernel_ptr<false, kInt4, 2>();
+    case kKdaInt41: return kernel_ptr<true, kInt4, 1>();
+    case kKdaInt42: return kernel_ptr<true, kInt4, 2>();
+    case kGdnFp82: return kernel_ptr<false, kFp8, 2>();
+    default: return kernel_ptr<true, kFp8, 2>();
   }
 }
 
@@ -744,16 +864,22 @@ bool occupancy(int which, int& cus, int& per_cu) {
 
 }  // namespace
 
-bool launch_stream128(bool kda, bool paper, const UpdateParams& p, int B, hipStream_t stream) {
+bool launch_stream128(bool kda, int fmt, const UpdateParams& p, int B, hipStream_t stream) {
   const int ntiles = B * p.HV;
-  int which = paper ? (kda ? kKdaPaper2 : kGdnPaper2) : (kda ? kKdaMixed2 : kGdnMixed2);
+  int which;
+  switch (fmt) {
+    case kPaper: which = kda ? kKdaPaper2 : kGdnPaper2; break;
+    case kInt4: which = kda ? kKdaInt42 : kGdnInt42; break;
+    case kFp8: which = kda ? kKdaFp82 : kGdnFp82; break;
+    default: which = kda ? kKdaMixed2 : kGdnMixed2; break;
+  }
   int cus = 0, per_cu = 0;
   if (!occupancy(which, cus, per_cu)) return false;
-  // The default tiers prefetch one tile with three workgroups per CU when
-  // each of the two-per-CU workgroups would stream at most 16 tiles (the
-  // batch of 256 requests x 32 heads), two tiles otherwise.
-  if (!paper && static_cast<long>(ntiles) <= 16L * cus * per_cu) {
-    which = kda ? kKdaMixed1 : kGdnMixed1;
+  // The default tiers and UINT4 prefetch one tile with three workgroups per
+  // CU when each of the two-per-CU workgroups would stream at most 16 tiles
+  // (the batch of 256 requests x 32 heads), two tiles otherwise.
+  if ((fmt == kMixed || fmt == kInt4) && static_cast<long>(ntiles) <= 16L * cus * per_cu) {
+    which = fmt == kInt4 ? (kda ? kKdaInt41 : kGdnInt41) : (kda ? kKdaMixed1 : kGdnMixed1);
     if (!occupancy(which, cus, per_cu)) return false;
   }
   // resident workgroups, rounded down to a multiple of HV (at least HV)
@@ -762,30 +888,14 @@ bool launch_stream128(bool kda, bool paper, const UpdateParams& p, int B, hipStr
   if (per_head < 1) per_head = 1;
   if (per_head > B) per_head = B;
   const int grid = static_cast<int>(per_head * p.HV);
-  const int tile_bytes =
-      p.k_hi * 128 * 2 + (128 - p.k_hi) * 128 + (128 - p.k_hi) * (paper ? 16 : 8);
-  const dim3 g(grid), blk(256);
-  switch (which) {
-    case kGdnMixed1:
-      hipLaunchKernelGGL((update_stream128<false, kMixed, 1>), g, blk, 0, stream, p, ntiles, tile_bytes);
-      break;
-    case kGdnMixed2:
-      hipLaunchKernelGGL((update_stream128<false, kMixed, 2>), g, blk, 0, stream, p, ntiles, tile_bytes);
-      break;
-    case kKdaMixed1:
-      hipLaunchKernelGGL((update_stream128<true, kMixed, 1>), g, blk, 0, stream, p, ntiles, tile_bytes);
-      break;
-    case kKdaMixed2:
-      hipLaunchKernelGGL((update_stream128<true, kMixed, 2>), g, blk, 0, stream, p, ntiles, tile_bytes);
-      break;
-    case kGdnPaper2:
-      hipLaunchKernelGGL((update_stream128<false, kPaper, 2>), g, blk, 0, stream, p, ntiles, tile_bytes);
-      break;
-    default:
-      hipLaunchKernelGGL((update_stream128<true, kPaper, 2>), g, blk, 0, stream, p, ntiles, tile_bytes);
-      break;
-  }
-  return true;
+  const int lo_rows = 128 - p.k_hi;
+  const int tile_bytes = p.k_hi * 128 * 2 + lo_rows * (fmt == kInt4 ? 64 : 128) +
+                         lo_rows * (fmt == kMixed ? 8 : 16);
+  UpdateParams pa = p;
+  int nt = ntiles, tb = tile_bytes;
+  void* args[] = {&pa, &nt, &tb};
+  return hipLaunchKernel(stream_kernel(which), dim3(grid), dim3(256), args, 0, stream) ==
+         hipSuccess;
 }
 
 }  // namespace damp

@@ -131,3 +131,79 @@ def test_prefill_parity(name):
     stats = compare_tiles(gpool.buffer.cpu().numpy(), ref, f"prefill {name}", s16_exact_min=0.99)
     _say(f"  o rel-L2 {err:.2e}  {stats}")
     assert err <= 1e-4
+
+
+STREAM_FORMATS = ["int4", "int4_h32", "fp8"]
+
+
+@pytest.mark.parametrize("name", STREAM_FORMATS)
+@pytest.mark.parametrize("kda,k_hi", [(False, 16), (True, 12), (False, 0), (True, 32),
+                                      (False, 8)])
+def test_many_tiles_per_workgroup(name, kda, k_hi):
+    """d = 128 (the persistent streaming kernel) with more requests than
+    resident workgroups, so each workgroup streams several tiles; slots in
+    random order, some padded or out of range (o = 0, their tiles untouched).
+    k_hi = 12 puts 16-bit and code rows in one wave, 0 and 32 leave only one
+    kind of row in slot 0."""
+    fmt = FORMATS[name]
+    d, HV, B = 128, 4, 300
+    HK = HV if kda else 2
+    _say(f"format many tiles {name} kda={kda} k_hi={k_hi}")
+    seed = 1400 + 3 * kda + k_hi
+    n_slots = B + 40
+    slots = inputs.slot_order(seed, n_slots, B)
+    slots[::37] = -1
+    slots[5] = n_slots  # out of range
+    perm = inputs.random_perms(seed, HV, d)
+    S = _states(seed, B, HV, d)
+    ref = orc.Pool(orc.KIND_MIXED, d, d, k_hi, 1, n_slots, HV, fmt=fmt)
+    live = (slots >= 0) & (slots < n_slots)
+    orc.pack(ref, 0, slots[live], S[live], perm)
+    gpool = gpu_pool_from(ref, D)
+    inp = inputs.step(inputs.decode_inputs(seed, 1, B, HK, HV, d, kda=kda), 0)
+    x = dev_inputs(inp)
+    o = torch.empty((B, HV, d), dtype=torch.float32, device="cuda")
+    fn = D.damp_state_update_kda if kda else D.damp_state_update_gdn
+    fn(gpool, 0, dev_i32(slots), x["q"], x["k"], x["v"], x["g"], x["beta"], perm=dev_u8(perm),
+       o=o)
+    o_ref = orc.update(ref, 0, slots, kda=kda, perm=perm, **inp)
+    torch.cuda.synchronize()
+    o_gpu = o.cpu().numpy()
+    assert np.all(o_gpu[~live] == 0) and np.all(o_ref[~live] == 0)
+    err = rel_l2(o_gpu, o_ref)
+    stats = compare_tiles(gpool.buffer.cpu().numpy(), ref, f"many tiles {name}")
+    _say(f"  o rel-L2 {err:.2e}  {stats}")
+    assert err <= 1e-4
+
+
+@pytest.mark.parametrize("name", STREAM_FORMATS)
+@pytest.mark.parametrize("kda", [False, True])
+def test_full_size_step(name, kda):
+    """The decode workload (B = 256, 32 value heads, d = 128, 16 FP16 rows)
+    in these formats, in the launch configuration of the benchmark; the
+    oracle runs the whole step, so every output and stored byte is compared."""
+    fmt = FORMATS[name]
+    B, HV, d, k_hi = 256, 32, 128, 16
+    HK = HV if kda else 16
+    seed = 1500 + kda
+    _say(f"format full-size {name} kda={kda}")
+    S = _states(seed, B, HV, d)
+    perm = inputs.random_perms(seed, HV, d)
+    slots = inputs.slot_order(seed, B, B)
+    ref = orc.Pool(orc.KIND_MIXED, d, d, k_hi, 1, B, HV, fmt=fmt)
+    orc.pack(ref, 0, slots, S, perm)
+    del S
+    gpool = gpu_pool_from(ref, D)
+    inp = inputs.step(inputs.decode_inputs(seed, 1, B, HK, HV, d, kda=kda), 0)
+    x = dev_inputs(inp)
+    o = torch.empty((B, HV, d), dtype=torch.float32, device="cuda")
+    fn = D.damp_state_update_kda if kda else D.damp_state_update_gdn
+    fn(gpool, 0, dev_i32(slots), x["q"], x["k"], x["v"], x["g"], x["beta"], perm=dev_u8(perm),
+       o=o)
+    torch.cuda.synchronize()
+    _say("  gpu step done; running the oracle")
+    o_ref = orc.update(ref, 0, slots, kda=kda, perm=perm, **inp)
+    err = rel_l2(o.cpu().numpy(), o_ref)
+    stats = compare_tiles(gpool.buffer.cpu().numpy(), ref, f"full-size {name}")
+    _say(f"  o rel-L2 {err:.2e}  {stats}")
+    assert err <= O_TOL_MIXED and err <= 1e-4
