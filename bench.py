@@ -321,6 +321,46 @@ def sweep(torch, D, inputs, steps: int, log=print):
     return out
 
 
+def tp_share(torch, D, inputs, steps: int, log=print):
+    """One GPU's share of an 8-way tensor-parallel deployment: B = 256 with 4
+    of the 32 value heads (and 2 of 16 key heads for GDN), d = 128, 16
+    high-precision rows, against the FP32 state: 1024 tiles, four per CU."""
+    out = []
+    d, HV, B = 128, 4, 256
+    for kda in (False, True):
+        HK = HV if kda else 2
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(8)
+        mu = torch.from_numpy(inputs.kda_mu(1, HV, d)).cuda() if kda else None
+        x = inputs.decode_inputs_device(gen, B, HK, HV, d, kda=kda, mu=mu)
+        perm = torch.from_numpy(inputs.random_perms(8, HV, d)).cuda()
+        S = torch.randn((B, HV, d, d), generator=gen, device="cuda") * 0.1
+        o = torch.empty((B, HV, d), dtype=torch.bfloat16, device="cuda")
+        for kind, k_hi in ((D.DAMP_STATE_FP32, 0), (D.DAMP_STATE_MIXED, 16)):
+            layout = D.damp_layout_init(d, d, k_hi, kind)
+            tb = D.damp_tile_bytes(layout)
+            rot = max(1, min(64, -(-(1 << 30) // (tb * B * HV))))
+            pool = D.Pool(layout, 1, B * rot, HV)
+            sets = [torch.arange(r * B, (r + 1) * B, dtype=torch.int32, device="cuda")
+                    for r in range(rot)]
+            for sl in sets:
+                D.damp_state_pack(pool, 0, sl, S, perm)
+            calls = [D.PreparedUpdate(kda, pool, 0, sl, x["q"], x["k"], x["v"], x["g"],
+                                      x["beta"], perm, 1.0, o) for sl in sets]
+            t = time_steps(torch, calls, 10, steps, prewarm_s=0.1)
+            nbytes = algorithmic_bytes(tb, B, HK, HV, d, kda, 2)
+            out.append(dict(model="KDA" if kda else "GDN", B=B, HK=HK, HV=HV,
+                            layout="fp32" if kind == D.DAMP_STATE_FP32 else "mixed", k_hi=k_hi,
+                            kernel_us=round(1e6 * t["mean_launch_s"], 2),
+                            GBs=round(nbytes / t["mean_launch_s"] / 1e9, 1)))
+            del pool, calls
+        del S
+        torch.cuda.empty_cache()
+    log("  TP=8 share: " + ", ".join(f"{r['model']} {r['layout']} {r['kernel_us']} us"
+                                      for r in out))
+    return out
+
+
 def multilayer(torch, D, inputs, steps: int, log=print):
     """48 GDN layers over one slot-indexed pool of 512 requests, 384 of them
     active in random non-contiguous order (32 value / 16 key heads, d = 128,
@@ -585,6 +625,7 @@ def main():
 
         if not args.no_sweep:
             extra["sweep"] = sweep(torch, D, inputs, 50, log=log)
+            extra["tp8_share"] = tp_share(torch, D, inputs, 100, log=log)
         if not args.no_multilayer:
             extra["multilayer_48"] = multilayer(torch, D, inputs, 64, log=log)
         extra["prefill_gdn"] = prefill_bench(torch, D, inputs, 10, log=log)

@@ -258,6 +258,39 @@ __device__ __forceinline__ void group_qparams_f16(float mn, float mx, float& s16
   inv = fmaf(fmaf(-rc, s16, 1.0f), rc, rc);
 }
 
+// group_qparams_f16 with both quotients from a hardware reciprocal refined
+// by one residual step (as row_qparams): the same s16, z16 and inv except
+// where a quotient's IEEE rounding differs in its last bit and that bit
+// moves the FP16 rounding of s or the integer rounding of -min / s (fp32
+// values within one ulp of such a boundary). The unrefined z quotient is
+// clamped first so that the residual step stays finite.
+template <int LEVELS = 255>
+__device__ __forceinline__ void group_qparams_f16_rcp(float mn, float mx, float& s16, float& z16,
+                                                      float& inv) {
+  constexpr float kL = static_cast<float>(LEVELS), kInvL = 1.0f / static_cast<float>(LEVELS);
+  mn = fminf(mn, dpp_mov<0xb1>(mn));
+  mx = fmaxf(mx, dpp_mov<0xb1>(mx));
+  const float r = mx - mn;
+  float s = r * kInvL;
+  s = fmaf(fmaf(-s, kL, r), kInvL, s);
+  if (!(s >= FLT_MIN)) {
+    const float a = fabsf(mn);
+    s = a * kInvL;
+    s = fmaf(fmaf(-s, kL, a), kInvL, s);
+    if (!(s >= FLT_MIN)) s = 1.0f;
+  }
+  s16 = round_f16(s);
+  if (!(s16 > 0.0f)) s16 = 5.9604644775390625e-08f;  // smallest positive FP16
+  if (s16 > 65504.0f) s16 = 65504.0f;
+  const float rc = __builtin_amdgcn_rcpf(s16);
+  inv = fmaf(fmaf(-rc, s16, 1.0f), rc, rc);
+  const float nm = -mn;
+  const float z0 = __builtin_amdgcn_fmed3f(nm * inv, -65536.0f, 65536.0f);
+  float zf = rintf(fmaf(fmaf(-z0, s16, nm), inv, z0));
+  zf = fminf(fmaxf(zf, -65504.0f), 65504.0f);
+  z16 = round_f16(zf);
+}
+
 // ------------------------------------------ small floating-point codes
 
 // The gfx950 conversions between fp32 and OCP E4M3 (bias 7, largest finite

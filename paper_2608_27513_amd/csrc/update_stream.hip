@@ -664,7 +664,10 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
 #pragma unroll
         for (int j = 1; j < CPT; ++j) amax = fmaxf(amax, fabsf(x[i][j]));
         amax = fmaxf(amax, dpp_mov<0xb1>(amax));
-        const float s = __fdiv_rn(amax > 1e-10f ? amax : 1e-10f, 448.0f);
+        // the quotient from a refined reciprocal (IEEE except in rare last-bit cases)
+        const float am = amax > 1e-10f ? amax : 1e-10f;
+        float s = am * (1.0f / 448.0f);
+        s = fmaf(fmaf(-s, 448.0f, am), 1.0f / 448.0f, s);
         const float inv = refined_rcp(s);
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
@@ -681,7 +684,7 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
         }
         float s, z, inv;
         if constexpr (kP) {  // the lane pair's group of 32, FP16 (s, z)
-          group_qparams_f16<kNib ? 15 : 255>(mn, mx, s, z, inv);
+          group_qparams_f16_rcp<kNib ? 15 : 255>(mn, mx, s, z, inv);
           wg[i] = pack_f16x2(s, z);
         } else {
           group_minmax<TPR>(mn, mx);
@@ -810,8 +813,8 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
 // resident workgroups per CU (queried once per device).
 enum StreamKernel {
   kGdnMixed1, kGdnMixed2, kKdaMixed1, kKdaMixed2,
-  kGdnPaper2, kKdaPaper2, kGdnInt41, kGdnInt42, kKdaInt41, kKdaInt42,
-  kGdnFp82, kKdaFp82, kNumStream
+  kGdnPaper2, kKdaPaper2, kGdnInt42, kKdaInt42, kGdnFp82, kKdaFp82,
+  kNumStream
 };
 
 template <bool KDA, int FMT, int DEPTH>
@@ -827,9 +830,7 @@ const void* stream_kernel(int which) {
     case kKdaMixed2: return kernel_ptr<true, kMixed, 2>();
     case kGdnPaper2: return kernel_ptr<false, kPaper, 2>();
     case kKdaPaper2: return kernel_ptr<true, kPaper, 2>();
-    case kGdnInt41: return kernel_ptr<false, kInt4, 1>();
     case kGdnInt42: return kernel_ptr<false, kInt4, 2>();
-    case kKdaInt41: return kernel_ptr<true, kInt4, 1>();
     case kKdaInt42: return kernel_ptr<true, kInt4, 2>();
     case kGdnFp82: return kernel_ptr<false, kFp8, 2>();
     default: return kernel_ptr<true, kFp8, 2>();
@@ -875,11 +876,12 @@ bool launch_stream128(bool kda, int fmt, const UpdateParams& p, int B, hipStream
   }
   int cus = 0, per_cu = 0;
   if (!occupancy(which, cus, per_cu)) return false;
-  // The default tiers and UINT4 prefetch one tile with three workgroups per
-  // CU when each of the two-per-CU workgroups would stream at most 16 tiles
-  // (the batch of 256 requests x 32 heads), two tiles otherwise.
-  if ((fmt == kMixed || fmt == kInt4) && static_cast<long>(ntiles) <= 16L * cus * per_cu) {
-    which = fmt == kInt4 ? (kda ? kKdaInt41 : kGdnInt41) : (kda ? kKdaMixed1 : kGdnMixed1);
+  // The default tiers prefetch one tile with three workgroups per CU when
+  // each of the two-per-CU workgroups would stream at most 16 tiles (the
+  // batch of 256 requests x 32 heads), two tiles otherwise. The group
+  // formats need more registers and always prefetch two.
+  if (fmt == kMixed && static_cast<long>(ntiles) <= 16L * cus * per_cu) {
+    which = kda ? kKdaMixed1 : kGdnMixed1;
     if (!occupancy(which, cus, per_cu)) return false;
   }
   // resident workgroups, rounded down to a multiple of HV (at least HV)
