@@ -182,11 +182,15 @@ __device__ __forceinline__ void row_qparams(float mn, float mx, float& s, float&
   const float r = mx - mn;
   float q = r * k255inv;
   q = fmaf(fmaf(-q, 255.0f, r), k255inv, q);
-  if (!(q >= FLT_MIN)) {
-    const float a = fabsf(mn);
-    q = a * k255inv;
-    q = fmaf(fmaf(-q, 255.0f, a), k255inv, q);
-    if (!(q >= FLT_MIN)) q = 1.0f;
+  // the fallback runs only in a wave that has such a row (a wave-uniform
+  // branch) rather than being evaluated and selected on every row
+  if (__builtin_expect(__builtin_amdgcn_ballot_w64(!(q >= FLT_MIN)) != 0, 0)) {
+    if (!(q >= FLT_MIN)) {
+      const float a = fabsf(mn);
+      q = a * k255inv;
+      q = fmaf(fmaf(-q, 255.0f, a), k255inv, q);
+      if (!(q >= FLT_MIN)) q = 1.0f;
+    }
   }
   const float rc = __builtin_amdgcn_rcpf(q);
   const float nm = -mn;
@@ -273,11 +277,13 @@ __device__ __forceinline__ void group_qparams_f16_rcp(float mn, float mx, float&
   const float r = mx - mn;
   float s = r * kInvL;
   s = fmaf(fmaf(-s, kL, r), kInvL, s);
-  if (!(s >= FLT_MIN)) {
-    const float a = fabsf(mn);
-    s = a * kInvL;
-    s = fmaf(fmaf(-s, kL, a), kInvL, s);
-    if (!(s >= FLT_MIN)) s = 1.0f;
+  if (__builtin_expect(__builtin_amdgcn_ballot_w64(!(s >= FLT_MIN)) != 0, 0)) {
+    if (!(s >= FLT_MIN)) {  // as row_qparams: only in a wave that has such a group
+      const float a = fabsf(mn);
+      s = a * kInvL;
+      s = fmaf(fmaf(-s, kL, a), kInvL, s);
+      if (!(s >= FLT_MIN)) s = 1.0f;
+    }
   }
   s16 = round_f16(s);
   if (!(s16 > 0.0f)) s16 = 5.9604644775390625e-08f;  // smallest positive FP16
