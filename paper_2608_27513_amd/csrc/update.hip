@@ -310,6 +310,7 @@ damp_status update(bool kda, const damp_pool* pool, int32_t layer, const int32_t
                    : codec == kCodecPaper ? kPaper
                    : codec == kCodecInt4  ? kInt4
                    : codec == kCodecFp8   ? kFp8
+                   : codec == kCodecNvfp4 ? kNvfp4
                                           : -1;
   if (sfmt >= 0 && D == 128 && p.k_hi <= 32 && tiles_fit) {
     if (!launch_stream128(kda, sfmt, p, B, s))

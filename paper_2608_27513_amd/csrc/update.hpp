@@ -29,8 +29,8 @@ struct UpdateParams {
 };
 
 // The streaming kernel for d = 128 mixed tiles with k_hi <= 32 (update_stream.hip)
-// in the default tiers (fmt = kMixed) or a group format of App. A.1's table
-// (kPaper, kInt4, kFp8). Returns false if it did not launch (the occupancy
+// in the default tiers (fmt = kMixed) or another format of App. A.1's table
+// (kPaper, kInt4, kFp8, kNvfp4). Returns false if it did not launch (the occupancy
 // query or the launch failed).
 bool launch_stream128(bool kda, int fmt, const UpdateParams& p, int B, hipStream_t stream);
 

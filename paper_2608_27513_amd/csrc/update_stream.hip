@@ -1,7 +1,7 @@
 // Persistent, software-pipelined decode-step update for d_k = d_v = 128 mixed
 // tiles with at most 32 high-precision rows (section 3.1 Eq. (1)-(2);
 // section 3.2 Eq. (3); section 5.2 and App. A.5), in the default tiers or
-// the UINT8, UINT4 and FP8 rows of App. A.1's format table.
+// the UINT8, UINT4, FP8 and NVFP4 rows of App. A.1's format table.
 //
 // The state update moves ~2.4 bytes per state value and does ~11 VALU
 // instructions per value, so on MI355X the memory time and the VALU time are
@@ -87,23 +87,42 @@ __device__ __forceinline__ float fold8(float a, float b, bool upper) {
                                                         true));
 }
 
+// Largest of a non-negative value over the 64 lanes of a wave, returned to
+// every lane: butterflies within rows of 16 lanes, then row broadcasts (the
+// lanes they do not write keep 0, the identity for non-negative values).
+__device__ __forceinline__ float wave_max_nonneg(float x) {
+  x = fmaxf(x, dpp_mov<0xb1>(x));   // quad_perm [1,0,3,2]
+  x = fmaxf(x, dpp_mov<0x4e>(x));   // quad_perm [2,3,0,1]
+  x = fmaxf(x, dpp_mov<0x141>(x));  // row_half_mirror
+  x = fmaxf(x, dpp_mov<0x140>(x));  // row_mirror: every lane holds its row's max
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x142, 0xa, 0xf,
+                                                          false)));
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x143, 0xc, 0xf,
+                                                          false)));
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 63));
+}
+
 // Packed bytes of one tile as loaded by one thread: row slot 0 (the first
-// 16 bytes of a 16-bit row slice, or its codes: 16 bytes, UINT4 8 in .xy),
-// the codes of slots 1..3 (16 bytes, UINT4 8), the second half of a 16-bit
-// row slot 0, and the metadata of one row of its wave: the (s, z) pair of the
-// default tiers (8 bytes) or the four words of its groups of 32 (16 bytes).
+// 16 bytes of a 16-bit row slice, or its codes: 16 bytes, 4-bit codes 8 in
+// .xy), the codes of slots 1..3 (16 bytes, 4-bit codes 8), the second half
+// of a 16-bit row slot 0, the metadata of one row of its wave (the (s, z)
+// pair of the default tiers or NVFP4's eight block scales: 8 bytes; the four
+// words of the groups of 32: 16 bytes) and NVFP4's global scale.
 template <int FMT>
 struct RawSetT {
-  using Codes = typename std::conditional<FMT == kInt4, u32x2, u32x4>::type;
+  using Codes =
+      typename std::conditional<FMT == kInt4 || FMT == kNvfp4, u32x2, u32x4>::type;
   u32x4 ra0;
   Codes rc[3];
   u32x4 rb0 = u32x4{0u, 0u, 0u, 0u};
-  typename std::conditional<FMT == kMixed, u32x2, u32x4>::type rm;
+  typename std::conditional<FMT == kMixed || FMT == kNvfp4, u32x2, u32x4>::type rm;
+  uint32_t gs = 0u;
 };
 
 // Sixteen low-tier values of one row slice from their codes: A c + B0 for
 // the integer codes (UINT8; UINT4 nibble j of word k is value 8 k + j), A c
-// for E4M3 (B0 unused). A and B0 fold the decay into the dequantization.
+// for E4M3 and E2M1 (B0 unused; E2M1 nibbles in the same order). A and B0
+// fold the decay into the dequantization.
 template <int FMT, typename W>
 __device__ __forceinline__ void decode16(const W& w, float A, float B0, float (&x)[16]) {
   if constexpr (FMT == kInt4) {
@@ -121,6 +140,17 @@ __device__ __forceinline__ void decode16(const W& w, float A, float B0, float (&
       x[8 * k + 5] = fmaf(A, ubyte<2>(od), B0);
       x[8 * k + 6] = fmaf(A, ubyte<3>(ev), B0);
       x[8 * k + 7] = fmaf(A, ubyte<3>(od), B0);
+    }
+  } else if constexpr (FMT == kNvfp4) {
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      float e[8];
+      e2m1_byte<0>(w[k], e[0], e[1]);
+      e2m1_byte<1>(w[k], e[2], e[3]);
+      e2m1_byte<2>(w[k], e[4], e[5]);
+      e2m1_byte<3>(w[k], e[6], e[7]);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) x[8 * k + j] = A * e[j];
     }
   } else if constexpr (FMT == kFp8) {
 #pragma unroll
@@ -152,8 +182,10 @@ struct OpsRegs {
 // row). The group formats of App. A.1's table, each with FP16 high rows and
 // one 4-byte word per group of 32 low values: FMT = kPaper (UINT8 codes, FP16
 // (s, z)), kInt4 (UINT4 codes, FP16 (s, z)), kFp8 (E4M3 codes, one fp32 scale
-// of Eq. (16)). With the block-32 transform (p.had; UINT8 and UINT4 only) the
-// recurrence runs in the
+// of Eq. (16)). FMT = kNvfp4: FP16 high rows, E2M1 codes in blocks of 16
+// (one lane's slice) with an E4M3 scale each, and one fp32 global scale per
+// tile from the largest magnitude of its updated low tier. With the block-32
+// transform (p.had; UINT8 and UINT4 only) the recurrence runs in the
 // transformed domain: H is symmetric and orthonormal, so a low row is used as
 // stored (s (c - z) of the transformed values) and only the FP16 rows are
 // transformed, on load and before the store; v is transformed on staging and
@@ -169,8 +201,11 @@ template <bool KDA, int FMT, int DEPTH>
 __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
     const UpdateParams p, const int ntiles, const int tile_bytes) {
   constexpr int D = 128, RG = 32, RPT = 4, CPT = 16, TPR = 8;
-  constexpr bool kP = FMT != kMixed;  // a group format: FP16 rows, 16 metadata bytes per row
-  constexpr bool kNib = FMT == kInt4;
+  constexpr bool kF16 = FMT != kMixed;  // FP16 high rows
+  // 16 metadata bytes per low row (one word per group of 32); the default
+  // tiers and NVFP4 have 8 (the (s, z) pair, or eight E4M3 block scales)
+  constexpr bool kP = FMT == kPaper || FMT == kInt4 || FMT == kFp8;
+  constexpr bool kNib = FMT == kInt4 || FMT == kNvfp4;  // two codes per byte
   constexpr int kCodeRow = kNib ? D / 2 : D;  // code bytes per low row
   constexpr int kSlice = kNib ? 8 : 16;       // code bytes per row slice
   using RawSet = RawSetT<FMT>;
@@ -187,14 +222,17 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
   __shared__ float vsh[3][D];
   __shared__ float opsc[3][4];
   // Per wave: the metadata of its 32 rows (8 wave + j + 32 i at index j +
-  // 8 i) of the next tile as loaded: (s, z) pairs, or (paper tiers, [0]) the
-  // four FP16 (s, z) words of the groups, which also pass through [1] as
-  // re-encoded.
+  // 8 i) of the next tile as loaded: 8 bytes per row ((s, z) pairs, NVFP4's
+  // block scales), or ([0]) the four words of the groups, which also pass
+  // through [1] as re-encoded.
   __shared__ float2 msh[4][kP ? 1 : 32];
   __shared__ u32x4 mshp[4][2][kP ? 32 : 1];
-  // Default tiers: the re-encoded (s, z) of every row of a tile, by tile
-  // parity, stored after the next tile's workgroup barrier as whole lines.
+  // 8-byte metadata: the re-encoded rows of a tile, by tile parity, stored
+  // after the next tile's workgroup barrier as whole lines.
   __shared__ float2 mout[2][kP ? 1 : D];
+  // NVFP4: each wave's largest magnitude of the updated low tier, by tile
+  // parity, for the tile's global scale
+  __shared__ float amx[2][4];
   // Per wave: its 8 high rows (slot 0) in tile order, 2 KB, for the
   // exchange between the lane layout and whole 1 KB loads and stores.
   __shared__ u32x4 hsh[4][2 * 64];
@@ -216,6 +254,7 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
   const bool hi0 = rg < k_hi;  // row slot 0 of this thread is in the bf16 tier
   const int lo0 = k_hi * D * 2;
   const int meta0 = lo0 + (D - k_hi) * kCodeRow;
+  const int off_gs = meta0 + (D - k_hi) * 8;  // NVFP4: the tile's fp32 global scale
   constexpr int kMetaRow = kP ? 16 : 8;  // metadata bytes per low row
   const int o_esize = p.o_bf16 ? 2 : 4;
   // slot ids are read-only here: scalar loads through the constant address space
@@ -251,8 +290,8 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
   // o. With the paper's tiers the waves holding the 16-bit rows (0 and 1 for
   // k_hi = 16) also transform them, so waves 2 and 3 stage and wave 1 writes:
   // measured, 2.7% (GDN) and 5.7% (KDA) faster than waves 0, 1 and 3.
-  constexpr int kOpsT = kP ? 128 : 0;  // first thread of the operand waves
-  constexpr int kOutWave = kP ? 1 : 3;
+  constexpr int kOpsT = kF16 ? 128 : 0;  // first thread of the operand waves
+  constexpr int kOutWave = kF16 ? 1 : 3;
   const int tr = t - kOpsT;            // tile row of an operand thread
   const bool ops_thread = tr >= 0 && tr < D;
   const int my_u =
@@ -326,6 +365,8 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
     if (part == 0) {
       if constexpr (kP) rs.rm = ld16(r, off_m);
       else rs.rm = ld8(r, off_m);
+      if constexpr (FMT == kNvfp4)
+        rs.gs = __builtin_amdgcn_raw_buffer_load_b32(r, off_gs, 0, kCachePolicyNT);
       if (kNib && wave_lo) {
         const u32x2 c = ld8(r, off_a0);
         rs.ra0 = __builtin_shufflevector(c, c, 0, 1, -1, -1);
@@ -417,11 +458,16 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
       aa[i] = KDA ? o4.z : alpha;
     }
     // per row slot: the dequantization of this lane's slice, A c + B0 (or A c
-    // for E4M3), with the decay folded in
+    // for E4M3 and E2M1), with the decay folded in
     float dA[RPT], dB[RPT];
 #pragma unroll
     for (int i = 0; i < RPT; ++i) {
-      if constexpr (kP) {  // this lane's group: one word
+      if constexpr (FMT == kNvfp4) {  // this lane's block: its E4M3 scale times the global one
+        const uint32_t sb =
+            reinterpret_cast<const uint8_t*>(&msh[wave][0])[(rgw + 8 * i) * 8 + cg];
+        dA[i] = aa[i] * (e4m3_byte<0>(sb) * __uint_as_float(cur.gs));
+        dB[i] = 0.0f;
+      } else if constexpr (kP) {  // this lane's group: one word
         const uint32_t m = reinterpret_cast<const uint32_t*>(&mshp[wave][0][0])[(rgw + 8 * i) * 4 +
                                                                                (cg >> 1)];
         if constexpr (FMT == kFp8) {
@@ -440,7 +486,7 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
     float x[RPT][CPT];
     const u32x4 ra0 = cur.ra0;
     if (hi0) {
-      if constexpr (kP) {  // FP16 rows, into the transformed domain with had
+      if constexpr (kF16) {  // FP16 rows, into the transformed domain with had
         const float a0 = aa[0] * (had ? kInvSqrt32 : 1.0f);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -629,6 +675,30 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
 #pragma unroll
       for (int j = 0; j < CPT; ++j) x[i][j] = fmaf(bk, dl[j], x[i][j]);
     }
+    // NVFP4: the tile's global scale from the largest magnitude of its
+    // updated low tier, over the workgroup (one more barrier); the block
+    // maxima are kept for the block scales
+    float bmx[RPT];
+    float s_g = 1.0f, d6 = 6.0f, rd6 = 1.0f;
+    if constexpr (FMT == kNvfp4) {
+      float am = 0.0f;
+#pragma unroll
+      for (int i = 0; i < RPT; ++i) {
+        float m = fabsf(x[i][0]);
+#pragma unroll
+        for (int j = 1; j < CPT; ++j) m = fmaxf(m, fabsf(x[i][j]));
+        bmx[i] = m;
+        if (i > 0 || !hi0) am = fmaxf(am, m);
+      }
+      am = wave_max_nonneg(am);
+      if (lane == 0) amx[pb][wave] = am;
+      lds_barrier();
+      s_g = nvfp4_global(fmaxf(fmaxf(amx[pb][0], amx[pb][1]), fmaxf(amx[pb][2], amx[pb][3])));
+      d6 = 6.0f * s_g;
+      rd6 = refined_rcp(d6);
+      __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(s_g), rs_cur, t == 0 ? off_gs : kDrop,
+                                            0, kCachePolicyNT);
+    }
     u32x4 wa0, wb0;
     Codes wc[RPT];
     float2 wm[RPT];    // default tiers: the row's (s, z)
@@ -636,7 +706,7 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
 #pragma unroll
     for (int i = 0; i < RPT; ++i) {
       if (i == 0 && hi0) {
-        if constexpr (kP) {  // FP16 rows, back from the transformed domain with had
+        if constexpr (kF16) {  // FP16 rows, back from the transformed domain with had
           if (had) {
             fwht32_pair(x[0], (cg & 1) != 0);
 #pragma unroll
@@ -658,7 +728,27 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
         wg[0] = 0u;
         continue;
       }
-      if constexpr (FMT == kFp8) {
+      if constexpr (FMT == kNvfp4) {
+        // the block scale E4M3(min(amax / (6 s_g), 448)) (the quotient from
+        // the refined reciprocal), codes E2M1(x / scale), zero codes under a
+        // zero scale
+        float tq = bmx[i] * rd6;
+        tq = fmaf(fmaf(-tq, d6, bmx[i]), rd6, tq);
+        const uint32_t sb = cvt_e4m3x2<false>(fminf(tq, 448.0f), 0.0f, 0u) & 0xffu;
+        const float scale = e4m3_byte<0>(sb) * s_g;
+        const bool nz = scale > 0.0f;
+        const float inv = nz ? refined_rcp(scale) : 0.0f;
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+          const float* y = &x[i][8 * k];
+          uint32_t v = cvt_e2m1x2<0>(y[0] * inv, y[1] * inv, 0u);
+          v = cvt_e2m1x2<1>(y[2] * inv, y[3] * inv, v);
+          v = cvt_e2m1x2<2>(y[4] * inv, y[5] * inv, v);
+          v = cvt_e2m1x2<3>(y[6] * inv, y[7] * inv, v);
+          wc[i][k] = nz ? v : 0u;
+        }
+        wg[i] = sb;
+      } else if constexpr (FMT == kFp8) {
         // Eq. (16): s = max |x| / 448 over the lane pair's group of 32
         float amax = fabsf(x[i][0]);
 #pragma unroll
@@ -691,7 +781,7 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
           row_qparams(mn, mx, s, z, inv);
           wm[i] = make_float2(s, z);
         }
-        if constexpr (kNib) {
+        if constexpr (FMT == kInt4) {
           // codes clamped to [0, 15] before the conversion (it rounds to
           // nearest even), then values 2 m and 2 m + 1 into the nibbles of byte m
 #pragma unroll
@@ -734,6 +824,11 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
         for (int i = 0; i < RPT; ++i)
           reinterpret_cast<uint32_t*>(&mshp[wave][1][0])[(rgw + 8 * i) * 4 + (cg >> 1)] = wg[i];
       }
+    } else if constexpr (FMT == kNvfp4) {  // each lane its block's scale byte
+#pragma unroll
+      for (int i = 0; i < RPT; ++i)
+        reinterpret_cast<uint8_t*>(&mout[pb][0])[(rg + RG * i) * 8 + cg] =
+            static_cast<uint8_t>(wg[i]);
     } else if (cg == 0) {
 #pragma unroll
       for (int i = 0; i < RPT; ++i) mout[pb][rg + RG * i] = wm[i];
@@ -814,7 +909,7 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
 enum StreamKernel {
   kGdnMixed1, kGdnMixed2, kKdaMixed1, kKdaMixed2,
   kGdnPaper2, kKdaPaper2, kGdnInt42, kKdaInt42, kGdnFp82, kKdaFp82,
-  kNumStream
+  kGdnNvfp42, kKdaNvfp42, kNumStream
 };
 
 template <bool KDA, int FMT, int DEPTH>
@@ -833,7 +928,9 @@ const void* stream_kernel(int which) {
     case kGdnInt42: return kernel_ptr<false, kInt4, 2>();
     case kKdaInt42: return kernel_ptr<true, kInt4, 2>();
     case kGdnFp82: return kernel_ptr<false, kFp8, 2>();
-    default: return kernel_ptr<true, kFp8, 2>();
+    case kKdaFp82: return kernel_ptr<true, kFp8, 2>();
+    case kGdnNvfp42: return kernel_ptr<false, kNvfp4, 2>();
+    default: return kernel_ptr<true, kNvfp4, 2>();
   }
 }
 
@@ -872,6 +969,7 @@ bool launch_stream128(bool kda, int fmt, const UpdateParams& p, int B, hipStream
     case kPaper: which = kda ? kKdaPaper2 : kGdnPaper2; break;
     case kInt4: which = kda ? kKdaInt42 : kGdnInt42; break;
     case kFp8: which = kda ? kKdaFp82 : kGdnFp82; break;
+    case kNvfp4: which = kda ? kKdaNvfp42 : kGdnNvfp42; break;
     default: which = kda ? kKdaMixed2 : kGdnMixed2; break;
   }
   int cus = 0, per_cu = 0;
@@ -891,8 +989,9 @@ bool launch_stream128(bool kda, int fmt, const UpdateParams& p, int B, hipStream
   if (per_head > B) per_head = B;
   const int grid = static_cast<int>(per_head * p.HV);
   const int lo_rows = 128 - p.k_hi;
-  const int tile_bytes = p.k_hi * 128 * 2 + lo_rows * (fmt == kInt4 ? 64 : 128) +
-                         lo_rows * (fmt == kMixed ? 8 : 16);
+  const bool nib = fmt == kInt4 || fmt == kNvfp4, meta8 = fmt == kMixed || fmt == kNvfp4;
+  const int tile_bytes = p.k_hi * 128 * 2 + lo_rows * (nib ? 64 : 128) +
+                         lo_rows * (meta8 ? 8 : 16) + (fmt == kNvfp4 ? 4 : 0);
   UpdateParams pa = p;
   int nt = ntiles, tb = tile_bytes;
   void* args[] = {&pa, &nt, &tb};

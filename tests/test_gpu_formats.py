@@ -133,7 +133,7 @@ def test_prefill_parity(name):
     assert err <= 1e-4
 
 
-STREAM_FORMATS = ["int4", "int4_h32", "fp8"]
+STREAM_FORMATS = ["int4", "int4_h32", "fp8", "nvfp4"]
 
 
 @pytest.mark.parametrize("name", STREAM_FORMATS)
