@@ -455,11 +455,7 @@ def prefill_bench(torch, D, inputs, steps: int, log=print, T: int = 64):
     flops = 7.0 * d * d * B * HV * T
     res = dict(B=B, T=T, HK=HK, HV=HV, d=d, k_hi=k_hi, chunk_us=round(1e6 * sec, 1),
                tokens_per_s=round(B * T / sec), tflops=round(flops / sec / 1e12, 2),
-               frac_fp32_vector_peak=round(flops / sec / 157.3e12, 4),
-               # the published fp32 vector peak counts packed two-wide FMAs;
-               # this build issues one fp32 FMA per lane and instruction
-               # (256 CUs x 4 SIMDs x 16 lanes x 2 flops x 2.4 GHz)
-               frac_fp32_unpacked_peak=round(flops / sec / 78.6e12, 4))
+               frac_fp32_vector_peak=round(flops / sec / 157.3e12, 4))
     log(f"  prefill T={T}: {res['chunk_us']} us per chunk, {res['tokens_per_s']:.3g} tokens/s, "
         f"{res['tflops']} TFLOP/s")
     del pool, x, o
