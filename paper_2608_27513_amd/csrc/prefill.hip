@@ -4,13 +4,16 @@
 // One workgroup owns one (request, value head) tile: it decodes the stored
 // state once into registers, runs the recurrence of Eq. (1) in fp32 for the
 // chunk's T tokens (emitting o for every token), and re-encodes only the
-// chunk-final state. The thread mapping is that of the decode update: a row
-// of the tile is split over TPR lanes, each holding CPT columns of RPT rows.
+// chunk-final state. At d = 128 the block kernel below does this; for the
+// smaller head sizes (and inputs too long for its 32-bit offsets) the
+// generic kernel keeps the mapping of the decode update: a row of the tile
+// is split over TPR lanes, each holding CPT columns of RPT rows.
 //
-// Per token, threads t < d_k stage the token's operands (k~, q~ gathered
-// through the permutation, the row decay, v) in LDS, double-buffered: the
-// next token's operands are loaded into registers while the current token
-// computes. Both key-axis reductions share one LDS pass, and
+// In the generic kernel, per token, threads t < d_k stage the token's
+// operands (k~, q~ gathered through the permutation, the row decay, v) in
+// LDS, double-buffered: the next token's operands are loaded into registers
+// while the current token computes. Both key-axis reductions share one LDS
+// pass. In both kernels
 //   o = scale (S_bar^T q~ + beta (q~ . k~) delta)
 // equals scale * S^T q~ for the updated state S.
 #include <climits>
@@ -224,39 +227,75 @@ __global__ __launch_bounds__(NT) void prefill_kernel(const PrefillParams p) {
 // (the upper half's rows padded onto other banks). The stored tile is
 // decoded and encoded once per chunk with the row-slice codecs, 16 rows at a
 // time through an LDS transpose buffer, so every storage format is handled.
-struct ColOps {
-  uint32_t k[2] = {0u, 0u}, q[2] = {0u, 0u}, g[2] = {0u, 0u};
-  uint32_t gs = 0u, beta = 0u, v = 0u;
+// d = 128 chunks in blocks of tokens. A workgroup of four waves owns one
+// tile; thread (wave w, lane l = 8 cl + rb) keeps tile rows 16 rb .. 16 rb +
+// 15 of columns 32 w + 4 cl .. + 3, 64 values. The operands of TB tokens
+// (k~, q~ gathered through the permutation, KDA's a~ = exp(g~), v, beta, the
+// scalar decay, q~ . k~) are converted to fp32 once per block by the whole
+// workgroup into LDS, double-buffered: the next block's inputs are loaded
+// into registers while the current block runs, and one barrier per block
+// publishes them. Per token a lane reads its 16 rows' operands as LDS
+// broadcasts (eight distinct addresses per wave), forms 8 partial read-outs
+// (S_bar^T k~ and S_bar^T q~ over its rows, for its 4 columns) and sums them
+// over the 8 row blocks with three DPP butterfly steps (lane bits 0..2), so
+// every lane holds its columns' totals: the update needs no other exchange
+// and the waves do not wait for each other within a block. GDN's scalar
+// decay is deferred: the lane keeps P with S = gamma P, gamma the product of
+// the decays since the last renormalization, so a token costs one FMA per
+// state value for each read-out and one for the update:
+//   w = gamma sum_u k_u P_u,  P_u += k_u (beta delta / gamma).
+struct BlkOps {
+  uint32_t k[4], q[4], v[4], g[4];
+  uint32_t beta[4];
 };
 
 template <int KIND, bool KDA>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void prefill_col128(const PrefillParams p) {
-  constexpr int D = 128, CPT = 16, TPR = 8, RH = 64;  // rows per lane
-  constexpr int OPN = D + 4;                           // padded operand rows
-  __shared__ float tbuf[16][D + 4];        // 16 tile rows (padded against bank conflicts)
-  __shared__ float4 opk[4][2][OPN / 4];    // [wave][parity] k~ (row u at u + 4 (u >= 64))
-  __shared__ float4 opq[4][2][OPN / 4];    // q~
-  __shared__ float4 opa[4][2][KDA ? OPN / 4 : 1];  // a~ = exp(g~) per row (KDA)
+__global__ __launch_bounds__(256) void prefill_blk128(const PrefillParams p) {
+  constexpr int D = 128, TB = 8, CPT = 16, TPR = 8, NA = KDA ? TB : 1;
+  // operand blocks by parity; the decode/encode transit buffer (32 rows)
+  // aliases them outside the token loop
+  struct OpBuf {
+    float4 k[TB][D / 4];
+    float4 q[TB][D / 4];
+    float4 v[TB][D / 4];
+    float4 a[NA][D / 4];
+    float4 sc[TB];  // beta, alpha (GDN), q~ . k~ over rows 0..63 and 64..127
+  };
+  constexpr int kTbufFloats = 32 * (D + 4);
+  constexpr int kOpFloats = 2 * static_cast<int>(sizeof(OpBuf) / 4);
+  __shared__ float4 lds4[(kOpFloats > kTbufFloats ? kOpFloats : kTbufFloats) / 4];
+  OpBuf* ob = reinterpret_cast<OpBuf*>(lds4);
+  float(*tbuf)[D + 4] = reinterpret_cast<float(*)[D + 4]>(lds4);
 
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int hh = lane >> 5;                 // which half of the column
-  const int col = 32 * wave + (lane & 31);  // this lane's column
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int rb = lane & 7, cl = lane >> 3;
+  const int c0 = 32 * wave + 4 * cl;  // this lane's first column
+  const int rr = t >> 3, cg = t & 7, col0 = cg * CPT;  // row-slice role in transit
   const int h = blockIdx.x, b = blockIdx.y;
-  const int rr = (t >> 3) & 15, cg = t & 7, col0 = cg * CPT;  // row-slice role (t < 128)
   const int T = p.T;
   const int hk = h / (p.HV / p.HK);
-  const int o_esize = p.o_bf16 ? 2 : 4;
-  auto write_o = [&](int tok, float val) {
-    if (!p.o || hh) return;
-    uint8_t* at = static_cast<uint8_t*>(p.o) +
-                  (((static_cast<size_t>(b) * T + tok) * p.HV + h) * D + col) * o_esize;
-    if (p.o_bf16) *reinterpret_cast<uint16_t*>(at) = f32_to_bf16(val);
-    else *reinterpret_cast<float*>(at) = val;
+
+  // o of token tok at o_lane + tok * o_step (the token part is wave-uniform)
+  const size_t o_esize = p.o_bf16 ? 2 : 4;
+  uint8_t* const o_lane = static_cast<uint8_t*>(p.o) +
+                          ((static_cast<size_t>(b) * T * p.HV + h) * D + c0) * o_esize;
+  const size_t o_step = static_cast<size_t>(p.HV) * D * o_esize;
+  auto o_ptr = [&](int tok) { return o_lane + static_cast<size_t>(tok) * o_step; };
+  auto write_o = [&](int tok, const float (&ov)[4]) {
+    if (!p.o || rb != 0) return;
+    if (p.o_bf16) {
+      *reinterpret_cast<uint2*>(o_ptr(tok)) =
+          make_uint2(pack_bf16x2(ov[0], ov[1]), pack_bf16x2(ov[2], ov[3]));
+    } else {
+      *reinterpret_cast<float4*>(o_ptr(tok)) = make_float4(ov[0], ov[1], ov[2], ov[3]);
+    }
   };
 
   const int slot = p.slot_idx[b];
   if (slot < 0 || slot >= p.num_slots) {  // padded request: o = 0, state untouched
-    for (int tok = 0; tok < T; ++tok) write_o(tok, 0.0f);
+    const float z[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int tok = 0; tok < T; ++tok) write_o(tok, z);
     return;
   }
   uint8_t* tile = p.layer_base + static_cast<size_t>(slot) * p.slot_stride +
@@ -266,35 +305,38 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void p
   uint8_t* meta_bytes = codes + static_cast<size_t>(D - k_hi) * code_row_bytes<KIND, D>();
   const bool had = p.had != 0;
 
-  // ---- decode the stored state once, transposing 16 rows at a time
-  float x[RH];
+  // ---- decode: pass c moves tile rows 16 j + 4 c + m (j < 8, m < 4), which
+  // the row-slice threads decode and lane (rb, cl) reads as x[4 c + m]
+  float x[16][4];
 #pragma unroll
-  for (int c = 0; c < D / 16; ++c) {
-    if (t < 128) {  // waves 0 and 1 decode the 16 rows as row slices
+  for (int c = 0; c < 4; ++c) {
+    {
       float sl[CPT];
-      decode_row<KIND, D, CPT>(tile, codes, meta_bytes, 16 * c + rr, k_hi, cg, col0, had, sl);
+      decode_row<KIND, D, CPT>(tile, codes, meta_bytes, 16 * (rr >> 2) + 4 * c + (rr & 3), k_hi,
+                               cg, col0, had, sl);
 #pragma unroll
       for (int q4 = 0; q4 < CPT / 4; ++q4)
         *reinterpret_cast<float4*>(&tbuf[rr][col0 + 4 * q4]) =
             make_float4(sl[4 * q4], sl[4 * q4 + 1], sl[4 * q4 + 2], sl[4 * q4 + 3]);
     }
     __syncthreads();
-    if (hh == c / 4) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) x[16 * (c % 4) + r] = tbuf[r][col];
+    for (int m = 0; m < 4; ++m) {
+      const float4 v4 = *reinterpret_cast<const float4*>(&tbuf[4 * rb + m][c0]);
+      x[4 * c + m][0] = v4.x;
+      x[4 * c + m][1] = v4.y;
+      x[4 * c + m][2] = v4.z;
+      x[4 * c + m][3] = v4.w;
     }
     __syncthreads();
   }
 
-  // ---- per-token operands: lane stages rows lane and lane + 64. Inputs are
-  // read through buffer resources based at this request, with the token's
-  // offset wave-uniform and the row's per lane.
-  int urow2[2];
-#pragma unroll
-  for (int e = 0; e < 2; ++e) {
-    const int r = lane + 64 * e;
-    urow2[e] = 2 * (p.perm ? (static_cast<int>(p.perm[static_cast<size_t>(h) * D + r]) & (D - 1)) : r);
-  }
+  // ---- operand staging: thread t handles tile row (and column) r of the
+  // tokens 2 i + (wave >> 1) of a block, i < 4
+  const int r = 64 * (wave & 1) + lane;
+  const int u2 = 2 * (p.perm ? (static_cast<int>(p.perm[static_cast<size_t>(h) * D + r]) & (D - 1))
+                             : r);
+  const int half = wave >> 1;
   const size_t tp = static_cast<size_t>(p.t_pitch);
   constexpr int kCfg = 0x00020000;  // raw 32-bit buffer
   auto rsrc = [&](const uint16_t* base, size_t per_token) {
@@ -305,124 +347,183 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void p
   const __amdgpu_buffer_rsrc_t rq = rsrc(p.q, static_cast<size_t>(p.HK) * D);
   const __amdgpu_buffer_rsrc_t rv = rsrc(p.v, static_cast<size_t>(p.HV) * D);
   const __amdgpu_buffer_rsrc_t rg = rsrc(p.g, static_cast<size_t>(p.HV) * (KDA ? D : 1));
-  const __amdgpu_buffer_rsrc_t rb = rsrc(p.beta, static_cast<size_t>(p.HV));
-  auto load_ops = [&](ColOps& o, int tok) {
-    const int tt = p.t0 + tok;
-    const int kq = ((tt * p.HK + hk) * D) * 2;
-    const int th = tt * p.HV + h;
+  const __amdgpu_buffer_rsrc_t rbt = rsrc(p.beta, static_cast<size_t>(p.HV));
+  auto load_blk = [&](BlkOps& o, int blk) {
 #pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      o.k[e] = __builtin_amdgcn_raw_buffer_load_b16(rk, urow2[e], kq, 0);
-      o.q[e] = __builtin_amdgcn_raw_buffer_load_b16(rq, urow2[e], kq, 0);
-      if (KDA) o.g[e] = __builtin_amdgcn_raw_buffer_load_b16(rg, urow2[e], th * D * 2, 0);
-    }
-    if (!KDA) o.gs = __builtin_amdgcn_raw_buffer_load_b16(rg, 0, th * 2, 0);
-    o.beta = __builtin_amdgcn_raw_buffer_load_b16(rb, 0, th * 2, 0);
-    o.v = __builtin_amdgcn_raw_buffer_load_b16(rv, 2 * col, th * D * 2, 0);
-  };
-  // converts the staged words and writes this wave's operand slice; returns
-  // q~ . k~ over all rows (every lane)
-  auto publish = [&](const ColOps& o, int par) {
-    float kq = 0.0f;
-    float* fk = reinterpret_cast<float*>(opk[wave][par]);
-    float* fq = reinterpret_cast<float*>(opq[wave][par]);
-    float* fa = reinterpret_cast<float*>(opa[wave][KDA ? par : 0]);
-#pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      const int at = lane + 68 * e;  // row lane + 64 e, the upper half shifted by 4
-      const float kf = bf16_to_f32(static_cast<uint16_t>(o.k[e]));
-      const float qf = bf16_to_f32(static_cast<uint16_t>(o.q[e]));
-      fk[at] = kf;
-      fq[at] = qf;
-      if (KDA) fa[at] = __expf(bf16_to_f32(static_cast<uint16_t>(o.g[e])));
-      kq = fmaf(kf, qf, kq);
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
-    return wave_sum_dpp(kq);
-  };
-  // the partner lane's copy of v (the other half of the column)
-  auto partner = [&](float v) {
-    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
-                                                    false);
-    return __uint_as_float(hh ? r[0] : r[1]);
-  };
-
-  __builtin_amdgcn_sched_barrier(0);
-  ColOps cur, nxt;
-  float qk = 0.0f, beta = 0.0f, vj = 0.0f, alpha = 1.0f;
-  if (T > 0) {
-    load_ops(cur, 0);
-    qk = publish(cur, 0);
-    beta = bf16_to_f32(static_cast<uint16_t>(cur.beta));
-    vj = bf16_to_f32(static_cast<uint16_t>(cur.v));
-    if (!KDA) alpha = __expf(bf16_to_f32(static_cast<uint16_t>(cur.gs)));
-  }
-  const int ob = 17 * hh;  // this half's first float4 of the operand rows
-#pragma unroll 1
-  for (int tok = 0; tok < T; ++tok) {
-    const int par = tok & 1;
-    if (tok + 1 < T) load_ops(nxt, tok + 1);
-    // decay and both read-outs over this lane's 64 rows
-    float w[4] = {0.0f, 0.0f, 0.0f, 0.0f}, pq[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-    for (int i = 0; i < RH / 4; ++i) {
-      const float4 k4 = opk[wave][par][ob + i], q4 = opq[wave][par][ob + i];
-      float4 a4 = make_float4(alpha, alpha, alpha, alpha);
-      if (KDA) a4 = opa[wave][KDA ? par : 0][ob + i];
-      const float kk[4] = {k4.x, k4.y, k4.z, k4.w}, qq[4] = {q4.x, q4.y, q4.z, q4.w};
-      const float aa[4] = {a4.x, a4.y, a4.z, a4.w};
-#pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        float& xv = x[4 * i + m];
-        xv *= aa[m];
-        w[m] = fmaf(kk[m], xv, w[m]);
-        pq[m] = fmaf(qq[m], xv, pq[m]);
+    for (int i = 0; i < 4; ++i) {
+      const int tok = TB * blk + 2 * i + half;
+      if (tok < T) {
+        const int tt = p.t0 + tok;
+        const int kq = ((tt * p.HK + hk) * D) * 2;
+        const int th = tt * p.HV + h;
+        o.k[i] = __builtin_amdgcn_raw_buffer_load_b16(rk, u2, kq, 0);
+        o.q[i] = __builtin_amdgcn_raw_buffer_load_b16(rq, u2, kq, 0);
+        o.v[i] = __builtin_amdgcn_raw_buffer_load_b16(rv, 2 * r, th * D * 2, 0);
+        o.g[i] = KDA ? __builtin_amdgcn_raw_buffer_load_b16(rg, u2, th * D * 2, 0)
+                     : __builtin_amdgcn_raw_buffer_load_b16(rg, 0, th * 2, 0);
+        o.beta[i] = __builtin_amdgcn_raw_buffer_load_b16(rbt, 0, th * 2, 0);
       }
     }
-    float wt = (w[0] + w[1]) + (w[2] + w[3]);
-    float pt = (pq[0] + pq[1]) + (pq[2] + pq[3]);
-    wt += partner(wt);  // the column's other 64 rows
-    pt += partner(pt);
-    const float delta = vj - wt;  // delta = v - S_bar^T k~
-    write_o(tok, p.scale * fmaf(beta * qk, delta, pt));
-    // rank-1 update S = S_bar + beta k~ delta^T
-    const float bd = beta * delta;
+  };
+  auto publish_blk = [&](const BlkOps& o, int blk, int par) {
+    OpBuf& B_ = ob[par];
 #pragma unroll
-    for (int i = 0; i < RH / 4; ++i) {
-      const float4 k4 = opk[wave][par][ob + i];
-      x[4 * i + 0] = fmaf(k4.x, bd, x[4 * i + 0]);
-      x[4 * i + 1] = fmaf(k4.y, bd, x[4 * i + 1]);
-      x[4 * i + 2] = fmaf(k4.z, bd, x[4 * i + 2]);
-      x[4 * i + 3] = fmaf(k4.w, bd, x[4 * i + 3]);
+    for (int i = 0; i < 4; ++i) {
+      const int tb = 2 * i + half;
+      if (TB * blk + tb < T) {
+        const float kf = bf16_to_f32(static_cast<uint16_t>(o.k[i]));
+        const float qf = bf16_to_f32(static_cast<uint16_t>(o.q[i]));
+        reinterpret_cast<float*>(B_.k[tb])[r] = kf;
+        reinterpret_cast<float*>(B_.q[tb])[r] = qf;
+        reinterpret_cast<float*>(B_.v[tb])[r] = bf16_to_f32(static_cast<uint16_t>(o.v[i]));
+        if (KDA)
+          reinterpret_cast<float*>(B_.a[KDA ? tb : 0])[r] =
+              __expf(bf16_to_f32(static_cast<uint16_t>(o.g[i])));
+        const float kq = wave_sum_dpp(kf * qf);
+        float* sc = reinterpret_cast<float*>(&B_.sc[tb]);
+        if (lane == 0) {
+          sc[2 + (wave & 1)] = kq;
+          if ((wave & 1) == 0) {
+            sc[0] = bf16_to_f32(static_cast<uint16_t>(o.beta[i]));
+            sc[1] = KDA ? 1.0f : __expf(bf16_to_f32(static_cast<uint16_t>(o.g[i])));
+          }
+        }
+      }
     }
-    if (tok + 1 < T) {
-      qk = publish(nxt, par ^ 1);
-      beta = bf16_to_f32(static_cast<uint16_t>(nxt.beta));
-      vj = bf16_to_f32(static_cast<uint16_t>(nxt.v));
-      if (!KDA) alpha = __expf(bf16_to_f32(static_cast<uint16_t>(nxt.gs)));
+  };
+
+  const int nblk = (T + TB - 1) / TB;
+  BlkOps cur;
+  if (nblk > 0) {
+    load_blk(cur, 0);
+    publish_blk(cur, 0, 0);
+  }
+  __syncthreads();
+  float gamma = 1.0f;
+#pragma unroll 1
+  for (int blk = 0; blk < nblk; ++blk) {
+    const int par = blk & 1;
+    if (blk + 1 < nblk) load_blk(cur, blk + 1);
+    const OpBuf& B_ = ob[par];
+    const int ntok = T - TB * blk < TB ? T - TB * blk : TB;
+#pragma unroll 1
+    for (int tb = 0; tb < ntok; ++tb) {
+      const int tok = TB * blk + tb;
+      float kr[16];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float4 k4 = B_.k[tb][4 * rb + j];
+        kr[4 * j] = k4.x;
+        kr[4 * j + 1] = k4.y;
+        kr[4 * j + 2] = k4.z;
+        kr[4 * j + 3] = k4.w;
+      }
+      if constexpr (KDA) {  // the decay of each row
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float4 a4 = B_.a[KDA ? tb : 0][4 * rb + j];
+          const float aj[4] = {a4.x, a4.y, a4.z, a4.w};
+#pragma unroll
+          for (int m = 0; m < 4; ++m)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) x[4 * j + m][c] *= aj[m];
+        }
+      }
+      // partial read-outs over this lane's 16 rows
+      float w[4], pq[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) w[c] = kr[0] * x[0][c];
+#pragma unroll
+      for (int i = 1; i < 16; ++i)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) w[c] = fmaf(kr[i], x[i][c], w[c]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float4 q4 = B_.q[tb][4 * rb + j];
+        const float qj[4] = {q4.x, q4.y, q4.z, q4.w};
+#pragma unroll
+        for (int m = 0; m < 4; ++m)
+#pragma unroll
+          for (int c = 0; c < 4; ++c)
+            pq[c] = (j == 0 && m == 0) ? qj[0] * x[0][c] : fmaf(qj[m], x[4 * j + m][c], pq[c]);
+      }
+      // sums over the 8 row blocks: lane bits 0, 1 (quad_perm) and 2
+      // (row_half_mirror pairs each lane with one of the other quad)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        w[c] += dpp_mov<0xb1>(w[c]);
+        pq[c] += dpp_mov<0xb1>(pq[c]);
+      }
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        w[c] += dpp_mov<0x4e>(w[c]);
+        pq[c] += dpp_mov<0x4e>(pq[c]);
+      }
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        w[c] += dpp_mov<0x141>(w[c]);
+        pq[c] += dpp_mov<0x141>(pq[c]);
+      }
+      // per token: g = gamma (1 for KDA), o = scale (g p + beta (q~.k~) delta),
+      // delta = v - g w, and the update's factor (beta / g) delta
+      const float4 sc = B_.sc[tb];
+      if (!KDA) gamma *= sc.y;
+      const float gw = KDA ? 1.0f : gamma;
+      const float sg = p.scale * gw, sbq = p.scale * sc.x * (sc.z + sc.w);
+      const float bg = KDA ? sc.x : sc.x * refined_rcp(gamma);
+      const float4 v4 = B_.v[tb][c0 / 4];
+      const float vv[4] = {v4.x, v4.y, v4.z, v4.w};
+      float ov[4], cf[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const float delta = fmaf(-gw, w[c], vv[c]);  // delta = v - S_bar^T k~
+        ov[c] = fmaf(sbq, delta, sg * pq[c]);
+        cf[c] = bg * delta;
+      }
+      write_o(tok, ov);
+      // rank-1 update S = S_bar + beta k~ delta^T (GDN: on P = S / gamma)
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) x[i][c] = fmaf(kr[i], cf[c], x[i][c]);
+      if (!KDA && !(gamma >= 9.094947e-13f && gamma <= 1.0995116e12f)) {  // outside [2^-40, 2^40]
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+#pragma unroll
+          for (int c = 0; c < 4; ++c) x[i][c] *= gamma;
+        gamma = 1.0f;
+      }
     }
+    if (blk + 1 < nblk) publish_blk(cur, blk + 1, par ^ 1);
+    __syncthreads();
+  }
+  if (!KDA) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) x[i][c] *= gamma;
   }
 
-  // ---- store the chunk-final state per its tier, 16 rows at a time
+  // ---- store the chunk-final state per its tier, in the decode's passes
   float s_g = 1.0f;
   if constexpr (KIND == kNvfp4) {  // the global scale of the final low tier
     float amax = 0.0f;
 #pragma unroll
-    for (int i = 0; i < RH; ++i)
-      if (RH * hh + i >= k_hi) amax = fmaxf(amax, fabsf(x[i]));
+    for (int i = 0; i < 16; ++i)
+      if (16 * rb + i >= k_hi)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) amax = fmaxf(amax, fabsf(x[i][c]));
     s_g = nvfp4_global(block_max<256>(amax));
     if (t == 0) store_global_scale<D>(meta_bytes, k_hi, s_g);
   }
 #pragma unroll
-  for (int c = 0; c < D / 16; ++c) {
-    if (hh == c / 4) {
+  for (int c = 0; c < 4; ++c) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) tbuf[r][col] = x[16 * (c % 4) + r];
-    }
+    for (int m = 0; m < 4; ++m)
+      *reinterpret_cast<float4*>(&tbuf[4 * rb + m][c0]) =
+          make_float4(x[4 * c + m][0], x[4 * c + m][1], x[4 * c + m][2], x[4 * c + m][3]);
     __syncthreads();
-    if (t < 128) {
+    {
       float sl[CPT];
 #pragma unroll
       for (int q4 = 0; q4 < CPT / 4; ++q4) {
@@ -432,173 +533,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void p
         sl[4 * q4 + 2] = v4.z;
         sl[4 * q4 + 3] = v4.w;
       }
-      encode_row<KIND, D, CPT, TPR>(sl, 16 * c + rr, k_hi, cg, col0, tile, codes, meta_bytes,
-                                    had, s_g);
+      encode_row<KIND, D, CPT, TPR>(sl, 16 * (rr >> 2) + 4 * c + (rr & 3), k_hi, cg, col0, tile,
+                                    codes, meta_bytes, had, s_g);
     }
-    __syncthreads();
-  }
-}
-
-// GDN chunks at d = 128 take their per-row operands from scalar registers:
-// a workgroup of two waves holds the tile transposed with rows in natural
-// key-channel order (the permutation is applied when the tile is decoded and
-// encoded), lane l of wave w keeping column 64 w + l of all 128 rows. The
-// token's k~ and q~ rows then come straight from the inputs by scalar loads,
-// shared by every lane at no LDS cost. The head's scalar decay is deferred:
-// the lane keeps P with S = gamma P, gamma the product of the decays since the
-// last renormalization, so a token costs one FMA per state value for each
-// read-out and one for the update:
-//   w = gamma sum_u k_u P_u,  P_u += k_u (beta delta / gamma).
-template <int KIND>
-__global__ __launch_bounds__(128) void prefill_gdn_sgpr128(const PrefillParams p) {
-  constexpr int D = 128, CPT = 16, TPR = 8;
-  __shared__ float tbuf[16][D + 4];  // 16 rows in transit (padded against bank conflicts)
-  __shared__ int inv[D];             // tile row of each natural key channel
-
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int col = 64 * wave + lane;
-  const int h = blockIdx.x, b = blockIdx.y;
-  const int rr = t >> 3, cg = t & 7, col0 = cg * CPT;  // row-slice role of the codecs
-  const int T = p.T;
-  const int hk = h / (p.HV / p.HK);
-  const int o_esize = p.o_bf16 ? 2 : 4;
-  auto write_o = [&](int tok, float val) {
-    if (!p.o) return;
-    uint8_t* at = static_cast<uint8_t*>(p.o) +
-                  (((static_cast<size_t>(b) * T + tok) * p.HV + h) * D + col) * o_esize;
-    if (p.o_bf16) *reinterpret_cast<uint16_t*>(at) = f32_to_bf16(val);
-    else *reinterpret_cast<float*>(at) = val;
-  };
-
-  const int slot = p.slot_idx[b];
-  if (slot < 0 || slot >= p.num_slots) {  // padded request: o = 0, state untouched
-    for (int tok = 0; tok < T; ++tok) write_o(tok, 0.0f);
-    return;
-  }
-  uint8_t* tile = p.layer_base + static_cast<size_t>(slot) * p.slot_stride +
-                  static_cast<size_t>(h) * p.tile_stride;
-  const int k_hi = KIND == kFp32 ? D : p.k_hi;
-  uint8_t* codes = tile + static_cast<size_t>(k_hi) * D * 2;
-  uint8_t* meta_bytes = codes + static_cast<size_t>(D - k_hi) * code_row_bytes<KIND, D>();
-  const bool had = p.had != 0;
-
-  inv[p.perm ? (static_cast<int>(p.perm[static_cast<size_t>(h) * D + t]) & (D - 1)) : t] = t;
-  __syncthreads();
-
-  // ---- decode: natural rows 16 c .. 16 c + 15 at a time
-  float x[D];
-#pragma unroll
-  for (int c = 0; c < D / 16; ++c) {
-    __builtin_amdgcn_sched_barrier(0);
-    float sl[CPT];
-    decode_row<KIND, D, CPT>(tile, codes, meta_bytes, inv[16 * c + rr], k_hi, cg, col0, had, sl);
-#pragma unroll
-    for (int q4 = 0; q4 < CPT / 4; ++q4)
-      *reinterpret_cast<float4*>(&tbuf[rr][col0 + 4 * q4]) =
-          make_float4(sl[4 * q4], sl[4 * q4 + 1], sl[4 * q4 + 2], sl[4 * q4 + 3]);
-    __syncthreads();
-#pragma unroll
-    for (int r = 0; r < 16; ++r) x[16 * c + r] = tbuf[r][col];
-    __syncthreads();
-  }
-
-  const size_t req = static_cast<size_t>(b) * p.t_pitch + p.t0;
-  const uint16_t* __restrict__ vb = p.v;
-  float gamma = 1.0f;
-#pragma unroll 1
-  for (int tok = 0; tok < T; ++tok) {
-    const size_t bt = req + tok;
-    const size_t bth = bt * p.HV + h;
-    const uint32_t* __restrict__ kr =
-        reinterpret_cast<const uint32_t*>(p.k + (bt * p.HK + hk) * D);
-    const uint32_t* __restrict__ qr =
-        reinterpret_cast<const uint32_t*>(p.q + (bt * p.HK + hk) * D);
-    const float alpha = __expf(bf16_to_f32(p.g[bth]));
-    const float beta = bf16_to_f32(p.beta[bth]);
-    const float vj = bf16_to_f32(vb[bth * D + col]);
-    // q~ . k~ over the channels (permutation invariant), two per lane
-    float kq = 0.0f;
-#pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      const uint16_t* kk = p.k + (bt * p.HK + hk) * D;
-      const uint16_t* qq = p.q + (bt * p.HK + hk) * D;
-      kq = fmaf(bf16_to_f32(kk[lane + 64 * e]), bf16_to_f32(qq[lane + 64 * e]), kq);
-    }
-    const float qk = wave_sum_dpp(kq);
-    gamma *= alpha;
-    // both read-outs: one FMA per state value each, k and q from SGPRs
-    float w0 = 0.0f, w1 = 0.0f, p0 = 0.0f, p1 = 0.0f;
-#pragma unroll
-    for (int d = 0; d < D / 2; ++d) {
-      const uint32_t pk = kr[d], pq = qr[d];
-      w0 = fmaf(__uint_as_float(pk << 16), x[2 * d], w0);
-      w1 = fmaf(__uint_as_float(pk & 0xffff0000u), x[2 * d + 1], w1);
-      p0 = fmaf(__uint_as_float(pq << 16), x[2 * d], p0);
-      p1 = fmaf(__uint_as_float(pq & 0xffff0000u), x[2 * d + 1], p1);
-    }
-    const float wt = gamma * (w0 + w1);
-    const float pt = gamma * (p0 + p1);
-    const float delta = vj - wt;  // delta = v - S_bar^T k~
-    write_o(tok, p.scale * fmaf(beta * qk, delta, pt));
-    // S = S_bar + beta k~ delta^T, i.e. P += k~ (beta delta / gamma)
-    const float cf = beta * delta / gamma;
-#pragma unroll
-    for (int d = 0; d < D / 2; ++d) {
-      const uint32_t pk = kr[d];
-      x[2 * d] = fmaf(__uint_as_float(pk << 16), cf, x[2 * d]);
-      x[2 * d + 1] = fmaf(__uint_as_float(pk & 0xffff0000u), cf, x[2 * d + 1]);
-    }
-    if (!(gamma >= 9.094947e-13f && gamma <= 1.0995116e12f)) {  // outside [2^-40, 2^40]
-#pragma unroll
-      for (int u = 0; u < D; ++u) x[u] *= gamma;
-      gamma = 1.0f;
-    }
-  }
-#pragma unroll
-  for (int u = 0; u < D; ++u) x[u] *= gamma;
-
-  // ---- store the chunk-final state per its tier, natural rows 16 at a time
-  float s_g = 1.0f;
-  if constexpr (KIND == kNvfp4) {  // the global scale of the final low tier
-    float amax = 0.0f;
-#pragma unroll
-    for (int u = 0; u < D; ++u)
-      if (inv[u] >= k_hi) amax = fmaxf(amax, fabsf(x[u]));
-    s_g = nvfp4_global(block_max<128>(amax));
-    if (t == 0) store_global_scale<D>(meta_bytes, k_hi, s_g);
-  }
-#pragma unroll
-  for (int c = 0; c < D / 16; ++c) {
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int r = 0; r < 16; ++r) tbuf[r][col] = x[16 * c + r];
-    __syncthreads();
-    float sl[CPT];
-#pragma unroll
-    for (int q4 = 0; q4 < CPT / 4; ++q4) {
-      const float4 v4 = *reinterpret_cast<const float4*>(&tbuf[rr][col0 + 4 * q4]);
-      sl[4 * q4] = v4.x;
-      sl[4 * q4 + 1] = v4.y;
-      sl[4 * q4 + 2] = v4.z;
-      sl[4 * q4 + 3] = v4.w;
-    }
-    encode_row<KIND, D, CPT, TPR>(sl, inv[16 * c + rr], k_hi, cg, col0, tile, codes, meta_bytes,
-                                  had, s_g);
     __syncthreads();
   }
 }
 
 template <int KIND, bool KDA, int D>
 void launch(const PrefillParams& p, int B, hipStream_t stream) {
-  // the column kernel addresses one request's inputs with 32-bit offsets
+  // the block kernel addresses one request's inputs with 32-bit offsets
   const int64_t span = static_cast<int64_t>(p.t_pitch) * (p.HK > p.HV ? p.HK : p.HV) * D * 2;
-  if constexpr (D == 128 && !KDA) {
-    (void)span;
-    hipLaunchKernelGGL((prefill_gdn_sgpr128<KIND>), dim3(p.HV, B), dim3(128), 0, stream, p);
-    return;
-  } else if constexpr (D == 128) {
+  if constexpr (D == 128) {
     if (span <= INT32_MAX) {
-      hipLaunchKernelGGL((prefill_col128<KIND, KDA>), dim3(p.HV, B), dim3(256), 0, stream, p);
+      hipLaunchKernelGGL((prefill_blk128<KIND, KDA>), dim3(p.HV, B), dim3(256), 0, stream, p);
       return;
     }
   }

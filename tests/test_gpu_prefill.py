@@ -44,6 +44,13 @@ CASES = [
     (128, False, 2, 4, 2, 8, 16, orc.KIND_MIXED, orc.FMT_PAPER),
     (128, True, 2, 2, 2, 1, 32, orc.KIND_MIXED, None),
     (128, False, 2, 2, 2, 12, 0, orc.KIND_FP32, None),
+    # d = 128 runs in blocks of 8 tokens: a partial last block; GDN's decay
+    # product leaving [2^-40, 2^40] (renormalized); the other formats
+    (128, True, 2, 2, 2, 17, 12, orc.KIND_MIXED, None),
+    (128, False, 2, 2, 2, 48, 16, orc.KIND_MIXED, None),
+    (128, False, 2, 4, 3, 24, 16, orc.KIND_MIXED, orc.FMT_INT4_H32),
+    (128, True, 2, 2, 2, 9, 16, orc.KIND_MIXED, orc.FMT_FP8),
+    (128, False, 2, 2, 2, 11, 16, orc.KIND_MIXED, orc.FMT_NVFP4),
 ]
 
 
@@ -71,8 +78,9 @@ def test_prefill_parity(d, kda, HK, HV, B, T, k_hi, kind, fmt):
         assert err <= 1e-4  # identical starting bytes, no quantization inside the chunk
 
 
-def test_prefill_padded_requests_and_bf16_output():
-    d, HK, HV, B, T = 64, 2, 4, 3, 4
+@pytest.mark.parametrize("d,T", [(64, 4), (128, 10)])
+def test_prefill_padded_requests_and_bf16_output(d, T):
+    HK, HV, B = 2, 4, 3
     ref = orc.Pool(orc.KIND_MIXED, d, d, 8, 1, 4, HV)
     orc.pack(ref, 0, np.arange(4), inputs.synthetic_states(710, 4, HV, d))
     pad = 4096
