@@ -321,6 +321,25 @@ def sweep(torch, D, inputs, steps: int, log=print):
     return out
 
 
+def copy_ceiling(torch, nbytes: int, rotations: int, steps: int, log=print):
+    """The practical ceiling of the update's memory traffic: a plain device
+    copy (torch's) moving the same bytes, half read and half written, over
+    `rotations` disjoint source/destination pairs so that no copy is served
+    from the last-level cache; timed like the update (steady clock, HIP
+    events around `steps` launches)."""
+    half = nbytes // 2 // 16 * 16
+    src = [torch.empty(half, dtype=torch.uint8, device="cuda").fill_(r) for r in range(rotations)]
+    dst = [torch.empty_like(x) for x in src]
+    calls = [lambda i=i: dst[i].copy_(src[i]) for i in range(rotations)]
+    t = time_steps(torch, calls, 20, steps, prewarm_s=0.2)
+    sec = t["mean_launch_s"]
+    res = dict(bytes=2 * half, copy_us=round(1e6 * sec, 2), copy_gbs=round(2 * half / sec / 1e9, 1))
+    log(f"  copy of the same state bytes: {res['copy_us']} us, {res['copy_gbs']} GB/s")
+    del src, dst
+    torch.cuda.empty_cache()
+    return res
+
+
 def tp_share(torch, D, inputs, steps: int, log=print):
     """One GPU's share of an 8-way tensor-parallel deployment: B = 256 with 4
     of the 32 value heads (and 2 of 16 key heads for GDN), d = 128, 16
@@ -573,6 +592,10 @@ def main():
         f"{head['kernel_gbs']:.0f} GB/s ({100 * head['kernel_frac_peak']:.1f}% of peak)")
     extra = {}
     if not args.quick:
+        cop = copy_ceiling(torch, 2 * head["tile_bytes"] * B * HV, args.rotations, args.steps,
+                           log=log)
+        cop["update_frac_of_copy"] = round(cop["copy_us"] / head["kernel_us"], 4)
+        extra["practical_ceiling"] = cop
         scat = measure(torch, D, gdn, D.DAMP_STATE_MIXED, k_hi, args.rotations, args.warmup,
                        args.steps, torch.bfloat16, scattered=True)
         log(f"  mixed, slots scattered over the pool: kernel {scat['kernel_us']:.1f} us, "
