@@ -173,7 +173,7 @@ __device__ __forceinline__ void decode16(const W& w, float A, float B0, float (&
   }
 }
 
-// Operands of one tile as loaded by threads t < 128 (raw bf16 bits).
+// Operands of one tile as loaded by the operand threads (raw bf16 bits).
 struct OpsRegs {
   uint32_t k, q, g, v, beta;
 };
@@ -251,7 +251,7 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
   const int B = ntiles / HV;
   const int b_step = G / HV;
   const int k_hi = p.k_hi;
-  const bool hi0 = rg < k_hi;  // row slot 0 of this thread is in the bf16 tier
+  const bool hi0 = rg < k_hi;  // row slot 0 of this thread is in the 16-bit tier
   const int lo0 = k_hi * D * 2;
   const int meta0 = lo0 + (D - k_hi) * kCodeRow;
   const int off_gs = meta0 + (D - k_hi) * 8;  // NVFP4: the tile's fp32 global scale
@@ -261,7 +261,7 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
   const __attribute__((address_space(4))) int32_t* slots =
       (const __attribute__((address_space(4))) int32_t*)p.slot_idx;
 
-  // every lane of this wave has a low row slot 0 (no bf16 second half to
+  // every lane of this wave has a low row slot 0 (no 16-bit second half to
   // load or store), or every lane a high one
   const bool wave_lo = 8 * wave >= k_hi;
   const bool wave_hi = 8 * wave + 8 <= k_hi;
@@ -419,9 +419,10 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
   __amdgpu_buffer_rsrc_t rs_n1 = make_rsrc(slot_n1);
   bool done = false;
   int buf = 0, pb = 0;
-  // The re-encoded (s, z) of a tile (default tiers) are stored after the
-  // next tile's workgroup barrier, when every wave's rows are in mout: wave
-  // w writes the 256 contiguous bytes of rows k_hi + 32 w ..
+  // The re-encoded 8-byte metadata of a tile (the default tiers' (s, z),
+  // NVFP4's block scales) are stored after the next tile's workgroup
+  // barrier, when every wave's rows are in mout: wave w writes the 256
+  // contiguous bytes of rows k_hi + 32 w ..
   __amdgpu_buffer_rsrc_t rs_prev = make_rsrc(-1);
   auto store_prev_meta = [&](int pbuf) {
     if constexpr (!kP) {
@@ -816,8 +817,8 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
     }
     // metadata of the wave's rows: the group formats' 16 bytes per row go
     // through the wave's LDS slice (a wave's 8 consecutive rows make a whole
-    // 128-byte line); the default tiers' (s, z) into the tile's table, stored
-    // after the next barrier (store_prev_meta)
+    // 128-byte line); 8-byte metadata into the tile's table, stored after the
+    // next barrier (store_prev_meta)
     if constexpr (kP) {
       if ((cg & 1) == 0) {
 #pragma unroll
@@ -897,7 +898,7 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
     tile(ops_a, ops_b, set_2, set_a);
     if (done) break;
   }
-  // the last tile's (s, z), once every wave has put its rows in mout
+  // the last tile's 8-byte metadata, once every wave has put its rows in mout
   if constexpr (!kP) {
     lds_barrier();
     store_prev_meta(pb ^ 1);

@@ -207,3 +207,42 @@ def test_full_size_step(name, kda):
     stats = compare_tiles(gpool.buffer.cpu().numpy(), ref, f"full-size {name}")
     _say(f"  o rel-L2 {err:.2e}  {stats}")
     assert err <= O_TOL_MIXED and err <= 1e-4
+
+
+@pytest.mark.parametrize("name", ["default", "int8_h32", "int8_g32"] + STREAM_FORMATS)
+@pytest.mark.parametrize("zeroed", ["some", "low_tier"])
+def test_degenerate_rows_from_zero_state(name, zeroed):
+    """d = 128 (the pipelined kernel) from the reset state with key channels
+    set to zero: their rows stay exactly zero, so the quantizers take their
+    constant-row rules (R9; the FP16 group rules; FP8's floor on the scale;
+    NVFP4's zero block scale). With every low-tier channel zeroed (identity
+    permutation), NVFP4's tile maximum is 0 and its global scale 1."""
+    fmt = {"default": None, "int8_h32": orc.FMT_PAPER, "int8_g32": orc.FMT_PAPER_PLAIN,
+           **FORMATS}[name]
+    d, HK, HV, B, k_hi = 128, 2, 4, 3, 16
+    seed = 1600 + (zeroed == "low_tier")
+    _say(f"degenerate rows {name} zeroed={zeroed}")
+    slots = inputs.slot_order(seed, B + 2, B)
+    ref = orc.Pool(orc.KIND_MIXED, d, d, k_hi, 1, B + 2, HV, fmt=fmt)
+    ref.buf[:] = 0x5A
+    orc.reset(ref, 0, slots)
+    gpool = gpu_pool_from(ref, D)
+    inp = inputs.step(inputs.decode_inputs(seed, 1, B, HK, HV, d), 0)
+    if zeroed == "some":
+        perm = inputs.random_perms(seed, HV, d)
+        chans = np.random.default_rng(seed).choice(d, size=40, replace=False)
+    else:
+        perm = None
+        chans = np.arange(k_hi, d)
+    inp["k"] = inp["k"].copy()
+    inp["k"][..., chans] = 0
+    x = dev_inputs(inp)
+    o = torch.empty((B, HV, d), dtype=torch.float32, device="cuda")
+    D.damp_state_update_gdn(gpool, 0, dev_i32(slots), x["q"], x["k"], x["v"], x["g"], x["beta"],
+                            perm=None if perm is None else dev_u8(perm), o=o)
+    o_ref = orc.update(ref, 0, slots, kda=False, perm=perm, **inp)
+    torch.cuda.synchronize()
+    err = rel_l2(o.cpu().numpy(), o_ref)
+    stats = compare_tiles(gpool.buffer.cpu().numpy(), ref, f"degenerate {name}")
+    _say(f"  o rel-L2 {err:.2e}  {stats}")
+    assert err <= 1e-4
