@@ -57,6 +57,8 @@ def parse():
     ap.add_argument("--no-multilayer", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration)")
+    ap.add_argument("--cpu-only", type=float, default=0.0, metavar="SECONDS",
+                    help="only time the CPU oracle for SECONDS and print its JSON (no GPU)")
     return ap.parse_args()
 
 
@@ -562,8 +564,27 @@ def cpu_baseline(seconds: float, log=print):
                        f"(fp32 o), {el:.1f} s", ms_per_step=1e3 * el / n)
 
 
+def cpu_single_thread(seconds: float, log=print):
+    """The same oracle timing on one host thread, in a child process started
+    with OMP_NUM_THREADS=1 (the oracle's thread count is fixed when it loads)."""
+    import subprocess
+
+    env = dict(os.environ, OMP_NUM_THREADS="1")
+    r = subprocess.run([sys.executable, os.path.abspath(__file__), "--cpu-only", str(seconds)],
+                       env=env, capture_output=True, text=True, timeout=300)
+    if r.returncode != 0:
+        log(f"  cpu oracle, one thread: failed ({r.stderr.strip()[-200:]})")
+        return None
+    res = json.loads(r.stdout.strip().splitlines()[-1])
+    log(f"  cpu oracle, one thread: {res['ms_per_step']:.0f} ms per step")
+    return res
+
+
 def main():
     args = parse()
+    if args.cpu_only > 0:  # child of cpu_single_thread: no GPU work
+        print(json.dumps(cpu_baseline(args.cpu_only, log=lambda *a: None)), flush=True)
+        return
     global PREWARM_S
     PREWARM_S = args.prewarm
     if args.gpus != 1:
@@ -653,6 +674,10 @@ def main():
     cpu = None
     if not args.quick and not args.no_cpu:
         cpu = cpu_baseline(args.cpu_seconds, log=log)
+        one = cpu_single_thread(min(args.cpu_seconds, 10.0), log=log)
+        if cpu is not None and one is not None:
+            cpu["one_thread"] = {"value": one["value"], "unit": one["unit"],
+                                 "cores": one["cores"], "ms_per_step": one["ms_per_step"]}
 
     traffic = profile_traffic()
     out = {
