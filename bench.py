@@ -342,6 +342,40 @@ def copy_ceiling(torch, nbytes: int, rotations: int, steps: int, log=print):
     return res
 
 
+def pack_unpack_bench(torch, D, steps: int, log=print):
+    """Pack (natural-order FP32 state -> packed tiles, Eq. (3)) and unpack
+    (packed -> FP32) of the B=256, 32-head, d=128 GDN state with 16 BF16
+    rows, each launch moving the FP32 state (537 MB) one way and the packed
+    tiles (158 MB) the other; two FP32 buffers and two pool halves alternate
+    so that no launch is served from the last-level cache."""
+    B, HV, d, k_hi = 256, 32, 128, 16
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(21)
+    S = [torch.randn((B, HV, d, d), generator=gen, device="cuda") * 0.1 for _ in range(2)]
+    from paper_2608_27513_amd import inputs
+    perm = torch.from_numpy(inputs.random_perms(21, HV, d)).cuda()
+    layout = D.damp_layout_init(d, d, k_hi)
+    pool = D.Pool(layout, 1, 2 * B, HV)
+    sets = [torch.arange(r * B, (r + 1) * B, dtype=torch.int32, device="cuda") for r in range(2)]
+    tb = D.damp_tile_bytes(layout)
+    nbytes = B * HV * (d * d * 4 + tb)
+    out = {}
+    for name, calls in (
+            ("pack", [lambda i=i: D.damp_state_pack(pool, 0, sets[i], S[i], perm) for i in range(2)]),
+            ("unpack", [lambda i=i: D.damp_state_unpack(pool, 0, sets[i], perm, S[i])
+                        for i in range(2)])):
+        t = time_steps(torch, calls, 5, steps, prewarm_s=0.1)
+        sec = t["mean_launch_s"]
+        out[name] = dict(kernel_us=round(1e6 * sec, 1), GBs=round(nbytes / sec / 1e9, 1),
+                         frac_hbm_peak=round(nbytes / sec / 1e9 / HBM_PEAK_GBS, 4))
+    out["bytes_per_launch"] = nbytes
+    log(f"  pack {out['pack']['kernel_us']} us ({out['pack']['GBs']} GB/s), "
+        f"unpack {out['unpack']['kernel_us']} us ({out['unpack']['GBs']} GB/s)")
+    del S, pool
+    torch.cuda.empty_cache()
+    return out
+
+
 def tp_share(torch, D, inputs, steps: int, log=print):
     """One GPU's share of an 8-way tensor-parallel deployment: B = 256 with 4
     of the 32 value heads (and 2 of 16 key heads for GDN), d = 128, 16
@@ -669,6 +703,7 @@ def main():
         if not args.no_multilayer:
             extra["multilayer_48"] = multilayer(torch, D, inputs, 64, log=log)
         extra["prefill_gdn"] = prefill_bench(torch, D, inputs, 10, log=log)
+        extra["pack_unpack_gdn"] = pack_unpack_bench(torch, D, 20, log=log)
         extra["calibration_kda"] = calibration_bench(torch, D, inputs, log=log)
 
     cpu = None
