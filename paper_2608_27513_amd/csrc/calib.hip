@@ -51,34 +51,15 @@ struct CalibParams {
   int32_t had;           // block-32 transform of each group
 };
 
-// Normalized block-32 Hadamard transform written out as its definition:
-// y_i = 32^(-1/2) sum_j (-1)^popcount(i & j) x_j, summed in ascending j.
-__device__ __forceinline__ void hadamard32_direct(const float (&x)[32], float (&y)[32]) {
-#pragma unroll
-  for (int i = 0; i < 32; ++i) {
-    float acc = 0.0f;
-#pragma unroll
-    for (int j = 0; j < 32; ++j)
-      acc = (__builtin_popcount(static_cast<unsigned>(i & j)) & 1) ? __fsub_rn(acc, x[j])
-                                                                   : __fadd_rn(acc, x[j]);
-    y[i] = __fmul_rn(acc, kInvSqrt32);
-  }
-}
-
-// s and z of Eq. (3) for n values, IEEE division; constant and zero groups
-// as for the stored tiers.
-__device__ __forceinline__ void qparams_exact(const float* x, int n, float& lo, float& s) {
-  lo = x[0];
-  float hi = x[0];
-  for (int j = 1; j < n; ++j) {
-    if (x[j] < lo) lo = x[j];
-    if (x[j] > hi) hi = x[j];
-  }
-  s = __fdiv_rn(__fsub_rn(hi, lo), 255.0f);
+// s of Eq. (3) from a row's or group's extrema, IEEE division; constant and
+// zero groups as for the stored tiers.
+__device__ __forceinline__ float qscale_exact(float lo, float hi) {
+  float s = __fdiv_rn(__fsub_rn(hi, lo), 255.0f);
   if (!(s >= FLT_MIN)) {
     s = __fdiv_rn(fabsf(lo), 255.0f);
     if (!(s >= FLT_MIN)) s = 1.0f;
   }
+  return s;
 }
 
 __device__ __forceinline__ float decode_exact(float x, float s, float z) {
@@ -87,64 +68,152 @@ __device__ __forceinline__ float decode_exact(float x, float s, float z) {
   return __fmul_rn(s, __fsub_rn(c, z));
 }
 
-__device__ __forceinline__ double sq_err(double acc, float xh, float x) {
+// (xh - x)^2 in double, the term of || Q_lo(x) - x ||^2
+__device__ __forceinline__ double sq_term(float xh, float x) {
   const double e = __dsub_rn(static_cast<double>(xh), static_cast<double>(x));
-  return __dadd_rn(acc, __dmul_rn(e, e));
+  return __dmul_rn(e, e);
 }
 
-// || Q_lo(x) - x ||^2 for the default low tier: one fp32 (s, z) per row.
-__device__ double row_err_rowwise(const float* x, int n) {
-  float lo, s;
-  qparams_exact(x, n, lo, s);
-  const float z = rintf(__fdiv_rn(-lo, s));
-  double acc = 0.0;
-  for (int j = 0; j < n; ++j) acc = sq_err(acc, decode_exact(x[j], s, z), x[j]);
-  return acc;
-}
-
-// || Q_lo(x) - x ||^2 for the paper's low tier: groups of 32 with FP16
-// (s, z) taken from the stored (rounded) values, optionally in the
-// transformed domain (the reconstruction is transformed back).
-__device__ double row_err_paper(const float* x, int n, bool had) {
-  double acc = 0.0;
-  for (int g0 = 0; g0 < n; g0 += 32) {
-    float xg[32], y[32], yh[32], xh[32];
+// Extrema over the lanes whose bit `span` and above agree (span = 64: the
+// wave, 32: each half).
+template <int SPAN>
+__device__ __forceinline__ void lane_minmax(float& lo, float& hi) {
 #pragma unroll
-    for (int j = 0; j < 32; ++j) xg[j] = x[g0 + j];
-    if (had) hadamard32_direct(xg, y);
-    else {
-#pragma unroll
-      for (int j = 0; j < 32; ++j) y[j] = xg[j];
-    }
-    float lo, s;
-    qparams_exact(y, 32, lo, s);
-    float s16 = round_f16(s);
-    if (!(s16 > 0.0f)) s16 = 5.9604644775390625e-08f;  // smallest positive FP16
-    if (s16 > 65504.0f) s16 = 65504.0f;
-    float zf = rintf(__fdiv_rn(-lo, s16));
-    if (zf > 65504.0f) zf = 65504.0f;
-    if (zf < -65504.0f) zf = -65504.0f;
-    const float z16 = round_f16(zf);
-#pragma unroll
-    for (int j = 0; j < 32; ++j) yh[j] = decode_exact(y[j], s16, z16);
-    if (had) hadamard32_direct(yh, xh);
-    else {
-#pragma unroll
-      for (int j = 0; j < 32; ++j) xh[j] = yh[j];
-    }
-#pragma unroll
-    for (int j = 0; j < 32; ++j) acc = sq_err(acc, xh[j], xg[j]);
+  for (int m = 1; m < SPAN; m <<= 1) {
+    lo = fminf(lo, __shfl_xor(lo, m, 64));
+    hi = fmaxf(hi, __shfl_xor(hi, m, 64));
   }
-  return acc;
 }
 
-// One workgroup per (head, tile row). Threads evaluate up to 256 samples at
-// a time into LDS; thread 0 then adds them to the accumulators in sample
-// order, continuing from the values already stored.
+// Per-wave scratch for the statistics of one row sample (d_v <= 128).
+struct RowScratch {
+  float x[128];   // the row
+  float yh[128];  // paper tiers with the transform: the reconstruction, transformed domain
+  double te[128];  // per column: (Q_lo(x) - x)^2
+  double tn[128];  // per column: x^2
+};
+
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+}
+
+// || Q_lo(x) - x ||^2 and || x ||^2 of one row by one wave, a lane per column
+// (columns lane, lane + 64). Every per-column operation is written out as
+// the definition: the row's (or, for the paper's tiers, each group of 32's)
+// s and z of Eq. (3) with IEEE division, the FP16 rounding of the stored
+// group (s, z), the normalized block-32 transform as its direct sum over
+// ascending j, and the reconstruction s (c - z). The extrema are order-free;
+// the two sums over the columns run in ascending column order in one lane
+// each (lanes 0 and 32). Returns the sums in those two lanes.
+__device__ void row_stats_wave(const float* xrow, int dv, bool paper, bool had, RowScratch& sc,
+                               int lane, double& err, double& en) {
+  for (int j = lane; j < dv; j += 64) sc.x[j] = xrow[j];
+  wave_sync();
+  if (!paper) {
+    float lo = INFINITY, hi = -INFINITY;
+    for (int j = lane; j < dv; j += 64) {
+      lo = fminf(lo, sc.x[j]);
+      hi = fmaxf(hi, sc.x[j]);
+    }
+    lane_minmax<64>(lo, hi);
+    const float s = qscale_exact(lo, hi);
+    const float z = rintf(__fdiv_rn(-lo, s));
+    for (int j = lane; j < dv; j += 64) {
+      const float xv = sc.x[j];
+      sc.te[j] = sq_term(decode_exact(xv, s, z), xv);
+      sc.tn[j] = __dmul_rn(static_cast<double>(xv), static_cast<double>(xv));
+    }
+  } else {
+    // lane holds output i = j % 32 of group j / 32, for j = lane + 64 m; the
+    // 32 lanes of a half-wave hold one group
+    float y[2], yh[2];
+    const int nm = (dv + 63) / 64;
+#pragma unroll
+    for (int m = 0; m < 2; ++m) {
+      const int j = lane + 64 * m;
+      if (m >= nm || j >= dv) {
+        y[m] = 0.0f;
+        continue;
+      }
+      const int base = j & ~31, i = j & 31;
+      if (had) {
+        float acc = 0.0f;
+        for (int jj = 0; jj < 32; ++jj)
+          acc = (__builtin_popcount(static_cast<unsigned>(i & jj)) & 1) ? __fsub_rn(acc, sc.x[base + jj])
+                                                                        : __fadd_rn(acc, sc.x[base + jj]);
+        y[m] = __fmul_rn(acc, kInvSqrt32);
+      } else {
+        y[m] = sc.x[j];
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < 2; ++m) {
+      const int j = lane + 64 * m;
+      const bool on = m < nm && j < dv;
+      float lo = on ? y[m] : INFINITY, hi = on ? y[m] : -INFINITY;
+      lane_minmax<32>(lo, hi);
+      if (!on) {
+        yh[m] = 0.0f;
+        continue;
+      }
+      const float s = qscale_exact(lo, hi);
+      float s16 = round_f16(s);
+      if (!(s16 > 0.0f)) s16 = 5.9604644775390625e-08f;  // smallest positive FP16
+      if (s16 > 65504.0f) s16 = 65504.0f;
+      float zf = rintf(__fdiv_rn(-lo, s16));
+      if (zf > 65504.0f) zf = 65504.0f;
+      if (zf < -65504.0f) zf = -65504.0f;
+      const float z16 = round_f16(zf);
+      yh[m] = decode_exact(y[m], s16, z16);
+    }
+    if (had) {
+      for (int m = 0; m < nm; ++m) {
+        const int j = lane + 64 * m;
+        if (j < dv) sc.yh[j] = yh[m];
+      }
+      wave_sync();
+    }
+    for (int m = 0; m < nm; ++m) {
+      const int j = lane + 64 * m;
+      if (j >= dv) continue;
+      float xh = yh[m];
+      if (had) {  // back from the transformed domain, the same direct sum
+        const int base = j & ~31, i = j & 31;
+        float acc = 0.0f;
+        for (int jj = 0; jj < 32; ++jj)
+          acc = (__builtin_popcount(static_cast<unsigned>(i & jj)) & 1) ? __fsub_rn(acc, sc.yh[base + jj])
+                                                                        : __fadd_rn(acc, sc.yh[base + jj]);
+        xh = __fmul_rn(acc, kInvSqrt32);
+      }
+      const float xv = sc.x[j];
+      sc.te[j] = sq_term(xh, xv);
+      sc.tn[j] = __dmul_rn(static_cast<double>(xv), static_cast<double>(xv));
+    }
+  }
+  wave_sync();
+  // ascending sums: lane 0 the error terms, lane 32 the energies
+  double acc = 0.0;
+  if (lane == 0 || lane == 32) {
+    const double* src = lane == 0 ? sc.te : sc.tn;
+    for (int j = 0; j < dv; ++j) acc = __dadd_rn(acc, src[j]);
+  }
+  err = acc;
+  en = acc;
+  wave_sync();  // the scratch is reused by the wave's next sample
+}
+
+// One workgroup per (head, tile row). Its four waves evaluate up to 256
+// samples at a time, one sample per wave at a time, into LDS; thread 0 then
+// adds them to the accumulators in sample order, continuing from the values
+// already stored.
 __global__ __launch_bounds__(kCalibThreads) void calib_accumulate_kernel(const CalibParams p) {
   __shared__ double se[kCalibThreads], sn[kCalibThreads], sl[kCalibThreads];
   __shared__ int sv[kCalibThreads];
-  const int t = threadIdx.x;
+  __shared__ RowScratch scr[kCalibThreads / 64];
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int h = blockIdx.x / p.dk;
   const int r = blockIdx.x % p.dk;
   const int u = p.perm ? static_cast<int>(p.perm[static_cast<size_t>(h) * p.dk + r]) : r;
@@ -156,29 +225,29 @@ __global__ __launch_bounds__(kCalibThreads) void calib_accumulate_kernel(const C
     acc_l = p.loga[hu];
   }
   for (int b0 = 0; b0 < p.B; b0 += kCalibThreads) {
-    const int b = b0 + t;
-    int valid = 0;
-    if (b < p.B) {
+    const int n = min(kCalibThreads, p.B - b0);
+    for (int i = wave; i < n; i += kCalibThreads / 64) {
+      const int b = b0 + i;
       const int slot = p.slot_idx[b];
-      if (slot >= 0 && slot < p.num_slots) {
-        valid = 1;
+      const bool valid = slot >= 0 && slot < p.num_slots;
+      if (valid) {
         const float* x = reinterpret_cast<const float*>(
             p.layer_base + static_cast<size_t>(slot) * p.slot_stride +
             static_cast<size_t>(h) * p.tile_stride) + static_cast<size_t>(r) * p.dv;
-        se[t] = p.paper ? row_err_paper(x, p.dv, p.had != 0) : row_err_rowwise(x, p.dv);
-        double e2 = 0.0;
-        for (int j = 0; j < p.dv; ++j)
-          e2 = __dadd_rn(e2, __dmul_rn(static_cast<double>(x[j]), static_cast<double>(x[j])));
-        sn[t] = e2;
-        const uint16_t gb = p.is_kda ? p.g[b * p.g_bstride + static_cast<int64_t>(h) * p.dk + u]
-                                     : p.g[b * p.g_bstride + h];
-        sl[t] = static_cast<double>(bf16_to_f32(gb));
+        double e = 0.0, e2 = 0.0;
+        row_stats_wave(x, p.dv, p.paper != 0, p.had != 0, scr[wave], lane, e, e2);
+        if (lane == 0) {
+          se[i] = e;
+          const uint16_t gb = p.is_kda ? p.g[b * p.g_bstride + static_cast<int64_t>(h) * p.dk + u]
+                                       : p.g[b * p.g_bstride + h];
+          sl[i] = static_cast<double>(bf16_to_f32(gb));
+        }
+        if (lane == 32) sn[i] = e2;
       }
+      if (lane == 0) sv[i] = valid ? 1 : 0;
     }
-    sv[t] = valid;
     __syncthreads();
     if (t == 0) {
-      const int n = min(kCalibThreads, p.B - b0);
       for (int i = 0; i < n; ++i) {
         if (!sv[i]) continue;
         acc_e = __dadd_rn(acc_e, se[i]);

@@ -46,12 +46,14 @@ def _device_sums(cal):
     return h[:D_ * 3 * H * d].reshape(D_, 3, H, d), h[D_ * 3 * H * d:]
 
 
-@pytest.mark.parametrize("kda,fmt", [(False, None), (True, None), (False, orc.FMT_PAPER),
-                                     (True, orc.FMT_PAPER), (True, orc.FMT_PAPER_PLAIN)])
-def test_accumulate_and_finalize_are_bit_exact(kda, fmt):
-    d, H, B = 64, 4, 5
-    _say(f"calib accumulate kda={kda} fmt={fmt}")
-    seed = 800 + 3 * kda + (0 if fmt is None else fmt[3] + 1)
+@pytest.mark.parametrize("kda,fmt,d", [(False, None, 64), (True, None, 64), (False, orc.FMT_PAPER, 64),
+                                       (True, orc.FMT_PAPER, 64), (True, orc.FMT_PAPER_PLAIN, 64),
+                                       (False, None, 128), (True, orc.FMT_PAPER, 128),
+                                       (False, orc.FMT_PAPER_PLAIN, 32), (True, None, 16)])
+def test_accumulate_and_finalize_are_bit_exact(kda, fmt, d):
+    H, B = 4, 5
+    _say(f"calib accumulate kda={kda} fmt={fmt} d={d}")
+    seed = 800 + 3 * kda + (0 if fmt is None else fmt[3] + 1) + d
     cal = D.Calib(_layout(d, fmt), kda=kda, num_heads=H, num_domains=2)
     ref = orc.Calib(kda=kda, H=H, dk=d, dv=d, num_domains=2, fmt=fmt)
     rng = np.random.default_rng(seed)
