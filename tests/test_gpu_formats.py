@@ -85,7 +85,8 @@ def test_reset_matches_oracle_bytes(name):
 
 @pytest.mark.parametrize("name", list(FORMATS))
 @pytest.mark.parametrize("kda,d,HK,HV,B,k_hi", [(False, 128, 2, 4, 3, 16), (True, 64, 2, 2, 2, 8),
-                                                (False, 32, 1, 2, 2, 0)])
+                                                (False, 32, 1, 2, 2, 0),
+                                                (True, 128, 2, 2, 2, 40)])  # K_hi > 32: generic kernel
 def test_single_step_parity(name, kda, d, HK, HV, B, k_hi):
     fmt = FORMATS[name]
     _say(f"format step {name} kda={kda} d={d} HK={HK} HV={HV} B={B} k_hi={k_hi}")
