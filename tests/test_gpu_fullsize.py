@@ -4,8 +4,9 @@ The GDN workload (B=256, 16 key / 32 value heads, d=128, 16 BF16 rows, 8
 outlier channels per head at 10x) and the KDA workload (B=256, 32 heads, per-channel
 decay with ~10% persistent channels, 16 channels chosen by the selection).
 The oracle packs every tile and runs the whole step, so every output and
-every stored byte is compared. Also the largest batch a launch takes and the
-empty batch.
+every stored byte is compared; the same for the paper's tiers. Also the
+largest batch a launch takes, the empty batch, and the prefill of a 64-token
+chunk for the whole batch, checked on sampled requests.
 """
 import numpy as np
 import pytest
@@ -125,3 +126,74 @@ def test_many_tiles_per_workgroup_with_padding(kda, k_hi, o_bf16):
     assert rel_l2(o_gpu, o_ref) <= tol
     stats = compare_tiles(gpool.buffer.cpu().numpy(), ref, "padded batch")
     _say(f"  o rel-L2 {rel_l2(o_gpu, o_ref):.2e} {stats}")
+
+
+@pytest.mark.parametrize("fmt", [orc.FMT_PAPER, orc.FMT_PAPER_PLAIN])
+@pytest.mark.parametrize("kda", [False, True])
+def test_full_size_step_paper_tiers(kda, fmt):
+    """The decode workload in the paper's tiers (FP16 rows, groups of 32 with
+    FP16 (s, z), with and without the block-32 transform), every output and
+    stored byte compared."""
+    B, HV, d, k_hi = 256, 32, 128, 16
+    HK = HV if kda else 16
+    seed = 20 + kda + 2 * fmt[3]
+    _say(f"full-size paper tiers kda={kda} had={fmt[3]}")
+    S = inputs.synthetic_states(seed, B, HV, d)
+    inputs.scale_channels(S, inputs.outlier_channels(seed, HV, d, 8), 10.0)
+    perm = inputs.random_perms(seed, HV, d)
+    slots = inputs.slot_order(seed, B, B)
+    ref = orc.Pool(orc.KIND_MIXED, d, d, k_hi, 1, B, HV, fmt=fmt)
+    orc.pack(ref, 0, slots, S, perm)
+    del S
+    gpool = gpu_pool_from(ref, D)
+    inp = inputs.step(inputs.decode_inputs(seed, 1, B, HK, HV, d, kda=kda), 0)
+    di = dev_inputs(inp)
+    o = torch.empty((B, HV, d), dtype=torch.float32, device="cuda")
+    fn = D.damp_state_update_kda if kda else D.damp_state_update_gdn
+    fn(gpool, 0, dev_i32(slots), di["q"], di["k"], di["v"], di["g"], di["beta"],
+       perm=dev_u8(perm), o=o)
+    torch.cuda.synchronize()
+    _say("  gpu step done; running the oracle")
+    o_ref = orc.update(ref, 0, slots, kda=kda, perm=perm, **inp)
+    err = rel_l2(o.cpu().numpy(), o_ref)
+    stats = compare_tiles(gpool.buffer.cpu().numpy(), ref, "full-size paper tiers")
+    _say(f"  o rel-L2 {err:.2e}  {stats}")
+    assert err <= O_TOL_MIXED and err <= 1e-4
+
+
+@pytest.mark.parametrize("kda", [False, True])
+def test_full_size_prefill_sampled(kda):
+    """The prefill in the benchmark's launch configuration (B = 256, 16 or 32
+    key and 32 value heads, d = 128, 16 BF16 rows, one 64-token chunk per
+    request): the GPU runs every request; the oracle runs four sampled
+    requests from the same starting bytes, and their outputs and stored
+    tiles are compared."""
+    B, HV, d, k_hi, T = 256, 32, 128, 16, 64
+    HK = HV if kda else 16
+    seed = 30 + kda
+    _say(f"full-size prefill kda={kda}: B={B} HK={HK} HV={HV} d={d} T={T}")
+    S = inputs.synthetic_states(seed, B, HV, d)
+    perm = inputs.random_perms(seed, HV, d)
+    slots = inputs.slot_order(seed, B, B)
+    full = orc.Pool(orc.KIND_MIXED, d, d, k_hi, 1, B, HV)
+    orc.pack(full, 0, slots, S, perm)
+    gpool = gpu_pool_from(full, D)
+    inp = inputs.as_prefill(inputs.decode_inputs(seed, T, B, HK, HV, d, kda=kda))
+    di = dev_inputs(inp)
+    o = torch.empty((B, T, HV, d), dtype=torch.float32, device="cuda")
+    fn = D.damp_state_prefill_kda if kda else D.damp_state_prefill_gdn
+    fn(gpool, 0, dev_i32(slots), di["q"], di["k"], di["v"], di["g"], di["beta"],
+       perm=dev_u8(perm), o=o)
+    torch.cuda.synchronize()
+    _say("  gpu chunk done; running the oracle on the sampled requests")
+    pick = np.array([0, 77, 150, 255])
+    ref = orc.Pool(orc.KIND_MIXED, d, d, k_hi, 1, len(pick), HV)
+    orc.pack(ref, 0, np.arange(len(pick)), S[pick], perm)
+    del S
+    o_ref = orc.prefill(ref, 0, np.arange(len(pick)), kda=kda, perm=perm,
+                        **{n: a[pick] for n, a in inp.items()})
+    err = rel_l2(o.cpu().numpy()[pick], o_ref)
+    got = gpool.buffer.cpu().numpy().reshape(B, -1)[slots[pick]].reshape(-1)
+    stats = compare_tiles(got, ref, "full-size prefill", s16_exact_min=0.99)
+    _say(f"  o rel-L2 {err:.2e}  {stats}")
+    assert err <= 1e-4
