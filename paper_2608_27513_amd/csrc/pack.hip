@@ -72,6 +72,8 @@ __global__ __launch_bounds__(Shape<D>::NT) void pack_kernel(const TileParams p) 
 template <int KIND, int D>
 __global__ __launch_bounds__(Shape<D>::NT) void unpack_kernel(const TileParams p) {
   using Sh = Shape<D>;
+  // d = 128: per wave, its 8 rows of one row slot in transit to the stores
+  __shared__ float ubuf[D == 128 ? Sh::NT / 64 : 1][D == 128 ? 8 * D : 1];
   const int t = threadIdx.x, h = blockIdx.x, b = blockIdx.y;
   const int cg = t % Sh::TPR, rg = t / Sh::TPR, col0 = cg * Sh::CPT;
   const int slot = p.slot_idx[b];
@@ -176,7 +178,35 @@ __global__ __launch_bounds__(Shape<D>::NT) void unpack_kernel(const TileParams p
         out[4 * j + 3] = __float_as_uint(__fmul_rn(sz.x, __fsub_rn(ubyte<3>(w[j]), sz.y)));
       }
     }
-    store_words<Sh::CPT * 4>(reinterpret_cast<uint8_t*>(dst + static_cast<size_t>(u) * D + col0), out);
+    if constexpr (D == 128 && Sh::NT == 256) {
+      // through the wave's LDS slice, so that every store instruction writes
+      // two whole 512-byte rows: lane l writes 16 bytes at chunk l (+ 64 m)
+      // of the wave's 8 rows of this slot
+      const int lane = t & 63, wv = t >> 6;
+      float4* rows = reinterpret_cast<float4*>(&ubuf[wv][0]);
+#pragma unroll
+      for (int k = 0; k < Sh::CPT / 4; ++k)
+        rows[(rg & 7) * (D / 4) + cg * (Sh::CPT / 4) + k] =
+            make_float4(__uint_as_float(out[4 * k]), __uint_as_float(out[4 * k + 1]),
+                        __uint_as_float(out[4 * k + 2]), __uint_as_float(out[4 * k + 3]));
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const int c = lane + 64 * m;  // chunk: row c / 32 of the wave, columns 4 (c % 32) ..
+        const int rr = 8 * wv + (c >> 5) + Sh::RG * i;
+        const int uu =
+            p.perm ? (static_cast<int>(p.perm[static_cast<size_t>(h) * D + rr]) & (D - 1)) : rr;
+        *reinterpret_cast<float4*>(dst + static_cast<size_t>(uu) * D + 4 * (c & 31)) = rows[c];
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+    } else {
+      store_words<Sh::CPT * 4>(reinterpret_cast<uint8_t*>(dst + static_cast<size_t>(u) * D + col0),
+                               out);
+    }
   }
 }
 
