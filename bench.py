@@ -480,16 +480,19 @@ def multilayer(torch, D, inputs, steps: int, log=print):
     return res
 
 
-def prefill_bench(torch, D, inputs, steps: int, log=print, T: int = 64):
+def prefill_bench(torch, D, inputs, steps: int, log=print, T: int = 64, kda: bool = False):
     """Prefill of one T-token chunk per request (App. A.5, prefill path) on
-    the B=256 GDN workload (16 key / 32 value heads, d=128, 16 BF16 rows):
+    the B=256 GDN workload (16 key / 32 value heads, d=128, 16 BF16 rows) or
+    the KDA one (32 heads, per-channel decay):
     decode the stored state once, T fp32 steps, store once. Reports tokens per
     second and the fp32 rate (7 flops per state value and token: decay, two
     read-outs, the update), against the vector fp32 peak."""
-    B, HK, HV, d, k_hi = 256, 16, 32, 128, 16
+    B, HV, d, k_hi = 256, 32, 128, 16
+    HK = HV if kda else 16
     gen = torch.Generator(device="cuda")
     gen.manual_seed(11)
-    steps_in = [inputs.decode_inputs_device(gen, B, HK, HV, d) for _ in range(T)]
+    mu = torch.from_numpy(inputs.kda_mu(1, HV, d)).cuda() if kda else None
+    steps_in = [inputs.decode_inputs_device(gen, B, HK, HV, d, kda=kda, mu=mu) for _ in range(T)]
     x = {name: torch.stack([s_[name] for s_ in steps_in], dim=1).contiguous()
          for name in steps_in[0]}
     del steps_in
@@ -503,16 +506,17 @@ def prefill_bench(torch, D, inputs, steps: int, log=print, T: int = 64):
         D.damp_state_pack(pool, 0, sl, S, perm)
     del S
     o = torch.empty((B, T, HV, d), dtype=torch.bfloat16, device="cuda")
-    calls = [lambda sl=sl: D.damp_state_prefill_gdn(pool, 0, sl, x["q"], x["k"], x["v"], x["g"],
-                                                    x["beta"], perm=perm, o=o) for sl in sets]
+    fn = D.damp_state_prefill_kda if kda else D.damp_state_prefill_gdn
+    calls = [lambda sl=sl: fn(pool, 0, sl, x["q"], x["k"], x["v"], x["g"], x["beta"], perm=perm,
+                              o=o) for sl in sets]
     t = time_steps(torch, calls, 3, steps)
     sec = t["mean_launch_s"]
     flops = 7.0 * d * d * B * HV * T
     res = dict(B=B, T=T, HK=HK, HV=HV, d=d, k_hi=k_hi, chunk_us=round(1e6 * sec, 1),
                tokens_per_s=round(B * T / sec), tflops=round(flops / sec / 1e12, 2),
                frac_fp32_vector_peak=round(flops / sec / 157.3e12, 4))
-    log(f"  prefill T={T}: {res['chunk_us']} us per chunk, {res['tokens_per_s']:.3g} tokens/s, "
-        f"{res['tflops']} TFLOP/s")
+    log(f"  prefill {'KDA' if kda else 'GDN'} T={T}: {res['chunk_us']} us per chunk, "
+        f"{res['tokens_per_s']:.3g} tokens/s, {res['tflops']} TFLOP/s")
     del pool, x, o
     torch.cuda.empty_cache()
     return res
@@ -703,6 +707,7 @@ def main():
         if not args.no_multilayer:
             extra["multilayer_48"] = multilayer(torch, D, inputs, 64, log=log)
         extra["prefill_gdn"] = prefill_bench(torch, D, inputs, 10, log=log)
+        extra["prefill_kda"] = prefill_bench(torch, D, inputs, 10, log=log, kda=True)
         extra["pack_unpack_gdn"] = pack_unpack_bench(torch, D, 20, log=log)
         extra["calibration_kda"] = calibration_bench(torch, D, inputs, log=log)
 
