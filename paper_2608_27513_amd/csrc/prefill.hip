@@ -260,6 +260,7 @@ __global__ __launch_bounds__(256) void prefill_blk128(const PrefillParams p) {
     float4 v[TB][D / 4];
     float4 a[NA][D / 4];
     float4 sc[TB];  // beta, alpha (GDN), q~ . k~ over rows 0..63 and 64..127
+    float4 ge[KDA ? D / 4 : 1];  // KDA, deferred decay: each row's product over the block
   };
   constexpr int kTbufFloats = 32 * (D + 4);
   constexpr int kOpFloats = 2 * static_cast<int>(sizeof(OpBuf) / 4);
@@ -392,11 +393,48 @@ __global__ __launch_bounds__(256) void prefill_blk128(const PrefillParams p) {
     }
   };
 
+  // KDA: the decays of a block are deferred per row. The lanes keep P with
+  // S = G P, G_r(t) the product of row r's decays over the block's tokens up
+  // to t; the staged operands become k~ G, q~ G (read-outs) and k~ / G (the
+  // update), and the block ends with x *= G_r(end). A block in which some
+  // G leaves [2^-60, 2^60] keeps the per-token decay (returns 1).
+  auto cumulate = [&](int par, int ntok_) -> int {
+    OpBuf& B_ = ob[par];
+    bool ok = true;
+    if (t < D) {
+      float G = 1.0f;
+      for (int tb = 0; tb < ntok_; ++tb) {
+        G *= reinterpret_cast<const float*>(B_.a[tb])[t];
+        ok = ok && G >= 8.6736174e-19f && G <= 1.1529215e18f;
+      }
+    }
+    const int slow = __syncthreads_or(ok ? 0 : 1);
+    if (!slow && t < D) {
+      float G = 1.0f;
+      for (int tb = 0; tb < ntok_; ++tb) {
+        float* kk_ = reinterpret_cast<float*>(B_.k[tb]);
+        float* qq_ = reinterpret_cast<float*>(B_.q[tb]);
+        float* aa_ = reinterpret_cast<float*>(B_.a[tb]);
+        G *= aa_[t];
+        const float kf = kk_[t];
+        kk_[t] = kf * G;
+        qq_[t] = qq_[t] * G;
+        aa_[t] = kf * refined_rcp(G);
+      }
+      reinterpret_cast<float*>(B_.ge)[t] = G;
+    }
+    return slow;
+  };
   const int nblk = (T + TB - 1) / TB;
   BlkOps cur;
+  int slow_cur = 1;
   if (nblk > 0) {
     load_blk(cur, 0);
     publish_blk(cur, 0, 0);
+    if constexpr (KDA) {
+      __syncthreads();
+      slow_cur = cumulate(0, T < TB ? T : TB);
+    }
   }
   __syncthreads();
   float gamma = 1.0f;
@@ -418,7 +456,7 @@ __global__ __launch_bounds__(256) void prefill_blk128(const PrefillParams p) {
         kr[4 * j + 2] = k4.z;
         kr[4 * j + 3] = k4.w;
       }
-      if constexpr (KDA) {  // the decay of each row
+      if (KDA && slow_cur) {  // the decay of each row, per token
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const float4 a4 = B_.a[KDA ? tb : 0][4 * rb + j];
@@ -481,7 +519,18 @@ __global__ __launch_bounds__(256) void prefill_blk128(const PrefillParams p) {
         cf[c] = bg * delta;
       }
       write_o(tok, ov);
-      // rank-1 update S = S_bar + beta k~ delta^T (GDN: on P = S / gamma)
+      // rank-1 update S = S_bar + beta k~ delta^T (GDN: on P = S / gamma;
+      // KDA with deferred decay: on P = S / G with k~ / G)
+      if (KDA && !slow_cur) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float4 b4 = B_.a[KDA ? tb : 0][4 * rb + j];
+          kr[4 * j] = b4.x;
+          kr[4 * j + 1] = b4.y;
+          kr[4 * j + 2] = b4.z;
+          kr[4 * j + 3] = b4.w;
+        }
+      }
 #pragma unroll
       for (int i = 0; i < 16; ++i)
 #pragma unroll
@@ -494,8 +543,28 @@ __global__ __launch_bounds__(256) void prefill_blk128(const PrefillParams p) {
         gamma = 1.0f;
       }
     }
-    if (blk + 1 < nblk) publish_blk(cur, blk + 1, par ^ 1);
+    if (KDA && !slow_cur) {  // S = G P at the end of the block
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float4 g4 = B_.ge[KDA ? 4 * rb + j : 0];
+        const float gj[4] = {g4.x, g4.y, g4.z, g4.w};
+#pragma unroll
+        for (int m = 0; m < 4; ++m)
+#pragma unroll
+          for (int c = 0; c < 4; ++c) x[4 * j + m][c] *= gj[m];
+      }
+    }
+    int slow_next = 1;
+    if (blk + 1 < nblk) {
+      publish_blk(cur, blk + 1, par ^ 1);
+      if constexpr (KDA) {
+        __syncthreads();
+        const int left = T - TB * (blk + 1);
+        slow_next = cumulate(par ^ 1, left < TB ? left : TB);
+      }
+    }
     __syncthreads();
+    slow_cur = slow_next;
   }
   if (!KDA) {
 #pragma unroll

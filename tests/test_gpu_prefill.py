@@ -98,3 +98,29 @@ def test_prefill_padded_requests_and_bf16_output(d, T):
     st = ref.slot_stride
     for s in (0, 1, 3):
         assert np.array_equal(host[pad + s * st:pad + (s + 1) * st], ref.buf[s * st:(s + 1) * st])
+
+
+def test_prefill_kda_blocks_with_vanishing_decay():
+    """KDA at d = 128 defers each row's decay over a block of 8 tokens unless
+    some row's running product leaves [2^-60, 2^60]; here the middle of three
+    blocks holds a channel decaying by e^-12 per token (product e^-96) and one
+    token with a zero decay (g = -inf), so the per-token and the deferred
+    blocks alternate within one chunk."""
+    d, HK, HV, B, T, k_hi = 128, 2, 2, 2, 24, 16
+    seed = 733
+    slots = inputs.slot_order(seed, B + 2, B)
+    perm = inputs.random_perms(seed, HV, d)
+    ref = orc.Pool(orc.KIND_MIXED, d, d, k_hi, 1, B + 2, HV)
+    orc.pack(ref, 0, slots, inputs.synthetic_states(seed, B, HV, d), perm)
+    gpool = gpu_pool_from(ref, D)
+    inp = inputs.as_prefill(inputs.decode_inputs(seed, T, B, HK, HV, d, kda=True))
+    g = inp["g"].copy()  # bf16 bits [B, T, HV, d]
+    g[0, 8:16, 0, 5] = inputs.to_bf16_bits(np.float32(-12.0))[0]
+    g[1, 12, 1, 70] = inputs.to_bf16_bits(np.float32(-np.inf))[0]
+    inp["g"] = g
+    o_gpu, o_ref = _run(True, ref, gpool, slots, inp, perm)
+    err = rel_l2(o_gpu, o_ref)
+    stats = compare_tiles(gpool.buffer.cpu().numpy(), ref, "prefill KDA vanishing decay",
+                          s16_exact_min=0.99)
+    _say(f"  o rel-L2 {err:.2e}  {stats}")
+    assert err <= 1e-4
