@@ -247,9 +247,10 @@ damp_status damp_state_update_kda(const damp_pool* pool, int32_t layer,
  *  T          tokens per request in this chunk (0 is a no-op).
  *  q, k       bf16 [B, T, HK, d_k];  v  bf16 [B, T, HV, d_v];
  *  g          bf16 [B, T, HV] (GDN) or [B, T, HV, d_k] (KDA): log-decay;
- *  beta       bf16 [B, T, HV];  o  [B, T, HV, d_v] in o_dtype.
+ *  beta       bf16 [B, T, HV];  o  [B, T, HV, d_v] in o_dtype, 16-byte
+ *             aligned.
  * A padded request (slot outside the pool) gets o = 0 for every token.
- * DAMP_ERR_INVALID_ARG also for T < 0. */
+ * DAMP_ERR_INVALID_ARG also for T < 0 and for a misaligned o. */
 damp_status damp_state_prefill_gdn(const damp_pool* pool, int32_t layer,
                                    const int32_t* slot_idx, int32_t B, int32_t T,
                                    int32_t num_k_heads, const uint16_t* q,

@@ -17,6 +17,7 @@
 //   o = scale (S_bar^T q~ + beta (q~ . k~) delta)
 // equals scale * S^T q~ for the updated state S.
 #include <climits>
+#include <cstdint>
 
 #include "device.hpp"
 #include "internal.hpp"
@@ -261,6 +262,7 @@ __global__ __launch_bounds__(256) void prefill_blk128(const PrefillParams p) {
     float4 a[NA][D / 4];
     float4 sc[TB];  // beta, alpha (GDN), q~ . k~ over rows 0..63 and 64..127
     float4 ge[KDA ? D / 4 : 1];  // KDA, deferred decay: each row's product over the block
+    float4 os[TB][D / 4];        // o of the block's tokens, stored as whole rows at its end
   };
   constexpr int kTbufFloats = 32 * (D + 4);
   constexpr int kOpFloats = 2 * static_cast<int>(sizeof(OpBuf) / 4);
@@ -518,7 +520,7 @@ __global__ __launch_bounds__(256) void prefill_blk128(const PrefillParams p) {
         ov[c] = fmaf(sbq, delta, sg * pq[c]);
         cf[c] = bg * delta;
       }
-      write_o(tok, ov);
+      if (rb == 0) ob[par].os[tb][c0 / 4] = make_float4(ov[0], ov[1], ov[2], ov[3]);
       // rank-1 update S = S_bar + beta k~ delta^T (GDN: on P = S / gamma;
       // KDA with deferred decay: on P = S / G with k~ / G)
       if (KDA && !slow_cur) {
@@ -565,7 +567,30 @@ __global__ __launch_bounds__(256) void prefill_blk128(const PrefillParams p) {
     }
     __syncthreads();
     slow_cur = slow_next;
+    // the block's o, a 16-byte piece per thread: 128 threads for bf16 rows
+    // (8 columns each), all 256 for fp32 rows (4 columns each)
+    if (p.o) {
+      const OpBuf& O_ = ob[par];
+      uint8_t* const o_row = static_cast<uint8_t*>(p.o) +
+                             ((static_cast<size_t>(b) * T * p.HV + h) * D) * o_esize;
+      if (p.o_bf16) {
+        const int tb = t >> 4, q8 = t & 15;
+        if (tb < ntok) {
+          const float4 lo = O_.os[tb][2 * q8], hi = O_.os[tb][2 * q8 + 1];
+          *reinterpret_cast<uint4*>(o_row + static_cast<size_t>(TB * blk + tb) * o_step +
+                                    16 * q8) =
+              make_uint4(pack_bf16x2(lo.x, lo.y), pack_bf16x2(lo.z, lo.w),
+                         pack_bf16x2(hi.x, hi.y), pack_bf16x2(hi.z, hi.w));
+        }
+      } else {
+        const int tb = t >> 5, q4 = t & 31;
+        if (tb < ntok)
+          *reinterpret_cast<float4*>(o_row + static_cast<size_t>(TB * blk + tb) * o_step +
+                                     16 * q4) = O_.os[tb][q4];
+      }
+    }
   }
+  __syncthreads();  // the last block's o is read before the transit buffer reuses it
   if (!KDA) {
 #pragma unroll
     for (int i = 0; i < 16; ++i)
@@ -707,6 +732,8 @@ damp_status prefill(bool kda, const damp_pool* pool, int32_t layer, const int32_
   if (B == 0 || T == 0) return DAMP_OK;
   if (!slot_idx || !q || !k || !v || !g || !beta || !o)
     return fail(DAMP_ERR_INVALID_ARG, "%s: a required pointer is NULL", name);
+  if (reinterpret_cast<uintptr_t>(o) % 16 != 0)
+    return fail(DAMP_ERR_INVALID_ARG, "%s: o is not 16-byte aligned", name);
   if (!layout_has_kernels(&pool->layout))
     return fail(DAMP_ERR_UNSUPPORTED, "%s: no kernel for this layout", name);
 

@@ -195,6 +195,10 @@ def test_prefill_validation_fails_before_launch(L):
         a = list(args)
         a[10] = None  # beta
         assert fn(*a) == D.DAMP_ERR_INVALID_ARG
+        a = list(args)
+        a[13] = ctypes.c_void_p(0x7f0000100008)  # o must be 16-byte aligned
+        st, msg = _status(fn, *a)
+        assert st == D.DAMP_ERR_INVALID_ARG and "aligned" in msg
 
 
 def test_layouts_without_kernels_are_reported(L):
