@@ -178,6 +178,23 @@ damp_status damp_pool_init(damp_pool* pool, const damp_layout* layout,
                            int32_t num_layers, int32_t num_slots,
                            int32_t num_v_heads, void* base, size_t bytes);
 
+/* Race check of a batch of slot ids. Every call that writes tiles
+ * (update, prefill, pack, reset, calibration sequence) requires the slots of
+ * its batch to be distinct: two requests sharing a slot would read and write
+ * the same tiles concurrently. The kernels do not check this; this call
+ * does. Entries outside [0, num_slots) are padding and are ignored.
+ *  slot_idx   int32[B]; a HOST pointer when on_device is 0, else a device
+ *             pointer that is copied to the host on `stream` (which is then
+ *             synchronised).
+ * Returns DAMP_ERR_INVALID_ARG naming the repeated slot, DAMP_OK otherwise.
+ * Validation mode: with the environment variable DAMP_CHECK_SLOTS set to a
+ * value other than "0", every call that writes tiles runs this check on its
+ * device slot ids before enqueuing anything and fails the same way; each
+ * such call then synchronises its stream (a debugging aid, not for capture
+ * into a graph). */
+damp_status damp_check_slots(const damp_pool* pool, const int32_t* slot_idx,
+                             int32_t B, int32_t on_device, void* stream);
+
 /* Writes the packed zero state into every head of `n` slots (for a new
  * request). `layer` selects one layer, or -1 for all layers. `slots` is a
  * device int32[n]; entries outside [0, num_slots) are skipped. */
@@ -291,9 +308,10 @@ damp_status damp_state_unpack(const damp_pool* pool, int32_t layer,
  *
  * For each head h and key channel u, over the N calibration samples n:
  *   E_u   = mean_n || Q_lo(S_n[h,u,:]) - S_n[h,u,:] ||^2     (Eq. (8))
- *           with Q_lo = the per-row quantizer above (IEEE division, no FMA),
- *           squared errors summed in double in ascending column order and
- *           samples summed in ascending n;
+ *           with Q_lo the low tier of `lo` (App. A.2: the deployed storage
+ *           mapping), evaluated with IEEE operations (exact division, no
+ *           FMA), squared errors summed in double in ascending column order
+ *           and samples summed in ascending n;
  *   a_eff = exp(mean_n log_a[n,h(,u)])                      (geometric mean)
  *   P_u   = 1 / max(1 - a_eff^2, tau)                       (Eq. (9))
  *   C_u   = E_u * P_u, and the k_hi largest C_u are kept    (Eq. (10)),
@@ -305,15 +323,23 @@ damp_status damp_state_unpack(const damp_pool* pool, int32_t layer,
  *             1: log_decay is [N, H, d_k] (per key channel, KDA).
  *  states     fp32 [N, H, d_k, d_v] device: reference (FP32) states.
  *  log_decay  fp32 device, see is_kda.
+ *  lo         host pointer to the layout whose low tier is Q_lo, or NULL for
+ *             the per-row quantizer of the default tiers. Supported: a
+ *             DAMP_STATE_MIXED layout with this d_k and d_v and the default
+ *             low tier (one fp32 (s, z) per row), or the paper's UINT8 tier
+ *             (groups of 32 with FP16 (s, z), hadamard 0 or 1; d_v <= 128
+ *             and a multiple of 32). Its k_hi is not used. Other layouts
+ *             return DAMP_ERR_UNSUPPORTED.
  *  k_hi       in [0, d_k]; tau > 0 (the paper uses 1e-4).
  *  sel_out    host int32 [H, k_hi], ascending per head.
  *  perm_out   host uint8 [H, d_k] (d_k <= 256).
  *  score_out  host double [H, d_k] receiving C_u, or NULL.
- * Allocates and frees device scratch; synchronises `stream`. */
+ * Allocates and frees (N + 2) * H * d_k doubles of device scratch;
+ * synchronises `stream`. */
 damp_status damp_select_channels(int32_t is_kda, int32_t N, int32_t H,
                                  int32_t d_k, int32_t d_v, const float* states,
-                                 const float* log_decay, int32_t k_hi,
-                                 double tau, int32_t* sel_out,
+                                 const float* log_decay, const damp_layout* lo,
+                                 int32_t k_hi, double tau, int32_t* sel_out,
                                  uint8_t* perm_out, double* score_out,
                                  void* stream);
 

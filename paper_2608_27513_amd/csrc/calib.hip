@@ -333,6 +333,22 @@ damp_status check_fp32_pool(const damp_calib* c, const damp_pool* pool, int32_t 
   return DAMP_OK;
 }
 
+// || Q_lo(x) - x ||^2 of independent rows (row i at states + i * dv) under
+// the paper's UINT8 group tier, one row per wave, the same per-row
+// evaluation as the accumulation above.
+__global__ __launch_bounds__(256) void row_error_group_kernel(const float* __restrict__ states,
+                                                              int64_t rows, int dv, int had,
+                                                              double* __restrict__ err) {
+  __shared__ RowScratch scr[4];
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + wave;
+  if (row >= rows) return;  // whole waves leave: the evaluation synchronises within a wave only
+  double e = 0.0, e2 = 0.0;
+  row_stats_wave(states + row * dv, dv, true, had != 0, scr[wave], lane, e, e2);
+  if (lane == 0) err[row] = e;
+}
+
 // Average ranks (ties share the mean of their positions), 1-based.
 std::vector<double> ranks_of(const double* x, int n) {
   std::vector<int> idx(n);
@@ -350,6 +366,14 @@ std::vector<double> ranks_of(const double* x, int n) {
 }
 
 }  // namespace
+
+void launch_row_errors_group(const float* states, int64_t rows, int dv, bool had, double* err,
+                             hipStream_t stream) {
+  const int64_t blocks = (rows + 3) / 4;
+  hipLaunchKernelGGL(row_error_group_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
+                     stream, states, rows, dv, had ? 1 : 0, err);
+}
+
 }  // namespace damp
 
 extern "C" {
@@ -443,6 +467,8 @@ damp_status damp_calibrate_sequence(const damp_calib* calib, int32_t domain,
   if (B == 0 || T == 0) return DAMP_OK;
   if (!slot_idx || !q || !k || !v || !g || !beta)
     return fail(DAMP_ERR_INVALID_ARG, "%s: a required pointer is NULL", name);
+  st = debug_check_slots(pool, slot_idx, B, as_stream(stream), name);
+  if (st != DAMP_OK) return st;
   const bool kda = calib->is_kda != 0;
   const int64_t per_tok = kda ? static_cast<int64_t>(calib->num_heads) * calib->lo.d_k
                               : calib->num_heads;

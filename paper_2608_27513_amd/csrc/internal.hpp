@@ -56,6 +56,13 @@ bool layout_has_kernels(const damp_layout* layout);
 // Validates a pool descriptor (non-null, consistent strides and counts).
 damp_status check_pool(const damp_pool* pool);
 
+// With the environment variable DAMP_CHECK_SLOTS set (and not "0"): copies
+// the device slot ids to the host on `stream` (synchronising it) and fails
+// with DAMP_ERR_INVALID_ARG if a slot inside the pool occurs twice. Without
+// it: DAMP_OK at once. Called by every entry point that writes tiles.
+damp_status debug_check_slots(const damp_pool* pool, const int32_t* slot_idx, int32_t B,
+                              hipStream_t stream, const char* name);
+
 // Thread-local error message.
 damp_status fail(damp_status st, const char* fmt, ...);
 void clear_error();
@@ -79,5 +86,12 @@ void prefill_window(bool kda, const damp_pool* pool, int32_t layer, const int32_
                     const uint16_t* q, const uint16_t* k, const uint16_t* v, const uint16_t* g,
                     const uint16_t* beta, const uint8_t* perm, float scale, void* o,
                     bool o_bf16, hipStream_t stream);
+
+// Enqueues || Q_lo(x) - x ||^2 in double for `rows` independent fp32 rows of
+// dv values (row i at states + i * dv) with Q_lo the paper's UINT8 group tier
+// (groups of 32, FP16 (s, z), optionally after the block-32 transform);
+// dv <= 128 and a multiple of 32. Row i's sum goes to err[i].
+void launch_row_errors_group(const float* states, int64_t rows, int dv, bool had, double* err,
+                             hipStream_t stream);
 
 }  // namespace damp

@@ -2,9 +2,12 @@
 //
 // Tile format: section 5.2 and App. A.5 (Eq. (17)) of the DAMP paper, with
 // one (s, z) pair per low-tier row; storage cost: Eq. (7) and Eq. (12).
+#include <algorithm>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
+#include <vector>
 
 #include "internal.hpp"
 
@@ -162,6 +165,48 @@ damp_status check_pool(const damp_pool* pool) {
   return DAMP_OK;
 }
 
+namespace {
+
+// The first slot in [0, num_slots) that occurs twice among ids[0..B), or -1.
+int32_t first_repeat(const int32_t* ids, int32_t B, int32_t num_slots) {
+  std::vector<int32_t> v;
+  v.reserve(static_cast<size_t>(B));
+  for (int32_t i = 0; i < B; ++i)
+    if (ids[i] >= 0 && ids[i] < num_slots) v.push_back(ids[i]);
+  std::sort(v.begin(), v.end());
+  const auto it = std::adjacent_find(v.begin(), v.end());
+  return it == v.end() ? -1 : *it;
+}
+
+damp_status check_slots(const damp_pool* pool, const int32_t* slot_idx, int32_t B,
+                        bool on_device, hipStream_t stream, const char* name) {
+  if (B <= 0) return DAMP_OK;
+  const int32_t* ids = slot_idx;
+  std::vector<int32_t> host;
+  if (on_device) {
+    host.resize(static_cast<size_t>(B));
+    hipError_t e = hipMemcpyAsync(host.data(), slot_idx, sizeof(int32_t) * host.size(),
+                                  hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return fail(DAMP_ERR_HIP, "%s: slot ids: %s", name, hipGetErrorString(e));
+    ids = host.data();
+  }
+  const int32_t rep = first_repeat(ids, B, pool->num_slots);
+  if (rep >= 0)
+    return fail(DAMP_ERR_INVALID_ARG, "%s: slot %d appears more than once in the batch", name,
+                rep);
+  return DAMP_OK;
+}
+
+}  // namespace
+
+damp_status debug_check_slots(const damp_pool* pool, const int32_t* slot_idx, int32_t B,
+                              hipStream_t stream, const char* name) {
+  const char* env = std::getenv("DAMP_CHECK_SLOTS");
+  if (!env || env[0] == '\0' || env[0] == '0') return DAMP_OK;
+  return check_slots(pool, slot_idx, B, true, stream, name);
+}
+
 }  // namespace damp
 
 using namespace damp;
@@ -223,6 +268,16 @@ size_t damp_pool_required_bytes(const damp_layout* layout, int32_t num_layers,
   if (!tile_geom(layout, &g) || num_layers <= 0 || num_slots <= 0 || num_v_heads <= 0) return 0;
   return g.stride * static_cast<size_t>(num_layers) * static_cast<size_t>(num_slots) *
          static_cast<size_t>(num_v_heads);
+}
+
+damp_status damp_check_slots(const damp_pool* pool, const int32_t* slot_idx, int32_t B,
+                             int32_t on_device, void* stream) {
+  clear_error();
+  damp_status st = check_pool(pool);
+  if (st != DAMP_OK) return st;
+  if (B < 0) return fail(DAMP_ERR_INVALID_ARG, "damp_check_slots: B = %d is negative", B);
+  if (B > 0 && !slot_idx) return fail(DAMP_ERR_INVALID_ARG, "damp_check_slots: slot_idx is NULL");
+  return check_slots(pool, slot_idx, B, on_device != 0, as_stream(stream), "damp_check_slots");
 }
 
 damp_status damp_pool_init(damp_pool* pool, const damp_layout* layout, int32_t num_layers,

@@ -275,6 +275,10 @@ damp_status run(Op op, const char* name, const damp_pool* pool, int32_t layer,
     return fail(DAMP_ERR_INVALID_ARG, "%s: a required pointer is NULL", name);
   if (!layout_has_kernels(&pool->layout))
     return fail(DAMP_ERR_UNSUPPORTED, "%s: no kernel for this layout", name);
+  if (op != Op::kUnpack) {
+    st = debug_check_slots(pool, slot_idx, B, as_stream(stream), name);
+    if (st != DAMP_OK) return st;
+  }
   TileParams p;
   p.tile_stride = pool->tile_stride;
   p.slot_stride = pool->tile_stride * static_cast<uint64_t>(pool->num_v_heads);

@@ -245,6 +245,8 @@ __global__ __launch_bounds__(NT) void prefill_kernel(const PrefillParams p) {
 // the decays since the last renormalization, so a token costs one FMA per
 // state value for each read-out and one for the update:
 //   w = gamma sum_u k_u P_u,  P_u += k_u (beta delta / gamma).
+// A token whose decay would take gamma outside [2^-40, 2^40] (a zero decay
+// included) scales P by gamma and its decay instead and resets gamma to 1.
 struct BlkOps {
   uint32_t k[4], q[4], v[4], g[4];
   uint32_t beta[4];
@@ -505,12 +507,20 @@ __global__ __launch_bounds__(256) void prefill_blk128(const PrefillParams p) {
         pq[c] += dpp_mov<0x141>(pq[c]);
       }
       // per token: g = gamma (1 for KDA), o = scale (g p + beta (q~.k~) delta),
-      // delta = v - g w, and the update's factor (beta / g) delta
+      // delta = v - g w, and the update's factor (beta / g) delta. GDN keeps
+      // gamma within [2^-40, 2^40]: when this token's decay would take it out
+      // (a vanishing or zero alpha included), the read-outs still take the
+      // exact factor, but the update runs on S_bar itself (P scaled by the old
+      // gamma and this alpha, gamma reset to 1), so 1 / gamma stays finite
       const float4 sc = B_.sc[tb];
-      if (!KDA) gamma *= sc.y;
-      const float gw = KDA ? 1.0f : gamma;
+      float gw = 1.0f, bg = sc.x;
+      bool fold = false;
+      if (!KDA) {
+        gw = gamma * sc.y;
+        fold = !(gw >= 9.094947e-13f && gw <= 1.0995116e12f);
+        if (!fold) bg = sc.x * refined_rcp(gw);
+      }
       const float sg = p.scale * gw, sbq = p.scale * sc.x * (sc.z + sc.w);
-      const float bg = KDA ? sc.x : sc.x * refined_rcp(gamma);
       const float4 v4 = B_.v[tb][c0 / 4];
       const float vv[4] = {v4.x, v4.y, v4.z, v4.w};
       float ov[4], cf[4];
@@ -533,17 +543,21 @@ __global__ __launch_bounds__(256) void prefill_blk128(const PrefillParams p) {
           kr[4 * j + 3] = b4.w;
         }
       }
+      if (!KDA) {
+        if (fold) {
+#pragma unroll
+          for (int i = 0; i < 16; ++i)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) x[i][c] = (x[i][c] * gamma) * sc.y;
+          gamma = 1.0f;
+        } else {
+          gamma = gw;
+        }
+      }
 #pragma unroll
       for (int i = 0; i < 16; ++i)
 #pragma unroll
         for (int c = 0; c < 4; ++c) x[i][c] = fmaf(kr[i], cf[c], x[i][c]);
-      if (!KDA && !(gamma >= 9.094947e-13f && gamma <= 1.0995116e12f)) {  // outside [2^-40, 2^40]
-#pragma unroll
-        for (int i = 0; i < 16; ++i)
-#pragma unroll
-          for (int c = 0; c < 4; ++c) x[i][c] *= gamma;
-        gamma = 1.0f;
-      }
     }
     if (KDA && !slow_cur) {  // S = G P at the end of the block
 #pragma unroll
@@ -736,6 +750,8 @@ damp_status prefill(bool kda, const damp_pool* pool, int32_t layer, const int32_
     return fail(DAMP_ERR_INVALID_ARG, "%s: o is not 16-byte aligned", name);
   if (!layout_has_kernels(&pool->layout))
     return fail(DAMP_ERR_UNSUPPORTED, "%s: no kernel for this layout", name);
+  st = debug_check_slots(pool, slot_idx, B, as_stream(stream), name);
+  if (st != DAMP_OK) return st;
 
   prefill_window(kda, pool, layer, slot_idx, B, 0, T, T, num_k_heads, q, k, v, g, beta, perm,
                  scale, o, o_dtype == DAMP_DT_BF16, as_stream(stream));

@@ -1,13 +1,16 @@
 // Offline selection of the protected key channels (section 5.1 Eq. (8)-(10),
 // App. A.2 Eq. (14)-(15), Alg. 1 of App. A.4).
 //
-// The device pass computes, for every calibration row S_n[h, u, :], the
-// squared reconstruction error under the low-tier quantizer of Eq. (3). Each
-// row is handled by one thread in ascending column order with IEEE
-// operations only (correctly rounded fp32 division, no contraction, double
-// accumulation), so the per-row sums are reproducible bit for bit. The host
-// then averages over samples in ascending order, forms the geometric-mean
-// decay, the persistence of Eq. (9), C = E P, and the top-k_hi partition.
+// The device computes, for every calibration row S_n[h, u, :], the squared
+// reconstruction error under the low-tier quantizer Q_lo: the per-row
+// quantizer of Eq. (3) (one thread per row, ascending columns) or the paper's
+// group tier (one wave per row, the calibration kernel's evaluation). Both
+// use IEEE operations only (correctly rounded fp32 division, no contraction,
+// double accumulation in ascending column order), so the per-row sums are
+// reproducible bit for bit. A second pass sums each (head, channel) over the
+// samples in ascending n, and the log-decays likewise, in double. The host
+// then forms E, the geometric-mean decay, the persistence of Eq. (9),
+// C = E P and the top-k_hi partition.
 #include <algorithm>
 #include <cfloat>
 #include <cmath>
@@ -50,69 +53,107 @@ __global__ __launch_bounds__(256) void row_error_kernel(const float* __restrict_
   err[i] = acc;
 }
 
-}  // namespace
-}  // namespace damp
-
-extern "C" damp_status damp_select_channels(int32_t is_kda, int32_t N, int32_t H, int32_t d_k,
-                                            int32_t d_v, const float* states,
-                                            const float* log_decay, int32_t k_hi, double tau,
-                                            int32_t* sel_out, uint8_t* perm_out,
-                                            double* score_out, void* stream) {
-  using namespace damp;
-  clear_error();
-  if (N <= 0 || H <= 0 || d_k <= 0 || d_k > 256 || d_v <= 0)
-    return fail(DAMP_ERR_INVALID_ARG, "damp_select_channels: bad sizes N=%d H=%d d_k=%d d_v=%d",
-                N, H, d_k, d_v);
-  if (k_hi < 0 || k_hi > d_k)
-    return fail(DAMP_ERR_INVALID_ARG, "damp_select_channels: k_hi = %d outside [0, %d]", k_hi,
-                d_k);
-  if (!(tau > 0.0)) return fail(DAMP_ERR_INVALID_ARG, "damp_select_channels: tau must be > 0");
-  if (!states || !log_decay || !perm_out || (k_hi > 0 && !sel_out))
-    return fail(DAMP_ERR_INVALID_ARG, "damp_select_channels: a required pointer is NULL");
-
-  const int64_t rows = static_cast<int64_t>(N) * H * d_k;
-  const int64_t nlog = static_cast<int64_t>(N) * H * (is_kda ? d_k : 1);
-  hipStream_t s = as_stream(stream);
-  double* d_err = nullptr;
-  if (hipMalloc(&d_err, rows * sizeof(double)) != hipSuccess)
-    return fail(DAMP_ERR_HIP, "damp_select_channels: hipMalloc of %lld bytes failed",
-                static_cast<long long>(rows * sizeof(double)));
-  const int64_t blocks = (rows + 255) / 256;
-  hipLaunchKernelGGL(row_error_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s,
-                     states, rows, d_v, d_err);
-  std::vector<double> err(rows);
-  std::vector<float> logs(nlog);
-  damp_status st = check_launch("damp_select_channels");
-  if (st == DAMP_OK) {
-    hipError_t e = hipMemcpyAsync(err.data(), d_err, rows * sizeof(double),
-                                  hipMemcpyDeviceToHost, s);
-    if (e == hipSuccess)
-      e = hipMemcpyAsync(logs.data(), log_decay, nlog * sizeof(float), hipMemcpyDeviceToHost, s);
-    if (e == hipSuccess) e = hipStreamSynchronize(s);
-    if (e != hipSuccess)
-      st = fail(DAMP_ERR_HIP, "damp_select_channels: %s", hipGetErrorString(e));
+// esum[h, u] = sum_n err[n, h, u] and lsum[h, u] = sum_n log a[n, h(, u)],
+// both in double, n ascending: one thread per (head, channel).
+__global__ __launch_bounds__(256) void sum_samples_kernel(const double* __restrict__ err,
+                                                          const float* __restrict__ logs, int N,
+                                                          int H, int dk, int is_kda,
+                                                          double* __restrict__ esum,
+                                                          double* __restrict__ lsum) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= H * dk) return;
+  const int h = i / dk, u = i % dk;
+  double e = 0.0, l = 0.0;
+  for (int n = 0; n < N; ++n) {
+    const size_t nh = static_cast<size_t>(n) * H + h;
+    e = __dadd_rn(e, err[nh * dk + u]);
+    l = __dadd_rn(l, static_cast<double>(is_kda ? logs[nh * dk + u] : logs[nh]));
   }
-  (void)hipFree(d_err);
-  if (st != DAMP_OK) return st;
+  esum[i] = e;
+  lsum[i] = l;
+}
 
+// Low tier the selection measures E under: 0 the per-row quantizer, 1 the
+// paper's groups of 32 with FP16 (s, z), 2 the same after the block-32
+// transform; -1 if `lo` is not a low tier with a kernel here.
+int select_tier(const damp_layout* lo, int d_k, int d_v) {
+  if (!lo) return 0;
+  if (lo->kind != DAMP_STATE_MIXED || lo->d_k != d_k || lo->d_v != d_v) return -1;
+  if (layout_is_default(lo)) return 0;
+  if (layout_is_paper(lo) && d_v <= 128 && d_v % 32 == 0) return lo->hadamard ? 2 : 1;
+  return -1;
+}
+
+}  // namespace
+
+int64_t select_scratch_doubles(int32_t N, int32_t H, int32_t d_k) {
+  const int64_t hk = static_cast<int64_t>(H) * d_k;
+  return static_cast<int64_t>(N) * hk + 2 * hk;
+}
+
+damp_status select_validate(const char* name, int32_t is_kda, int32_t N, int32_t H, int32_t d_k,
+                            int32_t d_v, const float* states, const float* log_decay,
+                            const damp_layout* lo, int32_t k_hi, double tau,
+                            const int32_t* sel_out, const uint8_t* perm_out) {
+  (void)is_kda;
+  if (N <= 0 || H <= 0 || d_k <= 0 || d_k > 256 || d_v <= 0)
+    return fail(DAMP_ERR_INVALID_ARG, "%s: bad sizes N=%d H=%d d_k=%d d_v=%d", name, N, H, d_k,
+                d_v);
+  if (k_hi < 0 || k_hi > d_k)
+    return fail(DAMP_ERR_INVALID_ARG, "%s: k_hi = %d outside [0, %d]", name, k_hi, d_k);
+  if (!(tau > 0.0)) return fail(DAMP_ERR_INVALID_ARG, "%s: tau must be > 0", name);
+  if (!states || !log_decay || !perm_out || (k_hi > 0 && !sel_out))
+    return fail(DAMP_ERR_INVALID_ARG, "%s: a required pointer is NULL", name);
+  if (static_cast<int64_t>(H) * d_k > INT32_MAX)
+    return fail(DAMP_ERR_INVALID_ARG, "%s: H * d_k too large", name);
+  if (select_tier(lo, d_k, d_v) < 0)
+    return fail(DAMP_ERR_UNSUPPORTED, "%s: Q_lo must be the per-row tier or the paper's UINT8 "
+                "group tier (d_v <= 128, a multiple of 32) with d_k, d_v as given", name);
+  return DAMP_OK;
+}
+
+damp_status select_run(const char* name, int32_t is_kda, int32_t N, int32_t H, int32_t d_k,
+                       int32_t d_v, const float* states, const float* log_decay,
+                       const damp_layout* lo, int32_t k_hi, double tau, int32_t* sel_out,
+                       uint8_t* perm_out, double* score_out, double* scratch,
+                       hipStream_t s) {
+  const int64_t rows = static_cast<int64_t>(N) * H * d_k;
+  const int64_t hk = static_cast<int64_t>(H) * d_k;
+  double* d_err = scratch;
+  double* d_esum = scratch + rows;
+  double* d_lsum = d_esum + hk;
+  const int tier = select_tier(lo, d_k, d_v);
+  if (tier == 0) {
+    hipLaunchKernelGGL(row_error_kernel, dim3(static_cast<unsigned>((rows + 255) / 256)),
+                       dim3(256), 0, s, states, rows, d_v, d_err);
+  } else {
+    launch_row_errors_group(states, rows, d_v, tier == 2, d_err, s);
+  }
+  hipLaunchKernelGGL(sum_samples_kernel, dim3(static_cast<unsigned>((hk + 255) / 256)),
+                     dim3(256), 0, s, d_err, log_decay, N, H, d_k, is_kda ? 1 : 0, d_esum,
+                     d_lsum);
+  damp_status st = check_launch(name);
+  if (st != DAMP_OK) return st;
+  std::vector<double> sums(2 * hk);
+  hipError_t e = hipMemcpyAsync(sums.data(), d_esum, 2 * hk * sizeof(double),
+                                hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return fail(DAMP_ERR_HIP, "%s: %s", name, hipGetErrorString(e));
+
+  const double* esum = sums.data();
+  const double* lsum = sums.data() + hk;
   std::vector<double> score(d_k);
   std::vector<int> order(d_k);
   std::vector<char> keep(d_k);
   for (int h = 0; h < H; ++h) {
     for (int u = 0; u < d_k; ++u) {
-      double esum = 0.0, lsum = 0.0;
-      for (int n = 0; n < N; ++n) {
-        esum = esum + err[(static_cast<size_t>(n) * H + h) * d_k + u];
-        lsum = lsum + static_cast<double>(
-                          is_kda ? logs[(static_cast<size_t>(n) * H + h) * d_k + u]
-                                 : logs[static_cast<size_t>(n) * H + h]);
-      }
-      const double E = esum / static_cast<double>(N);           // Eq. (8)
-      const double a_eff = std::exp(lsum / static_cast<double>(N));
+      const size_t i = static_cast<size_t>(h) * d_k + u;
+      const double E = esum[i] / static_cast<double>(N);           // Eq. (8)
+      const double a_eff = std::exp(lsum[i] / static_cast<double>(N));
       const double gap = 1.0 - a_eff * a_eff;
-      const double P = 1.0 / (gap > tau ? gap : tau);           // Eq. (9)
-      score[u] = E * P;                                          // C = E P
-      if (score_out) score_out[static_cast<size_t>(h) * d_k + u] = score[u];
+      const double P = 1.0 / (gap > tau ? gap : tau);              // Eq. (9)
+      score[u] = E * P;                                              // C = E P
+      if (score_out) score_out[i] = score[u];
       order[u] = u;
     }
     std::sort(order.begin(), order.end(), [&](int a, int b) {
@@ -131,4 +172,29 @@ extern "C" damp_status damp_select_channels(int32_t is_kda, int32_t N, int32_t H
       if (!keep[u]) perm_out[static_cast<size_t>(h) * d_k + p++] = static_cast<uint8_t>(u);
   }
   return DAMP_OK;
+}
+
+}  // namespace damp
+
+extern "C" damp_status damp_select_channels(int32_t is_kda, int32_t N, int32_t H, int32_t d_k,
+                                            int32_t d_v, const float* states,
+                                            const float* log_decay, const damp_layout* lo,
+                                            int32_t k_hi, double tau, int32_t* sel_out,
+                                            uint8_t* perm_out, double* score_out,
+                                            void* stream) {
+  using namespace damp;
+  clear_error();
+  const char* name = "damp_select_channels";
+  damp_status st = select_validate(name, is_kda, N, H, d_k, d_v, states, log_decay, lo, k_hi,
+                                   tau, sel_out, perm_out);
+  if (st != DAMP_OK) return st;
+  const size_t bytes = static_cast<size_t>(select_scratch_doubles(N, H, d_k)) * sizeof(double);
+  double* scratch = nullptr;
+  if (hipMalloc(&scratch, bytes) != hipSuccess)
+    return fail(DAMP_ERR_HIP, "%s: hipMalloc of %zu bytes failed", name, bytes);
+  st = select_run(name, is_kda, N, H, d_k, d_v, states, log_decay, lo, k_hi, tau, sel_out,
+                  perm_out, score_out, scratch, as_stream(stream));
+  // the stream was synchronised unless a launch failed; the free waits for the device
+  (void)hipFree(scratch);
+  return st;
 }

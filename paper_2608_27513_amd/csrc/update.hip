@@ -281,6 +281,8 @@ damp_status update(bool kda, const damp_pool* pool, int32_t layer, const int32_t
     return fail(DAMP_ERR_INVALID_ARG, "%s: a required pointer is NULL", name);
   if (!layout_has_kernels(&pool->layout))
     return fail(DAMP_ERR_UNSUPPORTED, "%s: no kernel for this layout", name);
+  st = debug_check_slots(pool, slot_idx, B, as_stream(stream), name);
+  if (st != DAMP_OK) return st;
 
   UpdateParams p;
   p.layer_base = layer_base(pool, layer);

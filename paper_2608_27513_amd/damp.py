@@ -51,7 +51,7 @@ class damp_pool(ctypes.Structure):
 
 
 EXPORTS = ("damp_layout_init", "damp_tile_bytes", "damp_tile_stride", "damp_bits_per_value",
-           "damp_pool_required_bytes", "damp_pool_init", "damp_pool_reset_slots",
+           "damp_pool_required_bytes", "damp_pool_init", "damp_check_slots", "damp_pool_reset_slots",
            "damp_state_update_gdn", "damp_state_update_kda", "damp_state_prefill_gdn",
            "damp_state_prefill_kda", "damp_state_pack", "damp_state_unpack",
            "damp_select_channels", "damp_calib_required_bytes", "damp_calib_init",
@@ -81,6 +81,7 @@ def lib() -> ctypes.CDLL:
         "damp_bits_per_value": (f64, [LP]),
         "damp_pool_required_bytes": (sz, [LP, i32, i32, i32]),
         "damp_pool_init": (st, [PP, LP, i32, i32, i32, P, sz]),
+        "damp_check_slots": (st, [PP, P, i32, i32, P]),
         "damp_pool_reset_slots": (st, [PP, i32, P, i32, P]),
         "damp_state_update_gdn": (st, [PP, i32, P, i32, i32, P, P, P, P, P, P, f32, P, i32, P]),
         "damp_state_update_kda": (st, [PP, i32, P, i32, i32, P, P, P, P, P, P, f32, P, i32, P]),
@@ -90,7 +91,7 @@ def lib() -> ctypes.CDLL:
                                         P]),
         "damp_state_pack": (st, [PP, i32, P, i32, P, P, P]),
         "damp_state_unpack": (st, [PP, i32, P, i32, P, P, P]),
-        "damp_select_channels": (st, [i32, i32, i32, i32, i32, P, P, i32, f64, P, P, P, P]),
+        "damp_select_channels": (st, [i32, i32, i32, i32, i32, P, P, LP, i32, f64, P, P, P, P]),
         "damp_calib_required_bytes": (sz, [i32, i32, i32]),
         "damp_calib_init": (st, [CP, LP, i32, i32, i32, P, sz, P]),
         "damp_calib_accumulate": (st, [CP, i32, PP, i32, P, i32, P, P, P]),
@@ -190,6 +191,18 @@ class Pool:
 def damp_pool_init(layout: damp_layout, num_layers: int, num_slots: int, num_v_heads: int,
                    buffer: torch.Tensor) -> Pool:
     return Pool(layout, num_layers, num_slots, num_v_heads, buffer=buffer)
+
+
+def damp_check_slots(pool: Pool, slot_idx, stream=None) -> None:
+    """Raises DampError (DAMP_ERR_INVALID_ARG) if a slot of the pool occurs
+    twice in slot_idx (a device int32 tensor, or host ids)."""
+    if isinstance(slot_idx, torch.Tensor) and slot_idx.device.type == "cuda":
+        slot_idx = _dev(slot_idx, torch.int32, "slot_idx")
+        _check(lib().damp_check_slots(ctypes.byref(pool.desc), _ptr(slot_idx), slot_idx.numel(), 1,
+                                      _stream(stream)))
+        return
+    ids = (ctypes.c_int32 * len(slot_idx))(*[int(x) for x in slot_idx])
+    _check(lib().damp_check_slots(ctypes.byref(pool.desc), ids, len(slot_idx), 0, None))
 
 
 def damp_pool_reset_slots(pool: Pool, layer: int, slots: torch.Tensor, stream=None) -> None:
@@ -326,9 +339,10 @@ def damp_state_unpack(pool: Pool, layer: int, slot_idx, perm=None, S_out=None, s
 
 # --------------------------------------------------------------- selection
 
-def damp_select_channels(states, log_decay, k_hi: int, *, kda: bool, tau: float = 1e-4,
-                         stream=None):
-    """Alg. 1 on device-resident calibration samples; returns host tensors
+def damp_select_channels(states, log_decay, k_hi: int, *, kda: bool, lo: damp_layout = None,
+                         tau: float = 1e-4, stream=None):
+    """Alg. 1 on device-resident calibration samples, with E measured under
+    the low tier of `lo` (None: the per-row quantizer); returns host tensors
     (sel int32 [H, k_hi], perm uint8 [H, d_k], score float64 [H, d_k])."""
     states = _dev(states, torch.float32, "states")
     if states.dim() != 4:
@@ -339,7 +353,8 @@ def damp_select_channels(states, log_decay, k_hi: int, *, kda: bool, tau: float 
     perm = torch.zeros((H, dk), dtype=torch.uint8)
     score = torch.zeros((H, dk), dtype=torch.float64)
     _check(lib().damp_select_channels(int(kda), N, H, dk, dv, _ptr(states), _ptr(log_decay),
-                                      k_hi, float(tau), _ptr(sel), _ptr(perm), _ptr(score),
+                                      None if lo is None else ctypes.byref(lo), k_hi,
+                                      float(tau), _ptr(sel), _ptr(perm), _ptr(score),
                                       _stream(stream)))
     return sel, perm, score
 

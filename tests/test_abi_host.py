@@ -36,7 +36,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = declared_functions()
-    assert len(names) == 22
+    assert len(names) == 23
     for n in names:
         assert hasattr(L, n), n
     assert sorted(D.EXPORTS) == names
@@ -234,14 +234,72 @@ def test_pack_reset_validation(L):
     assert L.damp_pool_reset_slots(ctypes.byref(pool), -1, p, 0, None) == D.DAMP_OK
 
 
+def test_duplicate_slots_are_rejected(L):
+    """Two requests of one batch sharing a slot would race on its tiles
+    (every tile is read and written in place): damp_check_slots finds the
+    repeat among host slot ids; padded and out-of-range entries are not
+    slots of the pool and may repeat."""
+    pool = _fake_pool(L, D.damp_layout_init(128, 128, 16), slots=64)
+
+    def check(ids):
+        arr = (ctypes.c_int32 * max(1, len(ids)))(*ids)
+        return _status(L.damp_check_slots, ctypes.byref(pool), arr, len(ids), 0, None)
+
+    assert check([3, 1, 2, 0])[0] == D.DAMP_OK
+    assert check([])[0] == D.DAMP_OK
+    assert check([-1, 5, -1, 64, 64, 70, -7])[0] == D.DAMP_OK  # padding only repeats
+    st, msg = check([4, 9, 63, 2, 9])
+    assert st == D.DAMP_ERR_INVALID_ARG and "slot 9" in msg
+    st, msg = check([0, 1, 2, 3, 4, 5, 6, 7, 0])
+    assert st == D.DAMP_ERR_INVALID_ARG and "slot 0" in msg
+    rng = np.random.default_rng(3)
+    ids = rng.permutation(64).astype(np.int32).tolist()
+    assert check(ids)[0] == D.DAMP_OK
+    ids[40] = ids[7]
+    st, msg = check(ids)
+    assert st == D.DAMP_ERR_INVALID_ARG and f"slot {ids[7]}" in msg
+    assert L.damp_check_slots(ctypes.byref(pool), None, 4, 0, None) == D.DAMP_ERR_INVALID_ARG
+    assert L.damp_check_slots(ctypes.byref(pool), None, 0, 0, None) == D.DAMP_OK
+    assert L.damp_check_slots(None, None, 0, 0, None) == D.DAMP_ERR_INVALID_ARG
+
+
 def test_select_validation(L):
     p = ctypes.c_void_p(0x7f0000100000)
     f = L.damp_select_channels
-    assert f(0, 4, 2, 128, 128, p, p, 129, 1e-4, p, p, None, None) == D.DAMP_ERR_INVALID_ARG
-    assert f(0, 4, 2, 128, 128, p, p, 16, 0.0, p, p, None, None) == D.DAMP_ERR_INVALID_ARG
-    assert f(0, 0, 2, 128, 128, p, p, 16, 1e-4, p, p, None, None) == D.DAMP_ERR_INVALID_ARG
-    assert f(0, 4, 2, 300, 128, p, p, 16, 1e-4, p, p, None, None) == D.DAMP_ERR_INVALID_ARG
-    assert f(0, 4, 2, 128, 128, None, p, 16, 1e-4, p, p, None, None) == D.DAMP_ERR_INVALID_ARG
+    assert f(0, 4, 2, 128, 128, p, p, None, 129, 1e-4, p, p, None, None) == D.DAMP_ERR_INVALID_ARG
+    assert f(0, 4, 2, 128, 128, p, p, None, 16, 0.0, p, p, None, None) == D.DAMP_ERR_INVALID_ARG
+    assert f(0, 0, 2, 128, 128, p, p, None, 16, 1e-4, p, p, None, None) == D.DAMP_ERR_INVALID_ARG
+    assert f(0, 4, 2, 300, 128, p, p, None, 16, 1e-4, p, p, None, None) == D.DAMP_ERR_INVALID_ARG
+    assert f(0, 4, 2, 128, 128, None, p, None, 16, 1e-4, p, p, None, None) == \
+        D.DAMP_ERR_INVALID_ARG
+
+
+def test_select_low_tier_argument(L):
+    """Q_lo of the selection is the low tier of `lo` (App. A.2): the per-row
+    tier or the paper's UINT8 group tier; other formats, another shape or an
+    FP32 layout are refused before anything runs."""
+    p = ctypes.c_void_p(0x7f0000100000)  # never dereferenced
+    f = L.damp_select_channels
+
+    def tier(d, fmt):
+        lo = D.damp_layout_init(d, d, 0)
+        if fmt is not None:
+            lo.hi_dtype, lo.group, lo.meta_dtype, lo.hadamard, lo.code_dtype = fmt
+        return lo
+
+    paper = (D.DAMP_DT_FP16, 32, D.DAMP_DT_FP16, 1, D.DAMP_DT_U8)
+    int4 = (D.DAMP_DT_FP16, 32, D.DAMP_DT_FP16, 0, D.DAMP_DT_U4)
+    fp8 = (D.DAMP_DT_FP16, 32, D.DAMP_DT_FP32, 0, D.DAMP_DT_E4M3)
+    for lo in (tier(128, int4), tier(128, fp8), tier(64, paper),
+               D.damp_layout_init(128, 128, 0, D.DAMP_STATE_FP32)):
+        st, msg = _status(f, 0, 4, 2, 128, 128, p, p, ctypes.byref(lo), 16, 1e-4, p, p, None, None)
+        assert st == D.DAMP_ERR_UNSUPPORTED and "Q_lo" in msg
+    big = tier(256, paper)  # groups of 32 are evaluated by one wave per row: d_v <= 128
+    assert f(0, 4, 2, 256, 256, p, p, ctypes.byref(big), 16, 1e-4, p, p, None, None) == \
+        D.DAMP_ERR_UNSUPPORTED
+    # invalid sizes are reported before the layout is looked at
+    assert f(0, 0, 2, 128, 128, p, p, ctypes.byref(tier(128, int4)), 16, 1e-4, p, p, None,
+             None) == D.DAMP_ERR_INVALID_ARG
 
 
 def test_split_agreement_functions_match_scipy(L):

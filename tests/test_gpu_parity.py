@@ -184,6 +184,39 @@ def test_beta0_decay1_is_a_fixed_point_on_gpu():
     assert (ca != cb).mean() <= 1e-5 and np.array_equal(za, zb)
 
 
+def test_slot_validation_mode_rejects_repeated_slots(monkeypatch):
+    """With DAMP_CHECK_SLOTS=1 every call that writes tiles copies its slot ids
+    to the host first and refuses a batch in which a pool slot repeats (the
+    two requests would race on its tiles), touching nothing; distinct slots,
+    padding and the mode switched off run as usual."""
+    d, HK, HV, B, k_hi = 64, 2, 4, 3, 8
+    ref = orc.Pool(orc.KIND_MIXED, d, d, k_hi, 1, 6, HV)
+    orc.pack(ref, 0, np.arange(6), inputs.synthetic_states(41, 6, HV, d))
+    gpool = gpu_pool_from(ref, D)
+    inp = inputs.step(inputs.decode_inputs(42, 1, B, HK, HV, d), 0)
+    x = dev_inputs(inp)
+    before = gpool.buffer.clone()
+    monkeypatch.setenv("DAMP_CHECK_SLOTS", "1")
+    dup = dev_i32([4, 1, 4])
+    with pytest.raises(D.DampError) as e:
+        D.damp_state_update_gdn(gpool, 0, dup, x["q"], x["k"], x["v"], x["g"], x["beta"])
+    assert e.value.status == D.DAMP_ERR_INVALID_ARG and "slot 4" in str(e.value)
+    with pytest.raises(D.DampError):
+        D.damp_state_pack(gpool, 0, dup, torch.zeros((B, HV, d, d), device="cuda"))
+    with pytest.raises(D.DampError):
+        D.damp_pool_reset_slots(gpool, 0, dup)
+    with pytest.raises(D.DampError):
+        D.damp_check_slots(gpool, dup)
+    torch.cuda.synchronize()
+    assert torch.equal(gpool.buffer, before)
+    ok = dev_i32([4, -1, 2])
+    D.damp_state_update_gdn(gpool, 0, ok, x["q"], x["k"], x["v"], x["g"], x["beta"])
+    D.damp_check_slots(gpool, dev_i32([-1, -1, 7, 7, 5]))  # padding may repeat
+    monkeypatch.setenv("DAMP_CHECK_SLOTS", "0")
+    D.damp_check_slots(gpool, [0, 1, 2])
+    torch.cuda.synchronize()
+
+
 # ------------------------------------------------------------- selection
 
 @pytest.mark.parametrize("kda", [False, True])
@@ -199,6 +232,38 @@ def test_selection_bit_exact(kda):
     assert np.array_equal(sel.numpy(), r["sel"])
     assert np.array_equal(perm.numpy(), r["perm"])
     assert np.array_equal(score.numpy(), r["C"])
+
+
+@pytest.mark.parametrize("kda,fmt,d", [(True, orc.FMT_PAPER, 128), (False, orc.FMT_PAPER, 64),
+                                       (True, orc.FMT_PAPER_PLAIN, 128), (False, None, 32)])
+def test_selection_under_the_deployed_low_tier(kda, fmt, d):
+    """E measured with the deployed Q_lo (App. A.2): the selection with the
+    paper's tier as `lo` equals the calibration oracle fed the same samples
+    (one domain), bit for bit: kept channels, pi and C."""
+    N, H, k_hi = 20, 4, 16
+    _say(f"select lo={fmt} kda={kda} d={d}")
+    states = inputs.synthetic_states(31 + d, N, H, d)
+    inputs.scale_channels(states, inputs.outlier_channels(32, H, d, 8), 10.0)
+    rng = np.random.default_rng(33)
+    g = inputs.to_bf16_bits(-np.abs(rng.normal(0, 1, (N, H, d) if kda else (N, H))))
+    cal = orc.Calib(kda=kda, H=H, dk=d, dv=d, fmt=fmt)
+    for n in range(N):  # sample n is a batch of one request
+        cal.accumulate(0, states[n:n + 1], g[n:n + 1])
+    want = cal.finalize(k_hi)
+    lo = D.damp_layout_init(d, d, 0)
+    if fmt is not None:
+        lo.hi_dtype, lo.group, lo.meta_dtype, lo.hadamard = fmt
+    sel, perm, score = D.damp_select_channels(torch.from_numpy(states).cuda(),
+                                              torch.from_numpy(orc.bf16_widen(g)).cuda(), k_hi,
+                                              kda=kda, lo=lo)
+    assert np.array_equal(score.numpy(), want["score"])
+    assert np.array_equal(sel.numpy(), want["sel"])
+    assert np.array_equal(perm.numpy(), want["perm"])
+    if fmt is not None:  # a different Q_lo measures different errors
+        _, _, s_row = D.damp_select_channels(torch.from_numpy(states).cuda(),
+                                             torch.from_numpy(orc.bf16_widen(g)).cuda(), k_hi,
+                                             kda=kda)
+        assert not np.array_equal(s_row.numpy(), score.numpy())
 
 
 # ------------------------------------------------- multi-step trajectory

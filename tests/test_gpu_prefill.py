@@ -124,3 +124,67 @@ def test_prefill_kda_blocks_with_vanishing_decay():
                           s16_exact_min=0.99)
     _say(f"  o rel-L2 {err:.2e}  {stats}")
     assert err <= 1e-4
+
+
+def test_prefill_gdn_vanishing_and_zero_decay():
+    """GDN at d = 128 defers the scalar decay as S = gamma P with gamma kept in
+    [2^-40, 2^40]; a token whose decay would take gamma out of that range is
+    applied to P directly. Here: a zero decay (g = -inf), decays below the
+    smallest normal fp32 number (g = -100, -90), and a run of e^-5 decays
+    whose product leaves the range in the middle of a block."""
+    d, HK, HV, B, T, k_hi = 128, 1, 2, 2, 24, 16
+    seed = 741
+    slots = inputs.slot_order(seed, B + 2, B)
+    perm = inputs.random_perms(seed, HV, d)
+    ref = orc.Pool(orc.KIND_MIXED, d, d, k_hi, 1, B + 2, HV)
+    orc.pack(ref, 0, slots, inputs.synthetic_states(seed, B, HV, d), perm)
+    gpool = gpu_pool_from(ref, D)
+    inp = inputs.as_prefill(inputs.decode_inputs(seed, T, B, HK, HV, d))
+    g = inp["g"].copy()  # bf16 bits [B, T, HV]
+    bits = lambda x: inputs.to_bf16_bits(np.float32(x))[0]
+    g[0, 3, 0] = bits(-np.inf)
+    g[0, 10, 0] = bits(-100.0)
+    g[1, 5:15, 1] = bits(-5.0)
+    g[1, 20, 1] = bits(-90.0)
+    g[0, 17, 1] = bits(-np.inf)
+    inp["g"] = g
+    o_gpu, o_ref = _run(False, ref, gpool, slots, inp, perm)
+    assert np.isfinite(o_gpu).all()
+    err = rel_l2(o_gpu, o_ref)
+    stats = compare_tiles(gpool.buffer.cpu().numpy(), ref, "prefill GDN vanishing decay",
+                          s16_exact_min=0.99)
+    _say(f"  o rel-L2 {err:.2e}  {stats}")
+    assert err <= 1e-4
+
+
+def test_calibrate_sequence_gdn_vanishing_decay():
+    """The calibration trajectory of GDN at d = 128 runs through the same
+    deferred-decay prefill kernel: zero and sub-normal decays (g = -inf,
+    -100) between the sampled tokens keep the FP32 trajectory finite and
+    equal to the oracle's."""
+    d, H, HK, B, T = 128, 2, 1, 2, 24
+    inp = inputs.decode_inputs(743, T, B, HK, H, d)
+    bits = lambda x: inputs.to_bf16_bits(np.float32(x))[0]
+    g = inp["g"].copy()  # step-major [T, B, H]
+    g[3, 0, 0] = bits(-np.inf)
+    g[10, 1, 1] = bits(-100.0)
+    g[12:14, 0, 1] = bits(-60.0)
+    inp["g"] = g
+    cal_ref = orc.Calib(kda=False, H=H, dk=d, dv=d)
+    S_ref = orc.calibrate_sequence(cal_ref, 0, np.zeros((B, H, d, d), np.float32), stride=8, **inp)
+    pool = D.Pool(D.damp_layout_init(d, d, 0, D.DAMP_STATE_FP32), 1, B, H)
+    slots = torch.arange(B, dtype=torch.int32, device="cuda")
+    D.damp_pool_reset_slots(pool, 0, slots)
+    cal = D.Calib(D.damp_layout_init(d, d, 0), kda=False, num_heads=H)
+    x = {n: torch.from_numpy(np.ascontiguousarray(np.swapaxes(a, 0, 1)).view(np.int16)).cuda()
+         .view(torch.bfloat16) for n, a in inp.items()}
+    D.damp_calibrate_sequence(cal, 0, pool, 0, slots, x["q"], x["k"], x["v"], x["g"], x["beta"])
+    S_gpu = D.damp_state_unpack(pool, 0, slots).cpu().numpy()
+    torch.cuda.synchronize()
+    assert np.isfinite(S_gpu).all()
+    assert np.linalg.norm(S_gpu - S_ref) <= 1e-5 * np.linalg.norm(S_ref)
+    h = cal.buffer.cpu().numpy()
+    sums = h[:3 * H * d].reshape(3, H, d)
+    assert np.isfinite(sums).all()
+    np.testing.assert_allclose(sums[0], cal_ref.sums[0, 0], rtol=2e-3)
+    np.testing.assert_allclose(sums[1], cal_ref.sums[0, 1], rtol=1e-5)
