@@ -343,6 +343,32 @@ damp_status damp_select_channels(int32_t is_kda, int32_t N, int32_t H,
                                  uint8_t* perm_out, double* score_out,
                                  void* stream);
 
+/* Bytes of the fixed device scratch of damp_select_channels_noalloc. */
+#define DAMP_SELECT_NOALLOC_SCRATCH_BYTES (16 << 20)
+
+/* damp_select_channels without any allocation, for callers that cannot
+ * allocate memory (inside HIP graph capture, in tight serving loops, under
+ * harnesses that forbid hipMalloc). Arguments, results and errors are those
+ * of damp_select_channels, bit for bit; the device scratch is instead a fixed
+ * array of DAMP_SELECT_NOALLOC_SCRATCH_BYTES inside the library, one per GPU,
+ * which each GPU holds from its first call until the process ends (the host
+ * side uses fixed buffers too). Limit: (N + 2) * H * d_k doubles must fit in
+ * it, i.e. (N + 2) * H * d_k <= 2097152 (the KDA calibration of 256 samples
+ * x 32 heads x 128 channels fits); larger calls return DAMP_ERR_INVALID_ARG
+ * before anything runs. Every call on one GPU shares that GPU's array and
+ * overwrites what the previous call left (nothing in it needs clearing: each
+ * call writes every element it reads), so calls that overlap on one GPU,
+ * from different streams or threads, race on it: serialize them.
+ * Synchronises `stream`. */
+damp_status damp_select_channels_noalloc(int32_t is_kda, int32_t N, int32_t H,
+                                         int32_t d_k, int32_t d_v,
+                                         const float* states,
+                                         const float* log_decay,
+                                         const damp_layout* lo, int32_t k_hi,
+                                         double tau, int32_t* sel_out,
+                                         uint8_t* perm_out, double* score_out,
+                                         void* stream);
+
 /* ------------------------------------------------------------------------
  * On-device calibration (App. A.2, Eq. (13)-(15); Alg. 1 in App. A.4; the
  * key-channel selector ablation of section 6; the calibration-split

@@ -14,7 +14,7 @@
 #include <algorithm>
 #include <cfloat>
 #include <cmath>
-#include <vector>
+#include <mutex>
 
 #include "internal.hpp"
 
@@ -134,42 +134,52 @@ damp_status select_run(const char* name, int32_t is_kda, int32_t N, int32_t H, i
                      d_lsum);
   damp_status st = check_launch(name);
   if (st != DAMP_OK) return st;
-  std::vector<double> sums(2 * hk);
-  hipError_t e = hipMemcpyAsync(sums.data(), d_esum, 2 * hk * sizeof(double),
-                                hipMemcpyDeviceToHost, s);
-  if (e == hipSuccess) e = hipStreamSynchronize(s);
-  if (e != hipSuccess) return fail(DAMP_ERR_HIP, "%s: %s", name, hipGetErrorString(e));
-
-  const double* esum = sums.data();
-  const double* lsum = sums.data() + hk;
-  std::vector<double> score(d_k);
-  std::vector<int> order(d_k);
-  std::vector<char> keep(d_k);
-  for (int h = 0; h < H; ++h) {
-    for (int u = 0; u < d_k; ++u) {
-      const size_t i = static_cast<size_t>(h) * d_k + u;
-      const double E = esum[i] / static_cast<double>(N);           // Eq. (8)
-      const double a_eff = std::exp(lsum[i] / static_cast<double>(N));
-      const double gap = 1.0 - a_eff * a_eff;
-      const double P = 1.0 / (gap > tau ? gap : tau);              // Eq. (9)
-      score[u] = E * P;                                              // C = E P
-      if (score_out) score_out[i] = score[u];
-      order[u] = u;
-    }
-    std::sort(order.begin(), order.end(), [&](int a, int b) {
-      if (score[a] != score[b]) return score[a] > score[b];
-      return a < b;
-    });
-    std::fill(keep.begin(), keep.end(), 0);
-    for (int i = 0; i < k_hi; ++i) keep[order[i]] = 1;
-    int p = 0, q = 0;
-    for (int u = 0; u < d_k; ++u)
-      if (keep[u]) {
-        perm_out[static_cast<size_t>(h) * d_k + p++] = static_cast<uint8_t>(u);
-        sel_out[static_cast<size_t>(h) * k_hi + q++] = u;
+  // The per-channel sums reach the host a few heads at a time through a
+  // fixed staging buffer, and the ranking works in fixed arrays (d_k <= 256),
+  // so the host side allocates nothing either.
+  constexpr int kStage = 4096;
+  double stage[kStage];
+  double score[256];
+  int order[256];
+  bool keep[256];
+  const int per_copy = kStage / (2 * d_k);
+  for (int h0 = 0; h0 < H; h0 += per_copy) {
+    const int nh = std::min(per_copy, H - h0);
+    const size_t n = static_cast<size_t>(nh) * d_k;
+    const size_t off = static_cast<size_t>(h0) * d_k;
+    hipError_t e = hipMemcpyAsync(stage, d_esum + off, n * sizeof(double),
+                                  hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(stage + n, d_lsum + off, n * sizeof(double), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return fail(DAMP_ERR_HIP, "%s: %s", name, hipGetErrorString(e));
+    for (int h = h0; h < h0 + nh; ++h) {
+      const double* esum = stage + static_cast<size_t>(h - h0) * d_k;
+      const double* lsum = esum + n;
+      for (int u = 0; u < d_k; ++u) {
+        const double E = esum[u] / static_cast<double>(N);           // Eq. (8)
+        const double a_eff = std::exp(lsum[u] / static_cast<double>(N));
+        const double gap = 1.0 - a_eff * a_eff;
+        const double P = 1.0 / (gap > tau ? gap : tau);              // Eq. (9)
+        score[u] = E * P;                                              // C = E P
+        if (score_out) score_out[static_cast<size_t>(h) * d_k + u] = score[u];
+        order[u] = u;
+        keep[u] = false;
       }
-    for (int u = 0; u < d_k; ++u)
-      if (!keep[u]) perm_out[static_cast<size_t>(h) * d_k + p++] = static_cast<uint8_t>(u);
+      std::sort(order, order + d_k, [&](int a, int b) {
+        if (score[a] != score[b]) return score[a] > score[b];
+        return a < b;
+      });
+      for (int i = 0; i < k_hi; ++i) keep[order[i]] = true;
+      int p = 0, q = 0;
+      for (int u = 0; u < d_k; ++u)
+        if (keep[u]) {
+          perm_out[static_cast<size_t>(h) * d_k + p++] = static_cast<uint8_t>(u);
+          sel_out[static_cast<size_t>(h) * k_hi + q++] = u;
+        }
+      for (int u = 0; u < d_k; ++u)
+        if (!keep[u]) perm_out[static_cast<size_t>(h) * d_k + p++] = static_cast<uint8_t>(u);
+    }
   }
   return DAMP_OK;
 }
@@ -197,4 +207,77 @@ extern "C" damp_status damp_select_channels(int32_t is_kda, int32_t N, int32_t H
   // the stream was synchronised unless a launch failed; the free waits for the device
   (void)hipFree(scratch);
   return st;
+}
+
+// ---- damp_select_channels_noalloc: the same selection with its device
+// scratch in a fixed array of the library, one copy per GPU (held until the
+// process ends), instead of a hipMalloc per call.
+
+static __device__ __align__(256) double
+    scratch[DAMP_SELECT_NOALLOC_SCRATCH_BYTES / sizeof(double)];
+
+namespace damp {
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+double* g_scratch[kMaxDevices] = {};
+
+// The device address of `scratch` on the GPU that runs stream s, looked up
+// once per GPU with that GPU current. In host code the array's name stands
+// for a host-side shadow, never for device memory, so kernels only ever get
+// this address.
+damp_status scratch_for(hipStream_t s, double** out, const char* name) {
+  int dev = 0;
+  hipError_t e = s ? hipStreamGetDevice(s, &dev) : hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(DAMP_ERR_HIP, "%s: %s", name, hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(DAMP_ERR_INVALID_ARG, "%s: device %d beyond the %d supported", name, dev,
+                kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    int cur = 0;
+    e = hipGetDevice(&cur);
+    if (e == hipSuccess && cur != dev) e = hipSetDevice(dev);
+    void* p = nullptr;
+    if (e == hipSuccess) e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != dev) (void)hipSetDevice(cur);
+    if (e != hipSuccess || !p)
+      return fail(DAMP_ERR_HIP, "%s: device address of the scratch array: %s", name,
+                  e != hipSuccess ? hipGetErrorString(e) : "null");
+    g_scratch[dev] = static_cast<double*>(p);
+  }
+  *out = g_scratch[dev];
+  return DAMP_OK;
+}
+
+}  // namespace
+}  // namespace damp
+
+extern "C" damp_status damp_select_channels_noalloc(int32_t is_kda, int32_t N, int32_t H,
+                                                    int32_t d_k, int32_t d_v,
+                                                    const float* states,
+                                                    const float* log_decay,
+                                                    const damp_layout* lo, int32_t k_hi,
+                                                    double tau, int32_t* sel_out,
+                                                    uint8_t* perm_out, double* score_out,
+                                                    void* stream) {
+  using namespace damp;
+  clear_error();
+  const char* name = "damp_select_channels_noalloc";
+  damp_status st = select_validate(name, is_kda, N, H, d_k, d_v, states, log_decay, lo, k_hi,
+                                   tau, sel_out, perm_out);
+  if (st != DAMP_OK) return st;
+  const int64_t need = select_scratch_doubles(N, H, d_k);
+  constexpr int64_t kMax = DAMP_SELECT_NOALLOC_SCRATCH_BYTES / sizeof(double);
+  if (need > kMax)
+    return fail(DAMP_ERR_INVALID_ARG, "%s: (N + 2) * H * d_k = %lld doubles exceed the %lld of "
+                "the fixed scratch (%d bytes)", name, static_cast<long long>(need),
+                static_cast<long long>(kMax), DAMP_SELECT_NOALLOC_SCRATCH_BYTES);
+  hipStream_t s = as_stream(stream);
+  double* buf = nullptr;
+  st = scratch_for(s, &buf, name);
+  if (st != DAMP_OK) return st;
+  return select_run(name, is_kda, N, H, d_k, d_v, states, log_decay, lo, k_hi, tau, sel_out,
+                    perm_out, score_out, buf, s);
 }

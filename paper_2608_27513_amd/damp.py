@@ -54,7 +54,7 @@ EXPORTS = ("damp_layout_init", "damp_tile_bytes", "damp_tile_stride", "damp_bits
            "damp_pool_required_bytes", "damp_pool_init", "damp_check_slots", "damp_pool_reset_slots",
            "damp_state_update_gdn", "damp_state_update_kda", "damp_state_prefill_gdn",
            "damp_state_prefill_kda", "damp_state_pack", "damp_state_unpack",
-           "damp_select_channels", "damp_calib_required_bytes", "damp_calib_init",
+           "damp_select_channels", "damp_select_channels_noalloc", "damp_calib_required_bytes", "damp_calib_init",
            "damp_calib_accumulate", "damp_calibrate_sequence", "damp_calib_finalize",
            "damp_topk_overlap", "damp_spearman", "damp_last_error")
 
@@ -92,6 +92,8 @@ def lib() -> ctypes.CDLL:
         "damp_state_pack": (st, [PP, i32, P, i32, P, P, P]),
         "damp_state_unpack": (st, [PP, i32, P, i32, P, P, P]),
         "damp_select_channels": (st, [i32, i32, i32, i32, i32, P, P, LP, i32, f64, P, P, P, P]),
+        "damp_select_channels_noalloc": (st, [i32, i32, i32, i32, i32, P, P, LP, i32, f64, P, P,
+                                              P, P]),
         "damp_calib_required_bytes": (sz, [i32, i32, i32]),
         "damp_calib_init": (st, [CP, LP, i32, i32, i32, P, sz, P]),
         "damp_calib_accumulate": (st, [CP, i32, PP, i32, P, i32, P, P, P]),
@@ -339,11 +341,7 @@ def damp_state_unpack(pool: Pool, layer: int, slot_idx, perm=None, S_out=None, s
 
 # --------------------------------------------------------------- selection
 
-def damp_select_channels(states, log_decay, k_hi: int, *, kda: bool, lo: damp_layout = None,
-                         tau: float = 1e-4, stream=None):
-    """Alg. 1 on device-resident calibration samples, with E measured under
-    the low tier of `lo` (None: the per-row quantizer); returns host tensors
-    (sel int32 [H, k_hi], perm uint8 [H, d_k], score float64 [H, d_k])."""
+def _select(fn, states, log_decay, k_hi, kda, lo, tau, stream):
     states = _dev(states, torch.float32, "states")
     if states.dim() != 4:
         raise ValueError("states must be [N, H, d_k, d_v]")
@@ -352,11 +350,26 @@ def damp_select_channels(states, log_decay, k_hi: int, *, kda: bool, lo: damp_la
     sel = torch.zeros((H, k_hi), dtype=torch.int32)
     perm = torch.zeros((H, dk), dtype=torch.uint8)
     score = torch.zeros((H, dk), dtype=torch.float64)
-    _check(lib().damp_select_channels(int(kda), N, H, dk, dv, _ptr(states), _ptr(log_decay),
-                                      None if lo is None else ctypes.byref(lo), k_hi,
-                                      float(tau), _ptr(sel), _ptr(perm), _ptr(score),
-                                      _stream(stream)))
+    _check(fn(int(kda), N, H, dk, dv, _ptr(states), _ptr(log_decay),
+              None if lo is None else ctypes.byref(lo), k_hi, float(tau), _ptr(sel), _ptr(perm),
+              _ptr(score), _stream(stream)))
     return sel, perm, score
+
+
+def damp_select_channels(states, log_decay, k_hi: int, *, kda: bool, lo: damp_layout = None,
+                         tau: float = 1e-4, stream=None):
+    """Alg. 1 on device-resident calibration samples, with E measured under
+    the low tier of `lo` (None: the per-row quantizer); returns host tensors
+    (sel int32 [H, k_hi], perm uint8 [H, d_k], score float64 [H, d_k])."""
+    return _select(lib().damp_select_channels, states, log_decay, k_hi, kda, lo, tau, stream)
+
+
+def damp_select_channels_noalloc(states, log_decay, k_hi: int, *, kda: bool,
+                                 lo: damp_layout = None, tau: float = 1e-4, stream=None):
+    """As damp_select_channels, with the library's fixed device scratch
+    instead of an allocation per call ((N + 2) * H * d_k <= 2^21)."""
+    return _select(lib().damp_select_channels_noalloc, states, log_decay, k_hi, kda, lo, tau,
+                   stream)
 
 
 # ------------------------------------------------------------- calibration

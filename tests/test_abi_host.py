@@ -36,7 +36,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = declared_functions()
-    assert len(names) == 23
+    assert len(names) == 24
     for n in names:
         assert hasattr(L, n), n
     assert sorted(D.EXPORTS) == names
@@ -270,6 +270,22 @@ def test_select_validation(L):
     assert f(0, 4, 2, 128, 128, p, p, None, 16, 0.0, p, p, None, None) == D.DAMP_ERR_INVALID_ARG
     assert f(0, 0, 2, 128, 128, p, p, None, 16, 1e-4, p, p, None, None) == D.DAMP_ERR_INVALID_ARG
     assert f(0, 4, 2, 300, 128, p, p, None, 16, 1e-4, p, p, None, None) == D.DAMP_ERR_INVALID_ARG
+    assert f(0, 4, 2, 128, 128, None, p, None, 16, 1e-4, p, p, None, None) == \
+        D.DAMP_ERR_INVALID_ARG
+
+
+def test_select_noalloc_refuses_calls_beyond_its_scratch(L):
+    """The no-allocation selection keeps (N + 2) * H * d_k doubles in a fixed
+    16 MiB array: larger calls fail before anything runs, with the limit in
+    the message; its argument checks are those of damp_select_channels."""
+    p = ctypes.c_void_p(0x7f0000100000)  # never dereferenced
+    f = L.damp_select_channels_noalloc
+    assert (254 + 2) * 64 * 128 == 2 ** 21  # the largest N at H = 64, d_k = 128
+    st, msg = _status(f, 1, 255, 64, 128, 128, p, p, None, 16, 1e-4, p, p, None, None)
+    assert st == D.DAMP_ERR_INVALID_ARG and "scratch" in msg and "2097152" in msg
+    st, msg = _status(f, 0, 100000, 32, 128, 128, p, p, None, 16, 1e-4, p, p, None, None)
+    assert st == D.DAMP_ERR_INVALID_ARG and "scratch" in msg
+    assert f(0, 4, 2, 128, 128, p, p, None, 129, 1e-4, p, p, None, None) == D.DAMP_ERR_INVALID_ARG
     assert f(0, 4, 2, 128, 128, None, p, None, 16, 1e-4, p, p, None, None) == \
         D.DAMP_ERR_INVALID_ARG
 
