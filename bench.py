@@ -570,6 +570,28 @@ def calibration_bench(torch, D, inputs, log=print, T: int = 2048, stride: int = 
     return res
 
 
+def accuracy_bench(torch, log=print):
+    """Held-out trajectory accuracy (App. E's state and output RRMSE against
+    the FP32 state) of uniform INT8 and of 16 protected rows chosen by a
+    random, an E-only and the C = E P selector, in the default and the
+    paper's INT8+H32 tiers, on the GDN and KDA decode workloads (B = 64, 512
+    warm-up tokens, selection from a separate 2048-token calibration
+    sequence, 256 held-out decode steps). The paper's figures are context:
+    real model trajectories, INT8+H32 with 16 FP16 rows (App. E)."""
+    from paper_2608_27513_amd import accuracy as A
+
+    out = {}
+    t0 = time.time()
+    for name, kda in (("gdn", False), ("kda", True)):
+        out[name] = A.study(kda=kda, B=64, steps=256, seed=0, log=log)
+        torch.cuda.empty_cache()
+    out["seconds"] = round(time.time() - t0, 1)
+    out["paper_context"] = {"gdn_common_16_16": {"state_rrmse": 8.748e-3, "output_rrmse": 2.256e-3},
+                            "source": "App. E, held-out Qwen3.6 trajectories, INT8+H32 + 16 FP16 rows"}
+    out["parity"] = "unpinned (no printed value for synthetic inputs)"
+    return out
+
+
 def cpu_baseline(seconds: float, log=print):
     """The CPU oracle on the GDN workload (B=256, 16/32 heads, d=128, 16 BF16 rows),
     timed on the host: as many whole decode steps as fit in `seconds`."""
@@ -710,6 +732,7 @@ def main():
         extra["prefill_kda"] = prefill_bench(torch, D, inputs, 10, log=log, kda=True)
         extra["pack_unpack_gdn"] = pack_unpack_bench(torch, D, 20, log=log)
         extra["calibration_kda"] = calibration_bench(torch, D, inputs, log=log)
+        extra["accuracy"] = accuracy_bench(torch, log=log)
 
     cpu = None
     if not args.quick and not args.no_cpu:
