@@ -217,3 +217,78 @@ def test_error_recurrence_with_each_format(fmt, kda):
         dS = Sq - S_ref
         assert np.linalg.norm(dS - (A @ dS_prev + R)) <= 1e-3 * np.linalg.norm(dS)
         dS_prev = dS
+
+
+def _nvfp4_tile(S, k_hi):
+    """Packs one natural-order tile [d, d] in NVFP4 and returns the low tier's
+    codes (one E2M1 code per value, [d - k_hi, d]), its E4M3 block-scale
+    bytes ([d - k_hi, d / 16]), the fp32 global scale and the reconstruction."""
+    d = S.shape[0]
+    pool = orc.Pool(orc.KIND_MIXED, d, d, k_hi, 1, 1, 1, fmt=orc.FMT_NVFP4)
+    orc.pack(pool, 0, [0], S[None, None])
+    nl = d - k_hi
+    t = pool.buf
+    c0 = k_hi * d * 2
+    packed = t[c0:c0 + nl * d // 2].reshape(nl, d // 2)
+    codes = np.empty((nl, d), np.uint8)
+    codes[:, 0::2] = packed & 0x0F  # the even column in the low nibble
+    codes[:, 1::2] = packed >> 4
+    m0 = c0 + nl * d // 2
+    sb = t[m0:m0 + nl * d // 16].reshape(nl, d // 16)
+    sg = t[m0 + nl * d // 16:m0 + nl * d // 16 + 4].copy().view(np.float32)[0]
+    rec = orc.unpack(pool, 0, [0])[0, 0]
+    return codes, sb, sg, rec
+
+
+def _wide_tiles(seed, n, d):
+    """Tiles whose rows span many octaves, with a few large outliers."""
+    rng = np.random.default_rng(seed)
+    for _ in range(n):
+        S = rng.standard_normal((d, d)).astype(np.float32)
+        S *= np.exp2(rng.uniform(-12, 12, size=(d, 1))).astype(np.float32)
+        idx = rng.integers(0, d, size=(3, 2))
+        S[idx[:, 0], idx[:, 1]] *= np.float32(rng.uniform(20, 200))
+        yield S
+
+
+def test_nvfp4_scale_rule_properties():
+    """Properties of NVFP4's two-level scale that fix its constants without
+    restating them (App. A.1's format table: E2M1 values whose largest
+    magnitude is 6, E4M3 block scales whose largest finite value is 448, one
+    fp32 global scale): the tile's largest magnitude uses the whole range of
+    both, so its block scale is 448, its code is +-6 and it reconstructs to
+    itself; every block's largest magnitude is coded +-6; every block scale
+    is a finite E4M3 value; every value
+    reconstructs within one E2M1 step (at most 1 in units of its block's
+    scale) of itself, saturation included; and scaling a tile by a power of
+    two scales only the global scale."""
+    d, k_hi = 64, 8
+    for S in _wide_tiles(41, 12, d):
+        codes, sb, sg, rec = _nvfp4_tile(S, k_hi)
+        lo, rec_lo = S[k_hi:], rec[k_hi:]
+        i, j = np.unravel_index(np.argmax(np.abs(lo)), lo.shape)
+        amax = np.abs(lo[i, j])
+        assert orc.e4m3_widen(sb[i, j // 16:j // 16 + 1])[0] == 448.0
+        assert codes[i, j] & 0x7 == 0x7 and (codes[i, j] >> 3) == (lo[i, j] < 0)
+        assert abs(abs(rec_lo[i, j]) - amax) <= 4 * np.spacing(amax)
+        assert orc.e4m3_widen(sb).max() == 448.0
+        assert np.all((sb & 0x7F) != 0x7F)  # no E4M3 NaN
+        block = np.repeat(orc.e4m3_widen(sb).astype(np.float64) * sg, 16, axis=1)
+        err = np.abs(rec_lo.astype(np.float64) - lo)
+        normal = block >= 2.0 ** -6 * sg  # E4M3 normal block scales
+        assert np.all(err[normal] <= block[normal] * (1 + 1e-6))
+        # each block's scale spans the E2M1 range: its largest magnitude is
+        # coded +-6 (within E4M3's rounding of the scale, 6 / (1 +- 2^-4)
+        # still rounds to 6), wherever that scale is a normal E4M3 value
+        blocks = np.abs(lo).reshape(d - k_hi, d // 16, 16)
+        top = np.argmax(blocks, axis=2)
+        top_codes = np.take_along_axis(codes.reshape(d - k_hi, d // 16, 16), top[..., None],
+                                       axis=2)[..., 0]
+        sbv = orc.e4m3_widen(sb)
+        live = (sbv >= 2.0 ** -6) & (blocks.max(axis=2) > 0)
+        assert live.sum() >= 32
+        assert np.all(top_codes[live] & 0x7 == 0x7)
+        for k in (-7, 5):
+            codes2, sb2, sg2, _ = _nvfp4_tile(S * np.float32(2.0 ** k), k_hi)
+            assert np.array_equal(codes2, codes) and np.array_equal(sb2, sb)
+            assert sg2 == sg * np.float32(2.0 ** k)
