@@ -173,7 +173,18 @@ __device__ __forceinline__ void decode16(const W& w, float A, float B0, float (&
   }
 }
 
-// Operands of one tile as loaded by the operand threads (raw bf16 bits).
+// A 16-bit value that is the same for the whole workgroup, through the scalar
+// cache: the 4-byte word holding it (aligned down, so it never crosses a
+// page the value is not on) and the value's half of it.
+__device__ __forceinline__ uint32_t sload_u16(const uint16_t* base, size_t i) {
+  const uintptr_t a = reinterpret_cast<uintptr_t>(base + i);
+  const __attribute__((address_space(4))) uint32_t* w =
+      (const __attribute__((address_space(4))) uint32_t*)(a & ~static_cast<uintptr_t>(3));
+  return (*w >> ((a & 2u) * 8u)) & 0xffffu;
+}
+
+// Operands of one tile as loaded by the operand threads (raw bf16 bits; beta
+// and GDN's g are one value per tile, in scalar registers).
 struct OpsRegs {
   uint32_t k, q, g, v, beta;
 };
@@ -315,14 +326,15 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
 
   // ---- operand staging: the operand threads gather one tile row each
   auto issue_ops = [&](OpsRegs& r, int b_) {
+    const size_t bh = static_cast<size_t>(b_) * HV + h;
+    r.beta = sload_u16(p.beta, bh);
+    if (!KDA) r.g = sload_u16(p.g, bh);
     if (ops_thread) {
-      const size_t bh = static_cast<size_t>(b_) * HV + h;
       const size_t kq = (static_cast<size_t>(b_) * p.HK + hk) * D;
       r.k = p.k[kq + my_u];
       r.q = p.q[kq + my_u];
-      r.g = KDA ? p.g[bh * D + my_u] : p.g[bh];
+      if (KDA) r.g = p.g[bh * D + my_u];
       r.v = p.v[bh * D + tr];
-      r.beta = p.beta[bh];
     }
   };
   auto publish_ops = [&](const OpsRegs& r, int buf) {
@@ -424,13 +436,13 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
   // barrier, when every wave's rows are in mout: wave w writes the 256
   // contiguous bytes of rows k_hi + 32 w ..
   __amdgpu_buffer_rsrc_t rs_prev = make_rsrc(-1);
-  auto store_prev_meta = [&](int pbuf) {
+  auto store_prev_meta = [&](int pbuf, int ln) {
     if constexpr (!kP) {
-      const int r = k_hi + 32 * wave + lane;
-      const bool on = lane < 32 && r < D;
+      const int r = k_hi + 32 * wave + ln;
+      const bool on = ln < 32 && r < D;
       const float2 mo = mout[pbuf][on ? r : 0];
       st8(u32x2{__float_as_uint(mo.x), __float_as_uint(mo.y)}, rs_prev,
-          on ? meta0 + (32 * wave + lane) * 8 : kDrop);
+          on ? meta0 + (32 * wave + ln) * 8 : kDrop);
     }
   };
   int turn = b % 3;
@@ -573,7 +585,7 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
     part[pb][wave][s0q] = make_float4(r3[0], r3[1], r3[2], r3[3]);
     if (has_next) publish_ops(pub, buf_n);  // loaded a whole tile ago
     lds_barrier();
-    store_prev_meta(pb ^ 1);
+    store_prev_meta(pb ^ 1, lane);
     if (pf) issue_raw_part(cur, rs_pf, 3);
 
     // -- column totals of this lane's 4 slots over the 4 waves (the k lanes:
@@ -901,7 +913,8 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
   // the last tile's 8-byte metadata, once every wave has put its rows in mout
   if constexpr (!kP) {
     lds_barrier();
-    store_prev_meta(pb ^ 1);
+    // the lane index afresh: keeping the loop's copy alive to here costs a spill
+    store_prev_meta(pb ^ 1, static_cast<int>(__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u))));
   }
 }
 
