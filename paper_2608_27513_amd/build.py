@@ -34,6 +34,7 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-ffp-contract
 PER_FILE = {
     "update.hip": ["-fno-honor-nans"],
     "update_stream.hip": ["-fno-honor-nans"],
+    "update_fp32.hip": ["-fno-honor-nans"],
     "pack.hip": ["-fno-honor-nans"],
 }
 

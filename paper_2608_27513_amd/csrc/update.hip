@@ -319,6 +319,10 @@ damp_status update(bool kda, const damp_pool* pool, int32_t layer, const int32_t
       return fail(DAMP_ERR_HIP, "%s: occupancy query or launch failed", name);
     return check_launch(name);
   }
+  if (codec == kCodecFp32 && D == 128) {
+    launch_fp32_128(kda, p, B, s);
+    return check_launch(name);
+  }
   if (kda) launch_codec<true>(layout_codec(&pool->layout), D, p, B, s);
   else launch_codec<false>(layout_codec(&pool->layout), D, p, B, s);
   return check_launch(name);

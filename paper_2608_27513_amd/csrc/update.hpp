@@ -34,4 +34,8 @@ struct UpdateParams {
 // query or the launch failed).
 bool launch_stream128(bool kda, int fmt, const UpdateParams& p, int B, hipStream_t stream);
 
+// The FP32-state update at d = 128 (update_fp32.hip): one workgroup per tile,
+// grid (HV, B), every access whole 128-byte lines.
+void launch_fp32_128(bool kda, const UpdateParams& p, int B, hipStream_t stream);
+
 }  // namespace damp
