@@ -257,10 +257,11 @@ def time_steps(torch, calls, warmup: int, steps: int, prewarm_s: float = None):
 
 
 def measure(torch, D, wl: Workload, kind: int, k_hi: int, rotations: int, warmup: int,
-            steps: int, o_dtype, scattered: bool = False, tiers=None):
+            steps: int, o_dtype, scattered: bool = False, tiers=None, per_launch: bool = False):
     pool, sets, layout = wl.make_pool(kind, k_hi, rotations, scattered, tiers)
     calls = wl.prepared(pool, sets, o_dtype)
     t = time_steps(torch, calls, warmup, steps)
+    stats = launch_stats(torch, calls) if per_launch else None
     tb = D.damp_tile_bytes(layout)
     nbytes = algorithmic_bytes(tb, wl.B, wl.HK, wl.HV, wl.d, wl.kda,
                                2 if o_dtype == torch.bfloat16 else 4)
@@ -274,6 +275,10 @@ def measure(torch, D, wl: Workload, kind: int, k_hi: int, rotations: int, warmup
         bits_per_value=D.damp_bits_per_value(layout),
     )
     res["kernel_frac_peak"] = res["kernel_gbs"] / HBM_PEAK_GBS
+    if stats is not None:
+        stats["frac_hbm_peak_at_median"] = round(nbytes / (stats["median_us"] * 1e-6) / 1e9 /
+                                                 HBM_PEAK_GBS, 4)
+        res["launch_stats"] = stats
     del pool, calls
     torch.cuda.empty_cache()
     return res
@@ -323,23 +328,69 @@ def sweep(torch, D, inputs, steps: int, log=print):
     return out
 
 
-def copy_ceiling(torch, nbytes: int, rotations: int, steps: int, log=print):
-    """The practical ceiling of the update's memory traffic: a plain device
-    copy (torch's) moving the same bytes, half read and half written, over
-    `rotations` disjoint source/destination pairs so that no copy is served
-    from the last-level cache; timed like the update (steady clock, HIP
-    events around `steps` launches)."""
-    half = nbytes // 2 // 16 * 16
-    src = [torch.empty(half, dtype=torch.uint8, device="cuda").fill_(r) for r in range(rotations)]
-    dst = [torch.empty_like(x) for x in src]
-    calls = [lambda i=i: dst[i].copy_(src[i]) for i in range(rotations)]
-    t = time_steps(torch, calls, 20, steps, prewarm_s=0.2)
-    sec = t["mean_launch_s"]
-    res = dict(bytes=2 * half, copy_us=round(1e6 * sec, 2), copy_gbs=round(2 * half / sec / 1e9, 1))
-    log(f"  copy of the same state bytes: {res['copy_us']} us, {res['copy_gbs']} GB/s")
-    del src, dst
+def copy_ceiling(torch, D, wl, rotations: int, steps: int, log=print):
+    """The practical ceiling of the update's state traffic: an in-place copy
+    (every 16-byte piece read and written back, non-temporal, like the
+    update's tile accesses; `libcopyceiling.so`, built beside libdamp) over
+    the same rotated pool regions the headline updates, timed like the update
+    (steady clock, HIP events around `steps` launches); the fastest of a few
+    grid sizes."""
+    import ctypes
+
+    from paper_2608_27513_amd import build as B
+
+    lib = ctypes.CDLL(B.BENCH_LIB)
+    lib.copy_ceiling_inplace.restype = ctypes.c_int
+    lib.copy_ceiling_inplace.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int,
+                                         ctypes.c_void_p]
+    pool, sets, layout = wl.make_pool(D.DAMP_STATE_MIXED, wl.k_hi, rotations)
+    region = wl.B * wl.HV * pool.tile_stride  # one rotation's slots are contiguous
+    base = pool.buffer.data_ptr()
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    best = None
+    for grid in (512, 1024, 2048):
+        def call(r, grid=grid):
+            rc = lib.copy_ceiling_inplace(ctypes.c_void_p(base + r * region), region, grid, stream)
+            if rc != 0:
+                raise RuntimeError(f"copy_ceiling_inplace returned {rc}")
+        calls = [lambda r=r: call(r) for r in range(rotations)]
+        t = time_steps(torch, calls, 20, steps, prewarm_s=0.2)
+        if best is None or t["mean_launch_s"] < best[1]:
+            best = (grid, t["mean_launch_s"])
+    sec = best[1]
+    res = dict(bytes=2 * region, grid=best[0], copy_us=round(1e6 * sec, 2),
+               copy_gbs=round(2 * region / sec / 1e9, 1),
+               copy_frac_hbm_peak=round(2 * region / sec / 1e9 / HBM_PEAK_GBS, 4),
+               kernel="in-place 16-byte non-temporal copy of the rotated pool regions")
+    log(f"  in-place copy of the same state bytes: {res['copy_us']} us, {res['copy_gbs']} GB/s "
+        f"(grid {best[0]})")
+    del pool
     torch.cuda.empty_cache()
     return res
+
+
+def launch_stats(torch, calls, groups: int = 10, per_group: int = 20):
+    """Kernel duration over groups x per_group launches (after the calls have
+    run at the steady clock): each group of back-to-back launches is
+    bracketed by its own HIP event pair on the launch stream, and the
+    duration per launch of each group is reported as the median, minimum and
+    maximum over the groups. An event pair around every single launch would
+    break the back-to-back stream and add each launch's own ramp."""
+    import statistics
+
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(groups)]
+    i = 0
+    for a, b in evs:
+        a.record()
+        for _ in range(per_group):
+            calls[i % len(calls)]()
+            i += 1
+        b.record()
+    torch.cuda.synchronize()
+    d = [1e3 * a.elapsed_time(b) / per_group for a, b in evs]
+    return dict(launches=groups * per_group, groups=groups, median_us=round(statistics.median(d), 3),
+                min_us=round(min(d), 3), max_us=round(max(d), 3))
 
 
 def pack_unpack_bench(torch, D, steps: int, log=print):
@@ -668,13 +719,12 @@ def main():
     gdn = Workload(torch, D, inputs, kda=False, B=B, HK=HK, HV=HV, d=d, k_hi=k_hi,
                    rotations=args.rotations, seed=0, log=log)
     head = measure(torch, D, gdn, D.DAMP_STATE_MIXED, k_hi, args.rotations, args.warmup,
-                   args.steps, torch.bfloat16)
+                   args.steps, torch.bfloat16, per_launch=True)
     log(f"  mixed: {head['us_per_step']:.1f} us/step, kernel {head['kernel_us']:.1f} us, "
         f"{head['kernel_gbs']:.0f} GB/s ({100 * head['kernel_frac_peak']:.1f}% of peak)")
     extra = {}
     if not args.quick:
-        cop = copy_ceiling(torch, 2 * head["tile_bytes"] * B * HV, args.rotations, args.steps,
-                           log=log)
+        cop = copy_ceiling(torch, D, gdn, args.rotations, max(args.steps, 100), log=log)
         cop["update_frac_of_copy"] = round(cop["copy_us"] / head["kernel_us"], 4)
         extra["practical_ceiling"] = cop
         scat = measure(torch, D, gdn, D.DAMP_STATE_MIXED, k_hi, args.rotations, args.warmup,
@@ -713,7 +763,7 @@ def main():
         kda = Workload(torch, D, inputs, kda=True, B=B, HK=32, HV=32, d=d, k_hi=k_hi,
                        rotations=args.rotations, seed=1, log=log)
         km = measure(torch, D, kda, D.DAMP_STATE_MIXED, k_hi, args.rotations, args.warmup,
-                     args.steps, torch.bfloat16)
+                     args.steps, torch.bfloat16, per_launch=True)
         kf = measure(torch, D, kda, D.DAMP_STATE_FP32, 0, max(2, args.rotations // 2),
                      args.warmup, args.steps, torch.bfloat16)
         log(f"  kda mixed: kernel {km['kernel_us']:.1f} us ({100 * km['kernel_frac_peak']:.1f}%),"
@@ -768,7 +818,8 @@ def main():
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(head["kernel_frac_peak"], 4),
                      "traffic": traffic,
-                     "kernel_us": round(head["kernel_us"], 2)},
+                     "kernel_us": round(head["kernel_us"], 2),
+                     "launch_stats": head.get("launch_stats")},
         "cpu_baseline": cpu,
         "storage": {"tile_bytes": head["tile_bytes"], "bits_per_value": head["bits_per_value"],
                     "reduction_vs_fp32_pct": round(100 * (1 - head["bits_per_value"] / 32), 2)},

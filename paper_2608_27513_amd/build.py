@@ -50,8 +50,27 @@ def _compile(src: str) -> str:
     return obj
 
 
+BENCH_SRC = os.path.join(HERE, "bench_csrc", "copy_ceiling.hip")
+BENCH_LIB = os.path.join(HERE, "libcopyceiling.so")
+
+
+def build_bench(verbose: bool = False) -> str:
+    """Compiles the benchmark's copy-ceiling kernel (not part of libdamp)."""
+    tmp = BENCH_LIB + ".tmp"
+    cmd = [HIPCC, *COMMON, "-shared", BENCH_SRC, "-o", tmp]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed on {BENCH_SRC}:\n{r.stderr}")
+    os.replace(tmp, BENCH_LIB)
+    if verbose:
+        print(f"built {BENCH_LIB}")
+    return BENCH_LIB
+
+
 def build(verbose: bool = False) -> str:
-    """Compiles every source under csrc/ and links libdamp.so; returns its path."""
+    """Compiles every source under csrc/ and links libdamp.so, and the
+    benchmark's copy kernel; returns the library's path."""
+    build_bench(verbose)
     os.makedirs(OBJDIR, exist_ok=True)
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
     with cf.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:

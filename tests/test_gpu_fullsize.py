@@ -197,3 +197,53 @@ def test_full_size_prefill_sampled(kda):
     stats = compare_tiles(got, ref, "full-size prefill", s16_exact_min=0.99)
     _say(f"  o rel-L2 {err:.2e}  {stats}")
     assert err <= 1e-4
+
+
+def test_multilayer_pool_at_its_last_layer():
+    """The 48-layer decode workload's pool: 48 GDN layers x 512 request slots x
+    32 value heads of 19 328-byte tiles (15.2 GB), 384 requests active in
+    random non-contiguous slots. One decode step of layer 47, whose tiles sit
+    past 14.9 GB into the pool, in the launch configuration the 48-layer
+    benchmark replays; the oracle runs the same step on a pool holding only
+    the active slots' tiles. Every output, every stored byte of the 384 active
+    slots of that layer, and the untouched rest of the layer (filled with a
+    canary) are compared."""
+    L, num_slots, B, HK, HV, d, k_hi = 48, 512, 384, 16, 32, 128, 16
+    layer = L - 1
+    seed = 48
+    _say(f"48-layer pool: layer {layer}, {B} of {num_slots} slots, {HV} heads, d={d}")
+    active = inputs.slot_order(seed, num_slots, B)
+    perm = inputs.random_perms(seed, HV, d)
+    ref = orc.Pool(orc.KIND_MIXED, d, d, k_hi, 1, B, HV)  # host slot i <-> pool slot active[i]
+    S = inputs.synthetic_states(seed, B, HV, d)
+    orc.pack(ref, 0, np.arange(B), S, perm)
+    del S
+    lay = D.damp_layout_init(d, d, k_hi)
+    need = D.damp_pool_required_bytes(lay, L, num_slots, HV)
+    assert need == 15_200_157_696
+    buf = torch.full((need,), 0xA5, dtype=torch.uint8, device="cuda")
+    gpool = D.Pool(lay, L, num_slots, HV, buffer=buf)
+    slot_bytes = HV * ref.tile_stride
+    rows = buf.view(L * num_slots, slot_bytes)
+    idx = torch.from_numpy(layer * num_slots + active.astype(np.int64)).cuda()
+    rows[idx] = torch.from_numpy(ref.buf.reshape(B, slot_bytes)).cuda()
+    inp = inputs.step(inputs.decode_inputs(seed, 1, B, HK, HV, d), 0)
+    di = dev_inputs(inp)
+    o = torch.empty((B, HV, d), dtype=torch.float32, device="cuda")
+    D.damp_state_update_gdn(gpool, layer, dev_i32(active), di["q"], di["k"], di["v"], di["g"],
+                            di["beta"], perm=dev_u8(perm), o=o)
+    torch.cuda.synchronize()
+    _say("  gpu step done; running the oracle")
+    o_ref = orc.update(ref, 0, np.arange(B), kda=False, perm=perm, **inp)
+    err = rel_l2(o.cpu().numpy(), o_ref)
+    stats = compare_tiles(rows[idx].cpu().numpy().reshape(-1), ref, "48-layer pool, layer 47")
+    _say(f"  o rel-L2 {err:.2e}  {stats}")
+    assert err <= O_TOL_MIXED and err <= 1e-4
+    # nothing else of layer 47, and nothing of its neighbouring layer, was written
+    keep = torch.ones(num_slots, dtype=torch.bool, device="cuda")
+    keep[torch.from_numpy(active.astype(np.int64)).cuda()] = False
+    lay47 = rows[layer * num_slots:(layer + 1) * num_slots]
+    assert bool((lay47[keep] == 0xA5).all())
+    assert bool((rows[(layer - 1) * num_slots:layer * num_slots] == 0xA5).all())
+    del buf, rows, lay47
+    torch.cuda.empty_cache()
