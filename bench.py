@@ -37,9 +37,33 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
-PROFILE = os.path.join(ROOT, "profiles", "update_gdn_mixed_b256_counters.txt")
+PROFILE = os.path.join(ROOT, "profiles", "update_gdn_mixed_b256.txt")
 KERNEL_SOURCES = ["paper_2608_27513_amd/csrc/update_stream.hip", "paper_2608_27513_amd/csrc/update.hpp",
                   "paper_2608_27513_amd/csrc/device.hpp"]
+# the sources each profiled kernel is built from (the hash in its summary)
+PROFILED_SOURCES = {
+    "update_stream128": KERNEL_SOURCES,
+    "update_fp32_128": ["paper_2608_27513_amd/csrc/update_fp32.hip", "paper_2608_27513_amd/csrc/update.hpp",
+                        "paper_2608_27513_amd/csrc/device.hpp"],
+    "prefill_blk128": ["paper_2608_27513_amd/csrc/prefill.hip", "paper_2608_27513_amd/csrc/device.hpp"],
+    "pack_unpack": ["paper_2608_27513_amd/csrc/pack.hip", "paper_2608_27513_amd/csrc/device.hpp"],
+    "copy_inplace_nt": ["paper_2608_27513_amd/bench_csrc/copy_ceiling.hip"],
+}
+
+
+# --only: one measurement of the full run (same set-up and timing), so that a
+# profiler run covers a single kernel on a single workload
+FP16_, U8_ = 2, 3
+ONLY = {
+    "gdn_mixed": ("gdn", 1, 16, None), "gdn_int8": ("gdn", 1, 0, None), "gdn_fp32": ("gdn", 0, 0, None),
+    "gdn_int8_h32": ("gdn", 1, 16, (FP16_, 32, FP16_, 1, U8_)),
+    "gdn_int8_g32": ("gdn", 1, 16, (FP16_, 32, FP16_, 0, U8_)),
+    "gdn_int4_h32": ("gdn", 1, 16, (FP16_, 32, FP16_, 1, 4)),
+    "gdn_int4_g32": ("gdn", 1, 16, (FP16_, 32, FP16_, 0, 4)),
+    "gdn_fp8": ("gdn", 1, 16, (FP16_, 32, 0, 0, 5)), "gdn_nvfp4": ("gdn", 1, 16, (FP16_, 16, 5, 0, 6)),
+    "kda_mixed": ("kda", 1, 16, None), "kda_fp32": ("kda", 0, 0, None),
+    "prefill_gdn": None, "prefill_kda": None, "pack_unpack": None, "copy": ("gdn", None, None, None),
+}
 
 
 def parse():
@@ -59,6 +83,8 @@ def parse():
                     help="only run a plain 1 GiB device copy (counter calibration)")
     ap.add_argument("--cpu-only", type=float, default=0.0, metavar="SECONDS",
                     help="only time the CPU oracle for SECONDS and print its JSON (no GPU)")
+    ap.add_argument("--only", choices=sorted(ONLY), default=None,
+                    help="run one measurement (for per-kernel profiles) and print its JSON")
     return ap.parse_args()
 
 
@@ -75,9 +101,9 @@ def copy_calibration(torch, reps: int = 5):
     print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "reps": reps}), flush=True)
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(paths=None) -> str:
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
+    for p in (KERNEL_SOURCES if paths is None else paths):
         h.update(open(os.path.join(ROOT, p), "rb").read())
     return h.hexdigest()[:16]
 
@@ -691,6 +717,29 @@ def cpu_single_thread(seconds: float, log=print):
     return res
 
 
+def run_only(args, torch, D, inputs, log):
+    name = args.only
+    spec = ONLY[name]
+    if name in ("prefill_gdn", "prefill_kda"):
+        res = prefill_bench(torch, D, inputs, args.steps, log=log, kda=name == "prefill_kda")
+    elif name == "pack_unpack":
+        res = pack_unpack_bench(torch, D, args.steps, log=log)
+    else:
+        kda = spec[0] == "kda"
+        wl = Workload(torch, D, inputs, kda=kda, B=256, HK=32 if kda else 16, HV=32, d=128,
+                      k_hi=16, rotations=args.rotations, seed=1 if kda else 0, log=log)
+        if name == "copy":
+            res = copy_ceiling(torch, D, wl, args.rotations, args.steps, log=log)
+        else:
+            _, kind, k_hi, tiers = spec
+            rot = args.rotations if kind == D.DAMP_STATE_MIXED else max(2, args.rotations // 2)
+            res = measure(torch, D, wl, kind, k_hi, rot, args.warmup, args.steps, torch.bfloat16,
+                          tiers=tiers)
+            log(f"  {name}: kernel {res['kernel_us']:.2f} us, {res['kernel_gbs']:.0f} GB/s "
+                f"({100 * res['kernel_frac_peak']:.1f}% of peak)")
+    print(json.dumps({"only": name, "steps": args.steps, "warmup": args.warmup, **res}), flush=True)
+
+
 def main():
     args = parse()
     if args.cpu_only > 0:  # child of cpu_single_thread: no GPU work
@@ -715,6 +764,9 @@ def main():
         return
     D.lib()
     B, HK, HV, d, k_hi = 256, 16, 32, 128, 16
+    if args.only is not None:
+        run_only(args, torch, D, inputs, log)
+        return
     log("setting up GDN B=256 HK=16 HV=32 d=128 K_hi=16")
     gdn = Workload(torch, D, inputs, kda=False, B=B, HK=HK, HV=HV, d=d, k_hi=k_hi,
                    rotations=args.rotations, seed=0, log=log)
