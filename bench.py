@@ -368,28 +368,29 @@ def copy_ceiling(torch, D, wl, rotations: int, steps: int, log=print):
     lib = ctypes.CDLL(B.BENCH_LIB)
     lib.copy_ceiling_inplace.restype = ctypes.c_int
     lib.copy_ceiling_inplace.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int,
-                                         ctypes.c_void_p]
+                                         ctypes.c_int, ctypes.c_void_p]
     pool, sets, layout = wl.make_pool(D.DAMP_STATE_MIXED, wl.k_hi, rotations)
     region = wl.B * wl.HV * pool.tile_stride  # one rotation's slots are contiguous
     base = pool.buffer.data_ptr()
     stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
     best = None
-    for grid in (512, 1024, 2048):
-        def call(r, grid=grid):
-            rc = lib.copy_ceiling_inplace(ctypes.c_void_p(base + r * region), region, grid, stream)
+    for grid, unroll in ((1024, 1), (512, 2), (768, 2), (256, 4)):  # about 4 MB in flight
+        def call(r, grid=grid, unroll=unroll):
+            rc = lib.copy_ceiling_inplace(ctypes.c_void_p(base + r * region), region, grid, unroll,
+                                          stream)
             if rc != 0:
                 raise RuntimeError(f"copy_ceiling_inplace returned {rc}")
         calls = [lambda r=r: call(r) for r in range(rotations)]
-        t = time_steps(torch, calls, 20, steps, prewarm_s=0.2)
+        t = time_steps(torch, calls, 20, steps, prewarm_s=0.1)
         if best is None or t["mean_launch_s"] < best[1]:
-            best = (grid, t["mean_launch_s"])
+            best = ((grid, unroll), t["mean_launch_s"])
     sec = best[1]
-    res = dict(bytes=2 * region, grid=best[0], copy_us=round(1e6 * sec, 2),
+    res = dict(bytes=2 * region, grid=best[0][0], unroll=best[0][1], copy_us=round(1e6 * sec, 2),
                copy_gbs=round(2 * region / sec / 1e9, 1),
                copy_frac_hbm_peak=round(2 * region / sec / 1e9 / HBM_PEAK_GBS, 4),
                kernel="in-place 16-byte non-temporal copy of the rotated pool regions")
     log(f"  in-place copy of the same state bytes: {res['copy_us']} us, {res['copy_gbs']} GB/s "
-        f"(grid {best[0]})")
+        f"(grid {best[0][0]}, {best[0][1]} per thread)")
     del pool
     torch.cuda.empty_cache()
     return res
