@@ -654,14 +654,18 @@ def accuracy_bench(torch, log=print):
     random, an E-only and the C = E P selector, in the default and the
     paper's INT8+H32 tiers, on the GDN and KDA decode workloads (B = 64, 512
     warm-up tokens, selection from a separate 2048-token calibration
-    sequence, 256 held-out decode steps). The paper's figures are context:
-    real model trajectories, INT8+H32 with 16 FP16 rows (App. E)."""
+    sequence, 256 held-out decode steps), with the benchmark's isotropic keys
+    and with keys whose energy concentrates in 8 channels per key head (x4
+    before normalization). The paper's figures are context: real model
+    trajectories, INT8+H32 with 16 FP16 rows (App. E)."""
     from paper_2608_27513_amd import accuracy as A
 
     out = {}
     t0 = time.time()
-    for name, kda in (("gdn", False), ("kda", True)):
-        out[name] = A.study(kda=kda, B=64, steps=256, seed=0, log=log)
+    for name, kda, kc in (("gdn", False, 0), ("kda", True, 0), ("gdn_key8x4", False, 8),
+                          ("kda_key8x4", True, 8)):
+        out[name] = A.study(kda=kda, B=64, steps=256, seed=0, key_channels=kc, key_factor=4.0,
+                            log=log)
         torch.cuda.empty_cache()
     out["seconds"] = round(time.time() - t0, 1)
     out["paper_context"] = {"gdn_common_16_16": {"state_rrmse": 8.748e-3, "output_rrmse": 2.256e-3},

@@ -42,7 +42,8 @@ def layout_for(d: int, k_hi: int, tier=None) -> D.damp_layout:
     return lay
 
 
-def warm_states(*, kda: bool, B: int, HK: int, HV: int, d: int, tokens: int, gen, mu=None):
+def warm_states(*, kda: bool, B: int, HK: int, HV: int, d: int, tokens: int, gen, mu=None,
+                key_scale=None):
     """FP32 states after `tokens` decode steps from zero, natural order
     [B, HV, d, d] (the library's FP32-state update)."""
     pool = D.Pool(D.damp_layout_init(d, d, 0, D.DAMP_STATE_FP32), 1, B, HV)
@@ -51,16 +52,17 @@ def warm_states(*, kda: bool, B: int, HK: int, HV: int, d: int, tokens: int, gen
     o = torch.empty((B, HV, d), dtype=torch.float32, device="cuda")
     fn = D.damp_state_update_kda if kda else D.damp_state_update_gdn
     for _ in range(tokens):
-        x = inputs.decode_inputs_device(gen, B, HK, HV, d, kda=kda, mu=mu)
+        x = inputs.decode_inputs_device(gen, B, HK, HV, d, kda=kda, mu=mu, key_scale=key_scale)
         fn(pool, 0, slots, x["q"], x["k"], x["v"], x["g"], x["beta"], o=o)
     return D.damp_state_unpack(pool, 0, slots)
 
 
 def calibrate(*, kda: bool, HK: int, HV: int, d: int, lo: D.damp_layout, tokens: int, gen,
-              mu=None, stride: int = 8) -> D.Calib:
+              mu=None, key_scale=None, stride: int = 8) -> D.Calib:
     """On-device calibration of one FP32 sequence from the zero state under
     the low tier of `lo` (App. A.2-A.3)."""
-    steps = [inputs.decode_inputs_device(gen, 1, HK, HV, d, kda=kda, mu=mu) for _ in range(tokens)]
+    steps = [inputs.decode_inputs_device(gen, 1, HK, HV, d, kda=kda, mu=mu, key_scale=key_scale)
+             for _ in range(tokens)]
     x = {n: torch.stack([s[n] for s in steps], dim=1).contiguous() for n in steps[0]}
     del steps
     pool = D.Pool(D.damp_layout_init(d, d, 0, D.DAMP_STATE_FP32), 1, 1, HV)
@@ -136,23 +138,30 @@ def trajectory_rrmse(*, kda: bool, HK: int, S0: torch.Tensor, variants: dict, st
 
 def study(*, kda: bool, B: int = 64, HK: int = None, HV: int = 32, d: int = 128, k_hi: int = 16,
           warm: int = 512, calib_tokens: int = 2048, steps: int = 256, seed: int = 0,
+          key_channels: int = 0, key_factor: float = 4.0,
           tiers=(("default", None), ("int8_h32", PAPER_TIER)), log=None) -> dict:
     """The held-out accuracy of uniform INT8 and of the random, E-only and
     DAMP selections, for each tier, on one decode workload (the synthetic
     distributions of the benchmark: GDN 16 key / 32 value heads with a
-    scalar decay, KDA 32 heads with per-channel decays)."""
+    scalar decay, KDA 32 heads with per-channel decays). key_channels > 0
+    draws keys whose energy concentrates in that many seeded channels per key
+    head (key_factor times the others before normalization), in warm-up,
+    calibration and held-out steps alike."""
     if HK is None:
         HK = HV if kda else HV // 2
     mu = torch.from_numpy(inputs.kda_mu(seed, HV, d)).cuda() if kda else None
+    ks = None
+    if key_channels > 0:
+        ks = torch.from_numpy(inputs.key_channel_scale(seed, HK, d, key_channels, key_factor)).cuda()
     g_warm = torch.Generator(device="cuda")
     g_warm.manual_seed(1000 + seed)
-    S0 = warm_states(kda=kda, B=B, HK=HK, HV=HV, d=d, tokens=warm, gen=g_warm, mu=mu)
+    S0 = warm_states(kda=kda, B=B, HK=HK, HV=HV, d=d, tokens=warm, gen=g_warm, mu=mu, key_scale=ks)
     variants = {}
     for tname, tier in tiers:
         g_cal = torch.Generator(device="cuda")
         g_cal.manual_seed(2000 + seed)
         cal = calibrate(kda=kda, HK=HK, HV=HV, d=d, lo=layout_for(d, 0, tier),
-                        tokens=calib_tokens, gen=g_cal, mu=mu)
+                        tokens=calib_tokens, gen=g_cal, mu=mu, key_scale=ks)
         sel = selections(cal, k_hi, seed)
         variants[f"{tname}/uniform_int8"] = (layout_for(d, 0, tier), None)
         for sname, perm in sel.items():
@@ -163,14 +172,16 @@ def study(*, kda: bool, B: int = 64, HK: int = None, HV: int = 32, d: int = 128,
 
     def held_out():
         for _ in range(steps):
-            yield inputs.decode_inputs_device(g_run, B, HK, HV, d, kda=kda, mu=mu)
+            yield inputs.decode_inputs_device(g_run, B, HK, HV, d, kda=kda, mu=mu, key_scale=ks)
 
     res = trajectory_rrmse(kda=kda, HK=HK, S0=S0, variants=variants, step_inputs=held_out())
     res["config"] = dict(model="KDA" if kda else "GDN", B=B, HK=HK, HV=HV, d=d, k_hi=k_hi,
-                         warm_tokens=warm, calib_tokens=calib_tokens, held_out_steps=steps)
+                         warm_tokens=warm, calib_tokens=calib_tokens, held_out_steps=steps,
+                         key_channels=key_channels, key_factor=key_factor if key_channels else None)
     if log:
+        tag = res["config"]["model"] + (f" ({key_channels} key channels x{key_factor})" if key_channels else "")
         for name, r in res.items():
             if isinstance(r, dict) and "state_rrmse" in r:
-                log(f"  {res['config']['model']} {name}: state RRMSE {r['state_rrmse']:.3e}, "
+                log(f"  {tag} {name}: state RRMSE {r['state_rrmse']:.3e}, "
                     f"output RRMSE {r['output_rrmse']:.3e}")
     return res

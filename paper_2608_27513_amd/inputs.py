@@ -122,17 +122,31 @@ def synthetic_states(seed: int, B: int, HV: int, d: int, rank: int = 16) -> np.n
     return S.reshape(B, HV, d, d).astype(f)
 
 
+def key_channel_scale(seed: int, hk: int, d: int, n: int = 8, factor: float = 4.0) -> np.ndarray:
+    """fp32 [hk, d]: 1 everywhere except n seeded channels per key head, which
+    get `factor` (an anisotropic key distribution whose energy concentrates
+    in a few key channels, applied before the L2 normalization)."""
+    s = np.ones((hk, d), np.float32)
+    ch = outlier_channels(seed, hk, d, n)
+    for h in range(hk):
+        s[h, ch[h]] = np.float32(factor)
+    return s
+
+
 def decode_inputs_device(gen, B: int, HK: int, HV: int, d: int, *, kda: bool = False,
-                         mu=None, device="cuda") -> dict:
+                         mu=None, key_scale=None, device="cuda") -> dict:
     """One decode step of the same distributions drawn on the GPU with a seeded
     torch.Generator (used for long warm-up and calibration runs, where moving
-    host arrays would dominate). Returns bf16 device tensors
+    host arrays would dominate). key_scale (device fp32 [HK, d], optional)
+    multiplies k before its normalization. Returns bf16 device tensors
     q, k [B, HK, d]; v [B, HV, d]; g [B, HV] or [B, HV, d]; beta [B, HV]."""
     import torch
 
     f = torch.float32
     q = torch.randn((B, HK, d), generator=gen, device=device, dtype=f)
     k = torch.randn((B, HK, d), generator=gen, device=device, dtype=f)
+    if key_scale is not None:
+        k = k * key_scale
     q = q / q.norm(dim=-1, keepdim=True).clamp_min(1e-12)
     k = k / k.norm(dim=-1, keepdim=True).clamp_min(1e-12)
     v = torch.randn((B, HV, d), generator=gen, device=device, dtype=f)
