@@ -91,6 +91,16 @@ __device__ __forceinline__ float fold8(float a, float b, bool upper) {
                                                         true));
 }
 
+// One butterfly stage between lanes L and L ^ 16: v_permlane16_swap of x
+// with itself leaves (own, partner) on even 16-lane rows and (partner, own)
+// on odd ones, so the lower lane keeps own + partner and the upper lane
+// (`upper`, odd row) partner - own.
+__device__ __forceinline__ float swap16_butterfly(float x, bool upper) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return fmaf(__uint_as_float(r[1]), upper ? -1.0f : 1.0f, __uint_as_float(r[0]));
+}
+
 // Largest of a non-negative value over the 64 lanes of a wave, returned to
 // every lane: butterflies within rows of 16 lanes, then row broadcasts (the
 // lanes they do not write keep 0, the identity for non-negative values).
@@ -204,7 +214,8 @@ struct OpsRegs {
 // transformed domain: H is symmetric and orthonormal, so a low row is used as
 // stored (s (c - z) of the transformed values) and only the FP16 rows are
 // transformed, on load and before the store; v is transformed on staging and
-// o transformed back before it is written. Eq. (1) commutes with the
+// o transformed back before it is written, both in registers (DPP and row
+// swaps between the lanes of a group). Eq. (1) commutes with the
 // transform: S H = Lambda S_prev H + beta k (H delta)^T, delta_H = H v - (S_bar
 // H)^T k, o = H (S H)^T q.
 //
@@ -303,10 +314,11 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
   const int rgw = lane >> 3;  // row group within the wave
   // Two waves stage the operands, one tile row per thread, and one wave writes
   // o. With the paper's tiers the waves holding the 16-bit rows (0 and 1 for
-  // k_hi = 16) also transform them, so waves 2 and 3 stage and wave 1 writes:
-  // measured, 2.7% (GDN) and 5.7% (KDA) faster than waves 0, 1 and 3.
+  // k_hi = 16) also transform them, so waves 2 and 3 stage and wave 2 writes
+  // (with o transformed in registers: 0.1 us (GDN) and 0.6 us (KDA) faster
+  // than wave 1, 1.3 us faster than wave 3 on KDA).
   constexpr int kOpsT = kF16 ? 128 : 0;  // first thread of the operand waves
-  constexpr int kOutWave = kF16 ? 1 : 3;
+  constexpr int kOutWave = kF16 ? 2 : 3;
   const int tr = t - kOpsT;            // tile row of an operand thread
   const bool ops_thread = tr >= 0 && tr < D;
   const int my_u =
@@ -349,11 +361,14 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
       opr[buf][tr] = make_float4(kf, qf, KDA ? __expf(gf) : 1.0f, 0.0f);
       float vf = bf16_to_f32(static_cast<uint16_t>(r.v));
       if (had) {  // v in the transformed domain: 32 consecutive lanes hold a group
-#pragma unroll
-        for (int m = 1; m < 32; m <<= 1) {
-          const float o_ = __shfl_xor(vf, m, 64);
-          vf = (tr & m) ? o_ - vf : vf + o_;
-        }
+        // one butterfly per lane bit: the partner through DPP (lane ^ 1,
+        // ^ 2, ^ 4 as two mirrors, ^ 8) or the row swap (^ 16); the lane
+        // with the bit set keeps partner - own, the other own + partner
+        vf = fmaf(vf, (tr & 1) ? -1.0f : 1.0f, dpp_mov<0xb1>(vf));
+        vf = fmaf(vf, (tr & 2) ? -1.0f : 1.0f, dpp_mov<0x4e>(vf));
+        vf = fmaf(vf, (tr & 4) ? -1.0f : 1.0f, dpp_mov<0x1b>(dpp_mov<0x141>(vf)));
+        vf = fmaf(vf, (tr & 8) ? -1.0f : 1.0f, dpp_mov<0x128>(vf));
+        vf = swap16_butterfly(vf, (tr & 16) != 0);
         vf *= kInvSqrt32;
       }
       vsh[buf][tr] = vf;
@@ -615,13 +630,32 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
     // wave: one swap gives its q lanes the delta of their 4 columns
     if (wave == kOutWave) {
       const float bqk = beta * (opsc[buf][2] + opsc[buf][3]);
+      const float osc = had ? p.scale * kInvSqrt32 : p.scale;
       float ov[4];
 #pragma unroll
       for (int m = 0; m < 4; ++m) {
         const float val = b5 ? tot[m] : dd[m];
         const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(val),
                                                         __float_as_uint(val), false, false);
-        ov[m] = live ? p.scale * fmaf(bqk, __uint_as_float(r[0]), __uint_as_float(r[1])) : 0.0f;
+        ov[m] = live ? osc * fmaf(bqk, __uint_as_float(r[0]), __uint_as_float(r[1])) : 0.0f;
+      }
+      if (had) {
+        // back from the transformed domain. Of a group's 32 columns a q lane
+        // holds 4: column bits 0 and 3 are its own (m & 1, m >> 1), bits 4,
+        // 1 and 2 are lane bits 0, 3 and 4 (the k lanes, lane bit 5 clear,
+        // take part but are not used)
+        float t0 = ov[0] + ov[1], t1 = ov[0] - ov[1], t2 = ov[2] + ov[3], t3 = ov[2] - ov[3];
+        ov[0] = t0 + t2;
+        ov[2] = t0 - t2;
+        ov[1] = t1 + t3;
+        ov[3] = t1 - t3;
+        const float s0 = (lane & 1) ? -1.0f : 1.0f, s3 = b3 ? -1.0f : 1.0f;
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+          ov[m] = fmaf(ov[m], s0, dpp_mov<0xb1>(ov[m]));
+          ov[m] = fmaf(ov[m], s3, dpp_mov<0x128>(ov[m]));
+          ov[m] = swap16_butterfly(ov[m], b4);
+        }
       }
       uint8_t* obase = static_cast<uint8_t*>(p.o) +
                        (static_cast<size_t>(b) * HV + h) * D * o_esize;
@@ -633,21 +667,6 @@ __global__ __launch_bounds__(256, DEPTH == 1 ? 3 : 2) void update_stream128(
           *reinterpret_cast<float2*>(&osh[c_pair + 8]) = make_float2(ov[2], ov[3]);
         }
         wave_sync();
-        if (had) {
-          // back from the transformed domain: columns lane and lane + 64,
-          // each group of 32 in 32 consecutive lanes
-          float o0 = osh[lane], o1 = osh[lane + 64];
-#pragma unroll
-          for (int m = 1; m < 32; m <<= 1) {
-            const float a_ = __shfl_xor(o0, m, 64), c_ = __shfl_xor(o1, m, 64);
-            o0 = (lane & m) ? a_ - o0 : o0 + a_;
-            o1 = (lane & m) ? c_ - o1 : o1 + c_;
-          }
-          wave_sync();
-          osh[lane] = o0 * kInvSqrt32;
-          osh[lane + 64] = o1 * kInvSqrt32;
-          wave_sync();
-        }
         // one store writes the whole row: 16 lanes x 16 bytes (bf16) or 32
         // lanes x 16 bytes (fp32); the other lanes' offsets lie past the
         // buffer and are dropped
