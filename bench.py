@@ -56,6 +56,7 @@ PROFILED_SOURCES = {
 FP16_, U8_ = 2, 3
 ONLY = {
     "gdn_mixed": ("gdn", 1, 16, None), "gdn_int8": ("gdn", 1, 0, None), "gdn_fp32": ("gdn", 0, 0, None),
+    "gdn_mixed_scattered": ("gdn", 1, 16, None),  # the headline batch at random slots of the pool
     "gdn_int8_h32": ("gdn", 1, 16, (FP16_, 32, FP16_, 1, U8_)),
     "gdn_int8_g32": ("gdn", 1, 16, (FP16_, 32, FP16_, 0, U8_)),
     "gdn_int4_h32": ("gdn", 1, 16, (FP16_, 32, FP16_, 1, 4)),
@@ -739,7 +740,7 @@ def run_only(args, torch, D, inputs, log):
             _, kind, k_hi, tiers = spec
             rot = args.rotations if kind == D.DAMP_STATE_MIXED else max(2, args.rotations // 2)
             res = measure(torch, D, wl, kind, k_hi, rot, args.warmup, args.steps, torch.bfloat16,
-                          tiers=tiers)
+                          tiers=tiers, scattered=name.endswith("_scattered"))
             log(f"  {name}: kernel {res['kernel_us']:.2f} us, {res['kernel_gbs']:.0f} GB/s "
                 f"({100 * res['kernel_frac_peak']:.1f}% of peak)")
     print(json.dumps({"only": name, "steps": args.steps, "warmup": args.warmup, **res}), flush=True)
