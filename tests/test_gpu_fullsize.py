@@ -62,6 +62,39 @@ def test_full_size_step(kda):
     assert err <= O_TOL_MIXED and err <= 1e-4
 
 
+@pytest.mark.parametrize("kda,B,HK,HV", [(False, 256, 2, 4), (True, 256, 4, 4), (False, 32, 16, 32),
+                                         (False, 16, 16, 32), (True, 64, 32, 32), (True, 1, 32, 32)])
+def test_small_batch_launch_shapes(kda, B, HK, HV):
+    """The small-batch launches the benchmark times: one GPU's share of an
+    8-way tensor-parallel step (B = 256 with 4 value heads: 1024 tiles, two
+    per workgroup), B = 32 (two per workgroup), B = 16, B = 64 (three rounds)
+    and B = 1, at scattered slots of a larger pool; every output and every
+    stored byte against the oracle."""
+    d, k_hi = 128, 16
+    seed = 60 + B + HV + kda
+    num_slots = B + 37
+    _say(f"small batch: kda={kda} B={B} HK={HK} HV={HV}")
+    S = inputs.synthetic_states(seed, num_slots, HV, d)
+    mu = inputs.kda_mu(seed, HV, d) if kda else None
+    perm = inputs.random_perms(seed, HV, d)
+    slots = inputs.slot_order(seed, num_slots, B)
+    ref = orc.Pool(orc.KIND_MIXED, d, d, k_hi, 1, num_slots, HV)
+    orc.pack(ref, 0, np.arange(num_slots, dtype=np.int32), S, perm)
+    gpool = gpu_pool_from(ref, D)
+    inp = inputs.step(inputs.decode_inputs(seed, 1, B, HK, HV, d, kda=kda, mu=mu), 0)
+    di = dev_inputs(inp)
+    o = torch.empty((B, HV, d), dtype=torch.float32, device="cuda")
+    fn = D.damp_state_update_kda if kda else D.damp_state_update_gdn
+    fn(gpool, 0, dev_i32(slots), di["q"], di["k"], di["v"], di["g"], di["beta"],
+       perm=dev_u8(perm), o=o)
+    torch.cuda.synchronize()
+    o_ref = orc.update(ref, 0, slots, kda=kda, perm=perm, **inp)
+    err = rel_l2(o.cpu().numpy(), o_ref)
+    stats = compare_tiles(gpool.buffer.cpu().numpy(), ref, "small batch")
+    _say(f"  o rel-L2 {err:.2e}  {stats}")
+    assert err <= O_TOL_MIXED and err <= 1e-4
+
+
 def test_largest_batch_and_empty_batch():
     B, HV, d, k_hi = 65535, 1, 16, 4
     _say(f"max batch: B={B} HV={HV} d={d}")
