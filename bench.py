@@ -48,6 +48,7 @@ PROFILED_SOURCES = {
     "prefill_blk128": ["paper_2608_27513_amd/csrc/prefill.hip", "paper_2608_27513_amd/csrc/device.hpp"],
     "pack_unpack": ["paper_2608_27513_amd/csrc/pack.hip", "paper_2608_27513_amd/csrc/device.hpp"],
     "copy_inplace_nt": ["paper_2608_27513_amd/bench_csrc/copy_ceiling.hip"],
+    "copy_tiles_nt": ["paper_2608_27513_amd/bench_csrc/copy_ceiling.hip"],
 }
 
 
@@ -64,6 +65,7 @@ ONLY = {
     "gdn_fp8": ("gdn", 1, 16, (FP16_, 32, 0, 0, 5)), "gdn_nvfp4": ("gdn", 1, 16, (FP16_, 16, 5, 0, 6)),
     "kda_mixed": ("kda", 1, 16, None), "kda_fp32": ("kda", 0, 0, None),
     "prefill_gdn": None, "prefill_kda": None, "pack_unpack": None, "copy": ("gdn", None, None, None),
+    "copy_tiles": ("gdn", None, None, None), "copy_tiles_scattered": ("gdn", None, None, None),
 }
 
 
@@ -355,13 +357,16 @@ def sweep(torch, D, inputs, steps: int, log=print):
     return out
 
 
-def copy_ceiling(torch, D, wl, rotations: int, steps: int, log=print):
+def copy_ceiling(torch, D, wl, rotations: int, steps: int, log=print, linear: bool = True,
+                 walks=("consecutive", "scattered")):
     """The practical ceiling of the update's state traffic: an in-place copy
     (every 16-byte piece read and written back, non-temporal, like the
     update's tile accesses; `libcopyceiling.so`, built beside libdamp) over
     the same rotated pool regions the headline updates, timed like the update
     (steady clock, HIP events around `steps` launches); the fastest of a few
-    grid sizes."""
+    grid sizes. Then the tile-walk copies (`walks`): the tiles of each step
+    copied in place in the update's own order and launch shape, at the
+    batch's consecutive slots and at slots scattered over the pool."""
     import ctypes
 
     from paper_2608_27513_amd import build as B
@@ -375,7 +380,7 @@ def copy_ceiling(torch, D, wl, rotations: int, steps: int, log=print):
     base = pool.buffer.data_ptr()
     stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
     best = None
-    for grid, unroll in ((1024, 1), (512, 2), (768, 2), (256, 4)):  # about 4 MB in flight
+    for grid, unroll in ((1024, 1), (512, 2), (768, 2), (256, 4)) if linear else ():  # ~4 MB in flight
         def call(r, grid=grid, unroll=unroll):
             rc = lib.copy_ceiling_inplace(ctypes.c_void_p(base + r * region), region, grid, unroll,
                                           stream)
@@ -385,13 +390,42 @@ def copy_ceiling(torch, D, wl, rotations: int, steps: int, log=print):
         t = time_steps(torch, calls, 20, steps, prewarm_s=0.1)
         if best is None or t["mean_launch_s"] < best[1]:
             best = ((grid, unroll), t["mean_launch_s"])
-    sec = best[1]
-    res = dict(bytes=2 * region, grid=best[0][0], unroll=best[0][1], copy_us=round(1e6 * sec, 2),
-               copy_gbs=round(2 * region / sec / 1e9, 1),
-               copy_frac_hbm_peak=round(2 * region / sec / 1e9 / HBM_PEAK_GBS, 4),
-               kernel="in-place 16-byte non-temporal copy of the rotated pool regions")
-    log(f"  in-place copy of the same state bytes: {res['copy_us']} us, {res['copy_gbs']} GB/s "
-        f"(grid {best[0][0]}, {best[0][1]} per thread)")
+    res = dict(bytes=2 * region)
+    if linear:
+        sec = best[1]
+        res.update(grid=best[0][0], unroll=best[0][1], copy_us=round(1e6 * sec, 2),
+                   copy_gbs=round(2 * region / sec / 1e9, 1),
+                   copy_frac_hbm_peak=round(2 * region / sec / 1e9 / HBM_PEAK_GBS, 4),
+                   kernel="in-place 16-byte non-temporal copy of the rotated pool regions")
+        log(f"  in-place copy of the same state bytes: {res['copy_us']} us, {res['copy_gbs']} GB/s "
+            f"(grid {best[0][0]}, {best[0][1]} per thread)")
+    # the same tiles copied in the update's own walk and launch shape, with the
+    # batch at consecutive slots and at slots scattered over the whole pool
+    lib.copy_tiles_inplace.restype = ctypes.c_int
+    lib.copy_tiles_inplace.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
+                                       ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int, ctypes.c_int,
+                                       ctypes.c_int, ctypes.c_void_p]
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    per_head = max(1, min((3 * cus) // wl.HV, wl.B))  # the update's three workgroups per CU
+    tb = D.damp_tile_bytes(layout)
+    n = wl.B * rotations
+    order = torch.from_numpy(wl.inputs.slot_order(7, n, n)).cuda()
+    all_walks = {"consecutive": sets, "scattered": [order[r * wl.B:(r + 1) * wl.B].contiguous()
+                                                    for r in range(rotations)]}
+    walks = {k: all_walks[k] for k in walks}
+    res["tile_walk"] = dict(grid=per_head * wl.HV, tile_bytes=tb,
+                            kernel="in-place copy of each step's tiles in the update's order")
+    for name, slot_sets in walks.items():
+        def tcall(sl):
+            rc = lib.copy_tiles_inplace(ctypes.c_void_p(base), ctypes.c_void_p(sl.data_ptr()), wl.B,
+                                        wl.HV, wl.HV * pool.tile_stride, pool.tile_stride, tb, n,
+                                        per_head * wl.HV, stream)
+            if rc != 0:
+                raise RuntimeError(f"copy_tiles_inplace returned {rc}")
+        calls = [lambda sl=sl: tcall(sl) for sl in slot_sets]
+        t = time_steps(torch, calls, 20, steps, prewarm_s=0.1)
+        res["tile_walk"][f"{name}_us"] = round(1e6 * t["mean_launch_s"], 2)
+        log(f"  tile-walk copy, {name} slots: {res['tile_walk'][f'{name}_us']} us")
     del pool
     torch.cuda.empty_cache()
     return res
@@ -735,7 +769,10 @@ def run_only(args, torch, D, inputs, log):
         wl = Workload(torch, D, inputs, kda=kda, B=256, HK=32 if kda else 16, HV=32, d=128,
                       k_hi=16, rotations=args.rotations, seed=1 if kda else 0, log=log)
         if name == "copy":
-            res = copy_ceiling(torch, D, wl, args.rotations, args.steps, log=log)
+            res = copy_ceiling(torch, D, wl, args.rotations, args.steps, log=log, walks=())
+        elif name.startswith("copy_tiles"):
+            res = copy_ceiling(torch, D, wl, args.rotations, args.steps, log=log, linear=False,
+                               walks=("scattered",) if name.endswith("_scattered") else ("consecutive",))
         else:
             _, kind, k_hi, tiers = spec
             rot = args.rotations if kind == D.DAMP_STATE_MIXED else max(2, args.rotations // 2)
@@ -789,6 +826,9 @@ def main():
                        args.steps, torch.bfloat16, scattered=True)
         log(f"  mixed, slots scattered over the pool: kernel {scat['kernel_us']:.1f} us, "
             f"{scat['kernel_gbs']:.0f} GB/s")
+        scat["frac_of_tile_walk_copy"] = round(cop["tile_walk"]["scattered_us"] / scat["kernel_us"], 4)
+        cop["update_frac_of_tile_walk_copy"] = round(cop["tile_walk"]["consecutive_us"] /
+                                                     head["kernel_us"], 4)
         extra["headline_random_slots"] = scat
         rot_fp = max(2, args.rotations // 2)
         fp = measure(torch, D, gdn, D.DAMP_STATE_FP32, 0, rot_fp, args.warmup, args.steps,
