@@ -55,18 +55,24 @@ __global__ __launch_bounds__(Shape<D>::NT) void pack_kernel(const TileParams p) 
     s_g = nvfp4_global(block_max<Sh::NT>(amax));
     if (t == 0) store_global_scale<D>(meta, k_hi, s_g);
   }
+  // every row slice of the thread is loaded before the first store: the
+  // compiler cannot move a load of the state above a store into the tile
+  // (the pointers may alias), so loading slot by slot would wait for the
+  // memory once per slot
+  float x[Sh::RPT][Sh::CPT];
 #pragma unroll
   for (int i = 0; i < Sh::RPT; ++i) {
     const int r = rg + Sh::RG * i;
     const int u = p.perm ? (static_cast<int>(p.perm[static_cast<size_t>(h) * D + r]) & (D - 1)) : r;
-    float x[Sh::CPT];
     uint32_t w[Sh::CPT];
     load_words<Sh::CPT * 4>(reinterpret_cast<const uint8_t*>(src + static_cast<size_t>(u) * D + col0), w);
 #pragma unroll
-    for (int j = 0; j < Sh::CPT; ++j) x[j] = __uint_as_float(w[j]);
-    encode_row<KIND, D, Sh::CPT, Sh::TPR>(x, r, k_hi, cg, col0, tile, codes, meta, p.had != 0,
-                                          s_g);
+    for (int j = 0; j < Sh::CPT; ++j) x[i][j] = __uint_as_float(w[j]);
   }
+#pragma unroll
+  for (int i = 0; i < Sh::RPT; ++i)
+    encode_row<KIND, D, Sh::CPT, Sh::TPR>(x[i], rg + Sh::RG * i, k_hi, cg, col0, tile, codes, meta,
+                                          p.had != 0, s_g);
 }
 
 template <int KIND, int D>
