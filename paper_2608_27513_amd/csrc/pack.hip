@@ -92,6 +92,29 @@ __global__ __launch_bounds__(Shape<D>::NT) void unpack_kernel(const TileParams p
   const uint8_t* meta_bytes = codes + static_cast<size_t>(D - k_hi) * code_row_bytes<KIND, D>();
   const float2* meta = reinterpret_cast<const float2*>(meta_bytes);
   const uint32_t* meta16 = reinterpret_cast<const uint32_t*>(meta_bytes);
+  // FP32 state and the default tiers: the bytes of every row slice are
+  // loaded before the first store (the tile and the state may alias as far
+  // as the compiler knows, so it would not move a later slot's loads above
+  // an earlier slot's stores)
+  constexpr bool kPre = KIND == kFp32 || KIND == kMixed;
+  uint32_t pre[kPre ? Sh::RPT : 1][kPre ? Sh::CPT : 1];
+  float2 presz[kPre ? Sh::RPT : 1];
+  if constexpr (kPre) {
+    if (live) {
+#pragma unroll
+      for (int i = 0; i < Sh::RPT; ++i) {
+        const int r = rg + Sh::RG * i;
+        if (KIND == kFp32) {
+          load_words<Sh::CPT * 4>(tile + (static_cast<size_t>(r) * D + col0) * 4, pre[i]);
+        } else if (r < k_hi) {
+          load_words<Sh::CPT * 2>(tile + (static_cast<size_t>(r) * D + col0) * 2, pre[i]);
+        } else {
+          load_words<Sh::CPT>(codes + static_cast<size_t>(r - k_hi) * D + col0, pre[i]);
+          presz[i] = meta[r - k_hi];
+        }
+      }
+    }
+  }
 #pragma unroll
   for (int i = 0; i < Sh::RPT; ++i) {
     const int r = rg + Sh::RG * i;
@@ -162,19 +185,18 @@ __global__ __launch_bounds__(Shape<D>::NT) void unpack_kernel(const TileParams p
 #pragma unroll
       for (int j = 0; j < Sh::CPT; ++j) out[j] = 0u;
     } else if (KIND == kFp32) {
-      load_words<Sh::CPT * 4>(tile + (static_cast<size_t>(r) * D + col0) * 4, out);
+#pragma unroll
+      for (int j = 0; j < Sh::CPT; ++j) out[j] = pre[i][j];
     } else if (r < k_hi) {
-      uint32_t w[Sh::CPT / 2];
-      load_words<Sh::CPT * 2>(tile + (static_cast<size_t>(r) * D + col0) * 2, w);
+      const uint32_t(&w)[Sh::CPT] = pre[i];
 #pragma unroll
       for (int j = 0; j < Sh::CPT / 2; ++j) {
         out[2 * j] = w[j] << 16;
         out[2 * j + 1] = w[j] & 0xffff0000u;
       }
     } else {
-      uint32_t w[Sh::CPT / 4];
-      load_words<Sh::CPT>(codes + static_cast<size_t>(r - k_hi) * D + col0, w);
-      const float2 sz = meta[r - k_hi];
+      const uint32_t(&w)[Sh::CPT] = pre[i];
+      const float2 sz = presz[i];
       // x_hat = s * (c - z), exactly as Eq. (3) reconstructs
 #pragma unroll
       for (int j = 0; j < Sh::CPT / 4; ++j) {
