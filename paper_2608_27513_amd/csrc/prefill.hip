@@ -339,6 +339,12 @@ __global__ __launch_bounds__(256) void prefill_blk128(const PrefillParams p) {
   // ---- operand staging: thread t handles tile row (and column) r of the
   // tokens 2 i + (wave >> 1) of a block, i < 4
   const int r = 64 * (wave & 1) + lane;
+  // The per-row operands (k~, q~, a~ and KDA's block products) sit at
+  // position ((r / 4) % 4) 32 + (r / 16) 4 + r % 4 of their 128 floats: a
+  // lane of row block rb reads the float4 of rows 16 rb + 4 j .. + 3 at
+  // index 8 j + rb, so for each j the eight row blocks of a wave read 128
+  // consecutive bytes (one bank each) instead of eight float4 64 bytes apart.
+  const int rsw = ((r >> 2) & 3) * 32 + (r >> 4) * 4 + (r & 3);
   const int u2 = 2 * (p.perm ? (static_cast<int>(p.perm[static_cast<size_t>(h) * D + r]) & (D - 1))
                              : r);
   const int half = wave >> 1;
@@ -378,11 +384,11 @@ __global__ __launch_bounds__(256) void prefill_blk128(const PrefillParams p) {
       if (TB * blk + tb < T) {
         const float kf = bf16_to_f32(static_cast<uint16_t>(o.k[i]));
         const float qf = bf16_to_f32(static_cast<uint16_t>(o.q[i]));
-        reinterpret_cast<float*>(B_.k[tb])[r] = kf;
-        reinterpret_cast<float*>(B_.q[tb])[r] = qf;
+        reinterpret_cast<float*>(B_.k[tb])[rsw] = kf;
+        reinterpret_cast<float*>(B_.q[tb])[rsw] = qf;
         reinterpret_cast<float*>(B_.v[tb])[r] = bf16_to_f32(static_cast<uint16_t>(o.v[i]));
         if (KDA)
-          reinterpret_cast<float*>(B_.a[KDA ? tb : 0])[r] =
+          reinterpret_cast<float*>(B_.a[KDA ? tb : 0])[rsw] =
               __expf(bf16_to_f32(static_cast<uint16_t>(o.g[i])));
         const float kq = wave_sum_dpp(kf * qf);
         float* sc = reinterpret_cast<float*>(&B_.sc[tb]);
@@ -454,7 +460,7 @@ __global__ __launch_bounds__(256) void prefill_blk128(const PrefillParams p) {
       float kr[16];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const float4 k4 = B_.k[tb][4 * rb + j];
+        const float4 k4 = B_.k[tb][8 * j + rb];
         kr[4 * j] = k4.x;
         kr[4 * j + 1] = k4.y;
         kr[4 * j + 2] = k4.z;
@@ -463,7 +469,7 @@ __global__ __launch_bounds__(256) void prefill_blk128(const PrefillParams p) {
       if (KDA && slow_cur) {  // the decay of each row, per token
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const float4 a4 = B_.a[KDA ? tb : 0][4 * rb + j];
+          const float4 a4 = B_.a[KDA ? tb : 0][8 * j + rb];
           const float aj[4] = {a4.x, a4.y, a4.z, a4.w};
 #pragma unroll
           for (int m = 0; m < 4; ++m)
@@ -481,7 +487,7 @@ __global__ __launch_bounds__(256) void prefill_blk128(const PrefillParams p) {
         for (int c = 0; c < 4; ++c) w[c] = fmaf(kr[i], x[i][c], w[c]);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const float4 q4 = B_.q[tb][4 * rb + j];
+        const float4 q4 = B_.q[tb][8 * j + rb];
         const float qj[4] = {q4.x, q4.y, q4.z, q4.w};
 #pragma unroll
         for (int m = 0; m < 4; ++m)
@@ -536,7 +542,7 @@ __global__ __launch_bounds__(256) void prefill_blk128(const PrefillParams p) {
       if (KDA && !slow_cur) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const float4 b4 = B_.a[KDA ? tb : 0][4 * rb + j];
+          const float4 b4 = B_.a[KDA ? tb : 0][8 * j + rb];
           kr[4 * j] = b4.x;
           kr[4 * j + 1] = b4.y;
           kr[4 * j + 2] = b4.z;
@@ -562,7 +568,7 @@ __global__ __launch_bounds__(256) void prefill_blk128(const PrefillParams p) {
     if (KDA && !slow_cur) {  // S = G P at the end of the block
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const float4 g4 = B_.ge[KDA ? 4 * rb + j : 0];
+        const float4 g4 = B_.ge[KDA ? 8 * j + rb : 0];
         const float gj[4] = {g4.x, g4.y, g4.z, g4.w};
 #pragma unroll
         for (int m = 0; m < 4; ++m)
